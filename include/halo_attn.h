@@ -1,0 +1,204 @@
+/*
+ * halo_attn.h -- C ABI of the shared-prefix paged-attention library (gfx950).
+ *
+ * The operation. A batch of requests (replicated agentic workflows, arXiv
+ * 2509.02121 §1) shares prompt prefixes and differs in per-request suffixes
+ * (§2, "Context reuse" and intra-batch prefix sharing). Their KV cache is paged
+ * (§7, PagedAttention) and the sharing is a prefix forest (§7, RadixAttention):
+ * segments of tokens, and for every request an ordered root-to-leaf path of
+ * segment ids. Each query attends over the concatenation of its path's
+ * segments with ordinary scaled dot-product attention; the result must be
+ * exactly that of unshared execution (§3 "Scope", semantic preserving), up to
+ * floating-point summation order. Chunked prefill of new tokens over a cached
+ * prefix is the prefix-caching case of §4.1.
+ *
+ *   s_j  = sm_scale * <q, k_j>            for every visible key j
+ *   o    = sum_j softmax(s)_j v_j,   lse = ln sum_j exp(s_j)
+ *   q head h reads kv head h / (num_q_heads / num_kv_heads).
+ *
+ * Memory layouts (all row-major, element type = kv_dtype unless stated):
+ *   k_pool  [num_pool_pages][num_kv_heads][page_size][head_dim]   token-major
+ *   v_pool  [num_pool_pages][num_kv_heads][head_dim][page_size]   dim-major
+ *   q, o    decode:  [num_requests][num_q_heads][head_dim]
+ *           prefill: [sum q_len][num_q_heads][head_dim], request r's rows
+ *                    follow request r-1's. o has element type out_dtype.
+ *   lse     [rows][num_q_heads] float32, natural log; -inf for a row that
+ *           sees no key (its o row is 0).
+ * A segment of length L occupies ceil(L / page_size) pages; token t sits in
+ * page seg_page_ids[seg_page_indptr[s] + t / page_size], slot t % page_size.
+ * Slots past L in the last page, and pages no segment lists, may hold any
+ * bits (NaN included) and never affect the results.
+ *
+ * Ownership. Every device buffer belongs to the caller (torch tensors in the
+ * Python binding). Run calls allocate nothing and enqueue work on the
+ * caller's HIP stream (passed as void*, a hipStream_t); HALO_OK means
+ * "validated and enqueued". A plan is host memory owned by the library from
+ * halo_plan_create until halo_plan_destroy; it is immutable, so several
+ * streams may run one plan concurrently if each has its own workspace.
+ *
+ * Errors. Every call returns a halo_status_t; halo_last_error_message()
+ * gives a thread-local description of the last failure. Structural checks
+ * (ids in range, page counts, head ratios, dtypes) happen on the host in
+ * halo_plan_create; device memory is never validated by run calls.
+ */
+#ifndef HALO_ATTN_H
+#define HALO_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HALO_OK = 0,
+  HALO_ERR_INVALID_ARGUMENT = 1,   /* malformed forest, null pointer, bad size */
+  HALO_ERR_UNSUPPORTED = 2,        /* valid but not built: head_dim, page size, dtype */
+  HALO_ERR_WORKSPACE_TOO_SMALL = 3,
+  HALO_ERR_HIP = 4                 /* a HIP runtime call or kernel launch failed */
+} halo_status_t;
+
+typedef enum { HALO_F32 = 0, HALO_BF16 = 1 } halo_dtype_t;
+
+/* Which pool halo_kv_page_gather reads. */
+typedef enum { HALO_POOL_K = 0, HALO_POOL_V = 1 } halo_pool_kind_t;
+
+typedef struct {
+  int32_t num_q_heads;      /* H_q; a multiple of num_kv_heads */
+  int32_t num_kv_heads;     /* H_kv >= 1 */
+  int32_t head_dim;         /* 64 or 128 */
+  int32_t page_size;        /* tokens per page; 16 */
+  int64_t num_pool_pages;   /* capacity of k_pool / v_pool, in pages */
+  halo_dtype_t kv_dtype;    /* element type of q, k_pool, v_pool */
+  halo_dtype_t out_dtype;   /* HALO_F32, or equal to kv_dtype */
+  float sm_scale;           /* score scale, normally 1/sqrt(head_dim) */
+} halo_attn_params_t;
+
+/* Prefix forest, HOST arrays in CSR form (§2 intra-batch prefix sharing). */
+typedef struct {
+  int32_t num_segments;
+  const int32_t* seg_len;          /* [S] tokens per segment, >= 0 */
+  const int32_t* seg_page_indptr;  /* [S+1], nondecreasing, starts at 0 */
+  const int32_t* seg_page_ids;     /* [seg_page_indptr[S]] page ids in [0, num_pool_pages);
+                                      segment s lists exactly ceil(seg_len[s]/page_size)
+                                      pages; a page may appear in several segments */
+  int32_t num_requests;
+  const int32_t* req_seg_indptr;   /* [R+1] */
+  const int32_t* req_seg_ids;      /* each request's path, root first; no segment twice */
+  const int32_t* q_len;            /* NULL: decode, one query per request.
+                                      Otherwise prefill: q_len[r] new tokens of request r,
+                                      whose K/V are the LAST segment of its path
+                                      (seg_len == q_len[r]); that segment may appear in
+                                      no other path. Chunk query i sees chunk keys <= i
+                                      and every key of the earlier segments. */
+} halo_forest_t;
+
+typedef struct halo_plan halo_plan_t;
+
+/* Validate a forest and build the work lists of one batch step.
+ * On success *plan is set, *device_meta_bytes is the size of the device
+ * buffer halo_plan_upload fills, and *workspace_bytes the scratch the run
+ * call needs (0 for prefill). Host arrays are copied; the caller may free
+ * them on return. Returns INVALID_ARGUMENT / UNSUPPORTED with a message on
+ * any malformed or unsupported input; *plan is then NULL. */
+halo_status_t halo_plan_create(const halo_attn_params_t* params,
+                               const halo_forest_t* forest,
+                               halo_plan_t** plan,
+                               size_t* device_meta_bytes,
+                               size_t* workspace_bytes);
+
+/* Copy the plan's metadata (page ids, work lists) into device_meta, a
+ * caller-owned device buffer of at least device_meta_bytes, asynchronously
+ * on stream. The plan must stay alive until the copy has completed. */
+halo_status_t halo_plan_upload(const halo_plan_t* plan, void* device_meta,
+                               size_t device_meta_bytes, void* stream);
+
+void halo_plan_destroy(halo_plan_t* plan);
+
+/* Decode attention over the forest (one query per request).
+ * q, k_pool, v_pool, o, device_meta, workspace: device pointers, layouts
+ * above; lse may be NULL. workspace holds per-chunk partial results and must
+ * be at least the plan's workspace_bytes (its contents on entry do not
+ * matter). The plan must be a decode plan whose metadata was uploaded to
+ * device_meta. Shared segments are read once per group of stacked query
+ * rows (the grouped prefix pass, §2 intra-batch prefix sharing); partial
+ * results over disjoint key ranges are combined with the exact log-sum-exp
+ * rule, so the result equals unshared attention (§3 "Scope"). */
+halo_status_t halo_prefix_attn_decode(const halo_plan_t* plan, const void* device_meta,
+                                      const void* q, const void* k_pool, const void* v_pool,
+                                      void* o, float* lse,
+                                      void* workspace, size_t workspace_bytes,
+                                      void* stream);
+
+/* Chunked prefill over cached prefixes (§4.1 prefix-caching discount):
+ * every chunk query attends to its path's earlier segments and causally to
+ * its own chunk. Arguments as for decode; the plan must be a prefill plan.
+ * workspace may be NULL when the plan's workspace_bytes is 0. */
+halo_status_t halo_prefix_attn_prefill(const halo_plan_t* plan, const void* device_meta,
+                                       const void* q, const void* k_pool, const void* v_pool,
+                                       void* o, float* lse,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/* Page gather (§7 PagedAttention): copy the tokens of num_seqs page lists out
+ * of one pool into a dense token-major buffer, bit for bit.
+ *   out[out_token_offset[i] + t][h][:] = token t of sequence i, head h
+ * for t < seq_len[i], where token t lives in page page_ids[seq_page_indptr[i]
+ * + t / page_size]. pool_kind says whether pool has the k_pool or the
+ * v_pool layout. page_ids, seq_page_indptr, seq_len, out_token_offset and
+ * out are DEVICE pointers; out is [*][num_kv_heads][head_dim] of kv_dtype.
+ * Only params' num_kv_heads, head_dim, page_size, num_pool_pages and
+ * kv_dtype are used. Every page of a sequence whose page count is not
+ * ceil(seq_len/page_size), and every page whose id is outside
+ * [0, num_pool_pages), is skipped (its tokens in out are left untouched);
+ * if error_flag (device int32, may be NULL) is given, 1 is then written
+ * there. 0 is never written, so the caller clears the flag beforehand. */
+halo_status_t halo_kv_page_gather(const void* pool, const halo_attn_params_t* params,
+                                  halo_pool_kind_t pool_kind,
+                                  const int32_t* page_ids, const int32_t* seq_page_indptr,
+                                  const int32_t* seq_len, const int64_t* out_token_offset,
+                                  int32_t num_seqs, void* out, int32_t* error_flag,
+                                  void* stream);
+
+/* Plan statistics for callers and benchmarks (host memory, no device work). */
+typedef struct {
+  int32_t is_prefill;
+  int32_t num_items;          /* wavefront work items */
+  int32_t num_shared_items;   /* of which cover a segment shared by >= 2 requests */
+  int32_t num_merge_rows;     /* output rows combined from several partials */
+  int64_t num_partial_rows;   /* partial (o, lse) rows written to the workspace */
+  int64_t num_query_rows;     /* rows of q / o */
+  int64_t distinct_kv_tokens; /* sum of segment lengths, each segment once */
+  int64_t visible_pairs;      /* sum over query rows and q heads of visible keys */
+} halo_plan_stats_t;
+
+halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* stats);
+
+/* Read-only view of the metadata image halo_plan_upload copies to the device,
+ * for inspection and host-side testing of the work lists. Byte offsets of
+ * each int32 array inside the image, and the element counts:
+ *   items:  n_items  x {row_begin, n_rows, span_begin, n_spans, kv_head,
+ *                       part_base (-1: final rows), keys, unused}
+ *   spans:  n_spans  x {segment, key_begin, key_end, causal}
+ *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position}
+ *   merge_rows [n_merge], merge_indptr [n_merge + 1], merge_parts: partial
+ *   row ids combined into each listed output row.
+ * *image stays valid until halo_plan_destroy. */
+typedef struct {
+  uint64_t seg_page_off, seg_len, page_ids, items, spans, rows;
+  uint64_t merge_rows, merge_indptr, merge_parts, total_bytes;
+  int32_t n_items, n_spans, n_rows, n_merge, n_merge_parts, n_pages;
+} halo_plan_layout_t;
+
+halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void** image,
+                                halo_plan_layout_t* layout);
+
+const char* halo_status_string(halo_status_t status);
+const char* halo_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HALO_ATTN_H */

@@ -1,0 +1,62 @@
+"""Build libhalo_attn.so (gfx950) in-tree with hipcc.
+
+    python -m paper_2509_02121_amd.build          # or build() from Python
+
+The planner is plain host C++ (g++); the kernels and run-time entry points
+are HIP compiled for gfx950 only. Every build recompiles from source.
+"""
+
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB_NAME = "libhalo_attn.so"
+LIB_PATH = os.path.join(PKG, LIB_NAME)
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+HIP_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    # packed fp32 VALU forms stay off: the kernels are written for scalar fp32
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function",
+]
+
+
+def _run(cmd):
+    print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+
+
+def build(verbose=True):
+    """Compile every source and link the shared library next to this file."""
+    tmp = tempfile.mkdtemp(prefix="halo_build_")
+    try:
+        plan_o = os.path.join(tmp, "halo_plan.o")
+        kern_o = os.path.join(tmp, "halo_kernels.o")
+        procs = [
+            subprocess.Popen(["g++", "-std=c++17", "-O2", "-fPIC", "-Wall", "-Wextra",
+                              "-I", INCLUDE, "-c", os.path.join(CSRC, "halo_plan.cpp"), "-o", plan_o]),
+            subprocess.Popen([HIPCC] + HIP_FLAGS + ["-I", INCLUDE, "-c",
+                                                   os.path.join(CSRC, "halo_kernels.hip"), "-o", kern_o]),
+        ]
+        rcs = [p.wait() for p in procs]
+        if any(rcs):
+            raise RuntimeError(f"compilation failed (exit codes {rcs})")
+        out_tmp = LIB_PATH + ".tmp"
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, kern_o, "-o", out_tmp])
+        os.replace(out_tmp, LIB_PATH)
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    return LIB_PATH
+
+
+if __name__ == "__main__":
+    sys.exit(0 if build() else 1)

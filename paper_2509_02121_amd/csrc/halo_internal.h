@@ -1,0 +1,90 @@
+// Internal structures shared by the host planner and the gfx950 kernels.
+#pragma once
+
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "halo_attn.h"
+
+namespace halo {
+
+// Rows of one wavefront work item: at most 16 query rows (one MFMA N tile).
+constexpr int kRowsPerItem = 16;
+// Keys consumed per inner step: two pages of 16 (one K=32 MFMA for P*V).
+constexpr int kKeysPerStep = 32;
+
+// One wavefront's work: up to 16 query rows against a list of key spans.
+// 32 bytes, read by all 64 lanes.
+struct Item {
+  int32_t row_begin;   // first entry in the row table
+  int32_t n_rows;      // 1..16
+  int32_t span_begin;  // first entry in the span table
+  int32_t n_spans;     // >= 1
+  int32_t kv_head;
+  int32_t part_base;   // >= 0: partial rows part_base + i in the workspace;
+                       // -1: final rows written straight to o / lse
+  int32_t keys;        // visible-key estimate (cost, for ordering only)
+  int32_t pad;
+};
+
+// A contiguous range of keys of one segment, [key_begin, key_end).
+// key_begin is a multiple of kKeysPerStep.
+struct Span {
+  int32_t seg;
+  int32_t key_begin;
+  int32_t key_end;
+  int32_t causal;      // 1: key j visible to a row iff j <= row.qpos
+};
+
+// One query row: its row index into q / o (token * H_q + head) and its
+// position inside the prefill chunk (for the causal span).
+struct Row {
+  int32_t q_row;
+  int32_t qpos;
+};
+
+// Offsets (bytes) of the arrays packed in the device metadata buffer.
+struct MetaLayout {
+  size_t seg_page_off = 0;   // int32 [S]  first page slot of each segment
+  size_t seg_len = 0;        // int32 [S]
+  size_t page_ids = 0;       // int32 [total pages]
+  size_t items = 0;          // Item  [n_items]
+  size_t spans = 0;          // Span  [n_spans]
+  size_t rows = 0;           // Row   [n_rows]
+  size_t merge_rows = 0;     // int32 [n_merge] output row (q_row) per merge entry
+  size_t merge_indptr = 0;   // int32 [n_merge + 1]
+  size_t merge_parts = 0;    // int32 [n_parts] partial row ids
+  size_t total = 0;
+};
+
+}  // namespace halo
+
+struct halo_plan {
+  halo_attn_params_t params;
+  bool prefill = false;
+  int32_t num_segments = 0;
+  int32_t num_requests = 0;
+  int64_t num_query_rows = 0;
+  int32_t n_items = 0;
+  int32_t n_shared_items = 0;
+  int32_t n_merge = 0;
+  int32_t n_spans = 0;
+  int32_t n_rows = 0;
+  int32_t n_merge_parts = 0;
+  int32_t n_pages = 0;
+  int64_t n_part_rows = 0;
+  int64_t distinct_kv_tokens = 0;
+  int64_t visible_pairs = 0;
+  size_t workspace_bytes = 0;
+  halo::MetaLayout layout;
+  std::vector<uint8_t> meta;   // host image of the device metadata
+};
+
+namespace halo {
+// Thread-local error reporting used by every entry point.
+halo_status_t fail(halo_status_t st, const std::string& msg);
+void clear_error();
+const char* last_error();
+}  // namespace halo

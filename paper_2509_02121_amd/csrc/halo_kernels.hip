@@ -1,0 +1,516 @@
+// gfx950 kernels and the run-time entry points of the C ABI.
+//
+// attn_items_kernel: one wavefront per work item (<= 16 query rows against a
+//   list of key spans). Per step of 32 keys (two 16-token pages):
+//     S^T = K Q^T  on v_mfma_f32_16x16x32_bf16 (4 MFMAs per 16 keys at d=128)
+//     online softmax in the log2 domain (row max / sum over the 4 lane groups)
+//     O^T += V^T P^T on the same MFMA (8 MFMAs at d=128)
+//   K tiles are token-major and V tiles dim-major in the page pools, so both
+//   MFMA A operands are one 16-byte load per lane straight from memory. Keys
+//   inside a 32-key step are permuted so that the softmax output of the QK
+//   product is already laid out as the PV B operand (no lane exchange).
+// merge_kernel: exact log-sum-exp combination of partial results over
+//   disjoint key ranges (the merge that makes shared == unshared).
+// gather_kernel: bit copy of paged tokens into a dense token-major buffer.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <string>
+
+#include "halo_internal.h"
+
+using namespace halo;
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x8_t __attribute__((ext_vector_type(8)));
+
+constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kLog2e = 1.44269504088896340736f;
+
+// ---------------------------------------------------------------- fragments
+// A fragment is the 8 K-slot values one lane feeds to a 16x16x32 MFMA.
+
+template <typename T> struct FragOf;
+template <> struct FragOf<__bf16> { using type = bf16x8_t; };
+template <> struct FragOf<float> { using type = f32x8_t; };
+
+__device__ __forceinline__ bf16x8_t load8(const __bf16* p) {
+  return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
+}
+__device__ __forceinline__ f32x8_t load8(const float* p) {
+  const uint4* q = reinterpret_cast<const uint4*>(p);
+  struct Pair { uint4 a, b; } v{q[0], q[1]};
+  return __builtin_bit_cast(f32x8_t, v);
+}
+
+template <typename F> __device__ __forceinline__ F zero_frag() { return F{}; }
+
+// D(16x16) += A(16x32) B(32x16). bf16: one MFMA. fp32: the same 32-deep
+// contraction as eight 16x16x4 MFMAs, slot j of every lane in the j-th one,
+// so both element types share one register layout.
+__device__ __forceinline__ f32x4_t mma(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mma(f32x8_t a, f32x8_t b, f32x4_t c) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
+  return c;
+}
+
+__device__ __forceinline__ bf16x8_t to_frag(const float (&p)[8], bf16x8_t*) {
+  bf16x8_t r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = (__bf16)p[j];
+  return r;
+}
+__device__ __forceinline__ f32x8_t to_frag(const float (&p)[8], f32x8_t*) {
+  f32x8_t r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = p[j];
+  return r;
+}
+
+__device__ __forceinline__ void store4(float* dst, f32x4_t v) {
+  *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store4(__bf16* dst, f32x4_t v) {
+  typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+  bf16x4_t r;
+  r[0] = (__bf16)v[0];
+  r[1] = (__bf16)v[1];
+  r[2] = (__bf16)v[2];
+  r[3] = (__bf16)v[3];
+  *reinterpret_cast<uint2*>(dst) = __builtin_bit_cast(uint2, r);
+}
+
+// ---------------------------------------------------------------- attention
+
+struct AttnArgs {
+  const void* q;
+  const void* k_pool;
+  const void* v_pool;
+  void* o;
+  float* lse;
+  float* part_o;
+  float* part_lse;
+  const int32_t* seg_page_off;
+  const int32_t* seg_len;
+  const int32_t* page_ids;
+  const Item* items;
+  const Span* spans;
+  const Row* rows;
+  int32_t n_items;
+  int32_t num_kv_heads;
+  float scale_log2;   // sm_scale * log2(e)
+};
+
+// One work item on one wavefront. Lane l: col = l % 16, grp = l / 16.
+//  * QK: A = K rows (A row = col), B = Q^T (B column = query row col);
+//    result lane (col, grp) holds S[row col][keys of slot j], j = 4X + i.
+//  * A 32-key step spans pages P0, P1. Slot j of lane group grp is the key
+//    16*(grp/2) + 8*(grp%2) + j of the step, so a lane's 8 V^T values are 8
+//    consecutive keys of one page (one 16-byte load), and A row r of the QK
+//    tile X is key 16*(r/8) + 8*((r/4)%2) + 4X + r%4.
+//  * PV: A = V^T rows (A row = d index col of block b), B = P^T; result lane
+//    (col, grp) holds O^T[d = 16b + 4grp + i][row col].
+template <typename T, int D, typename TO>
+__device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int lane) {
+  using F = typename FragOf<T>::type;
+  constexpr int NS = D / 32;   // QK steps over d
+  constexpr int NB = D / 16;   // PV output blocks over d
+  constexpr int64_t kTile = 16 * D;   // elements of one (page, head) tile
+  const int col = lane & 15;
+  const int grp = lane >> 4;
+
+  Row row{-1, 0};
+  if (col < it.n_rows) row = a.rows[it.row_begin + col];
+
+  F qf[NS];
+  {
+    const T* qp = static_cast<const T*>(a.q) + (int64_t)(row.q_row < 0 ? 0 : row.q_row) * D + 8 * grp;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qf[s] = row.q_row >= 0 ? load8(qp + 32 * s) : zero_frag<F>();
+  }
+
+  const int64_t page_stride = (int64_t)a.num_kv_heads * kTile;
+  const T* kbase = static_cast<const T*>(a.k_pool) + (int64_t)it.kv_head * kTile;
+  const T* vbase = static_cast<const T*>(a.v_pool) + (int64_t)it.kv_head * kTile;
+  const int krow_page = col >> 3;
+  const int krow_key = ((col >> 2) & 1) * 8 + (col & 3);
+  const int slot_page = grp >> 1;
+  const int slot_key = (grp & 1) * 8;
+
+  float m = kNegInf;
+  float lsum = 0.f;
+  f32x4_t acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int si = 0; si < it.n_spans; ++si) {
+    const Span sp = a.spans[it.span_begin + si];
+    const int32_t* pids = a.page_ids + a.seg_page_off[sp.seg];
+    for (int t0 = sp.key_begin; t0 < sp.key_end; t0 += kKeysPerStep) {
+      const bool has1 = t0 + 16 < sp.key_end;
+      const int pid0 = pids[t0 >> 4];
+      const int pid1 = has1 ? pids[(t0 >> 4) + 1] : pid0;
+
+      // K operand: two 16-key tiles of this step.
+      F kf[2][NS];
+      {
+        const bool ok = krow_page == 0 || has1;
+        const int pid = krow_page ? pid1 : pid0;
+        const T* kp = kbase + (int64_t)pid * page_stride + krow_key * D + 8 * grp;
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+          for (int s = 0; s < NS; ++s) kf[x][s] = ok ? load8(kp + 4 * x * D + 32 * s) : zero_frag<F>();
+      }
+      // V^T operand: rows d = 16b + col, 8 consecutive keys of one page.
+      F vf[NB];
+      {
+        const bool ok = slot_page == 0 || has1;
+        const int pid = slot_page ? pid1 : pid0;
+        const T* vp = vbase + (int64_t)pid * page_stride + col * 16 + slot_key;
+#pragma unroll
+        for (int b = 0; b < NB; ++b) vf[b] = ok ? load8(vp + b * 256) : zero_frag<F>();
+      }
+
+      f32x4_t sacc[2];
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        sacc[x] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s) sacc[x] = mma(kf[x][s], qf[s], sacc[x]);
+      }
+
+      const int key0 = t0 + 16 * slot_page + slot_key;   // key of slot 0
+      float sv[8];
+      float mt = kNegInf;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int key = key0 + j;
+        const bool vis = key < sp.key_end && (!sp.causal || key <= row.qpos);
+        sv[j] = vis ? sacc[j >> 2][j & 3] * a.scale_log2 : kNegInf;
+        mt = fmaxf(mt, sv[j]);
+      }
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float m_new = fmaxf(m, mt);
+      const float m_use = m_new == kNegInf ? 0.f : m_new;
+      const float alpha = exp2f(m - m_use);
+      float p[8];
+      float psum = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        p[j] = exp2f(sv[j] - m_use);
+        psum += p[j];
+      }
+      lsum = lsum * alpha + psum;
+      m = m_new;
+      // Keys past the span end may be NaN page tails: zero V there (P is 0,
+      // but 0 * NaN would still poison the sum).
+      if (key0 + 8 > sp.key_end) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (key0 + j >= sp.key_end)
+#pragma unroll
+            for (int b = 0; b < NB; ++b) vf[b][j] = (T)0.f;
+      }
+      const F pf = to_frag(p, (F*)nullptr);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        acc[b] *= alpha;
+        acc[b] = mma(vf[b], pf, acc[b]);
+      }
+    }
+  }
+
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if (col >= it.n_rows) return;
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  const float lse2 = lsum > 0.f ? m + __log2f(lsum) : kNegInf;
+  if (it.part_base >= 0) {
+    const int64_t prow = (int64_t)it.part_base + col;
+    float* dst = a.part_o + prow * D + 4 * grp;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[b] * inv);
+    if (grp == 0) a.part_lse[prow] = lse2;
+  } else {
+    TO* dst = static_cast<TO*>(a.o) + (int64_t)row.q_row * D + 4 * grp;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[b] * inv);
+    if (grp == 0 && a.lse) a.lse[row.q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
+  }
+}
+
+template <typename T, int D, typename TO>
+__global__ __launch_bounds__(256) void attn_items_kernel(AttnArgs a) {
+  const int item_id = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
+  if (item_id >= a.n_items) return;
+  const Item it = a.items[item_id];
+  run_item<T, D, TO>(a, it, threadIdx.x & 63);
+}
+
+// ---------------------------------------------------------------- merge
+
+struct MergeArgs {
+  const float* part_o;
+  const float* part_lse;
+  const int32_t* merge_rows;
+  const int32_t* merge_indptr;
+  const int32_t* merge_parts;
+  void* o;
+  float* lse;
+  int32_t n_merge;
+};
+
+// Rows with several partials (o_i normalized, lse_i in log2):
+//   M = max_i lse_i, w_i = 2^(lse_i - M), O = sum w_i o_i / sum w_i,
+//   LSE = (M + log2 sum w_i) * ln 2.  Rows with no parts: O = 0, LSE = -inf.
+template <int D, typename TO>
+__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
+  constexpr int TPR = D / 4;
+  constexpr int RPB = 256 / TPR;
+  const int r = blockIdx.x * RPB + threadIdx.x / TPR;
+  const int t = threadIdx.x % TPR;
+  if (r >= a.n_merge) return;
+  const int q_row = a.merge_rows[r];
+  const int p0 = a.merge_indptr[r], p1 = a.merge_indptr[r + 1];
+  float mx = kNegInf;
+  for (int p = p0; p < p1; ++p) mx = fmaxf(mx, a.part_lse[a.merge_parts[p]]);
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  if (mx != kNegInf) {
+    for (int p = p0; p < p1; ++p) {
+      const int pr = a.merge_parts[p];
+      const float w = exp2f(a.part_lse[pr] - mx);
+      const float4 v = *reinterpret_cast<const float4*>(a.part_o + (int64_t)pr * D + 4 * t);
+      wsum += w;
+      acc += w * f32x4_t{v.x, v.y, v.z, v.w};
+    }
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 4 * t, acc * inv);
+  if (t == 0 && a.lse) a.lse[q_row] = wsum > 0.f ? (mx + __log2f(wsum)) * kLn2 : kNegInf;
+}
+
+// ---------------------------------------------------------------- gather
+
+struct GatherArgs {
+  const void* pool;
+  const int32_t* page_ids;
+  const int32_t* seq_page_indptr;
+  const int32_t* seq_len;
+  const int64_t* out_token_offset;
+  void* out;
+  int32_t* error_flag;
+  int64_t num_pool_pages;
+  int32_t num_seqs;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t v_layout;
+};
+
+// One block per (page slot, head) tile, grid-stride. W is an unsigned word of
+// the element's width, so every bit pattern (NaN payloads included) moves
+// unchanged.
+template <typename W>
+__global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
+  __shared__ W tile[128 * 17];
+  const int D = a.head_dim;
+  const int64_t total_tiles = (int64_t)a.seq_page_indptr[a.num_seqs] * a.num_kv_heads;
+  const W* pool = static_cast<const W*>(a.pool);
+  W* out = static_cast<W*>(a.out);
+  for (int64_t tl = blockIdx.x; tl < total_tiles; tl += gridDim.x) {
+    const int64_t slot = tl / a.num_kv_heads;
+    const int h = (int)(tl % a.num_kv_heads);
+    int lo = 0, hi = a.num_seqs - 1;   // last sequence whose first slot <= slot
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.seq_page_indptr[mid] <= slot) lo = mid; else hi = mid - 1;
+    }
+    const int len = a.seq_len[lo];
+    const int npages = a.seq_page_indptr[lo + 1] - a.seq_page_indptr[lo];
+    const int pid = a.page_ids[slot];
+    if (len < 0 || npages != (len + 15) / 16 || pid < 0 || pid >= a.num_pool_pages) {
+      if (threadIdx.x == 0 && a.error_flag) a.error_flag[0] = 1;
+      continue;
+    }
+    const int t0 = (int)(slot - a.seq_page_indptr[lo]) * 16;
+    const int n = min(16, len - t0);
+    const int64_t out_tok = a.out_token_offset[lo] + t0;
+    const W* src = pool + ((int64_t)pid * a.num_kv_heads + h) * 16 * D;
+    if (!a.v_layout) {
+      for (int e = threadIdx.x; e < n * D; e += blockDim.x) {
+        const int tok = e / D, c = e - tok * D;
+        out[((out_tok + tok) * a.num_kv_heads + h) * D + c] = src[e];
+      }
+    } else {
+      for (int e = threadIdx.x; e < 16 * D; e += blockDim.x) {
+        const int c = e >> 4, tok = e & 15;
+        tile[c * 17 + tok] = src[e];
+      }
+      __syncthreads();
+      for (int e = threadIdx.x; e < n * D; e += blockDim.x) {
+        const int tok = e / D, c = e - tok * D;
+        out[((out_tok + tok) * a.num_kv_heads + h) * D + c] = tile[c * 17 + tok];
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// ---------------------------------------------------------------- host side
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+halo_status_t hip_check(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(HALO_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  return HALO_OK;
+}
+
+template <typename T, int D, typename TO>
+void launch_attention(const AttnArgs& args, const MergeArgs& margs, hipStream_t stream) {
+  if (args.n_items > 0) {
+    const int blocks = (args.n_items + 3) / 4;
+    hipLaunchKernelGGL((attn_items_kernel<T, D, TO>), dim3(blocks), dim3(256), 0, stream, args);
+  }
+  if (margs.n_merge > 0) {
+    constexpr int rpb = 256 / (D / 4);
+    const int blocks = (margs.n_merge + rpb - 1) / rpb;
+    hipLaunchKernelGGL((merge_kernel<D, TO>), dim3(blocks), dim3(256), 0, stream, margs);
+  }
+}
+
+halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const void* device_meta,
+                            const void* q, const void* k_pool, const void* v_pool, void* o, float* lse,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (!plan) return fail(HALO_ERR_INVALID_ARGUMENT, "plan must not be NULL");
+  if (plan->prefill != want_prefill)
+    return fail(HALO_ERR_INVALID_ARGUMENT,
+                want_prefill ? "plan was built for decode (q_len == NULL)" : "plan was built for prefill");
+  if (!device_meta || !q || !k_pool || !v_pool || !o)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "device_meta, q, k_pool, v_pool and o must not be NULL");
+  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(o) ||
+      (reinterpret_cast<uintptr_t>(device_meta) & 255) != 0)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "q, k_pool, v_pool, o must be 16-byte aligned, device_meta 256-byte");
+  if (workspace_bytes < plan->workspace_bytes)
+    return fail(HALO_ERR_WORKSPACE_TOO_SMALL, "workspace needs " + std::to_string(plan->workspace_bytes) +
+                                                  " bytes, got " + std::to_string(workspace_bytes));
+  if (plan->workspace_bytes > 0 && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) != 0))
+    return fail(HALO_ERR_INVALID_ARGUMENT, "workspace must be a 256-byte aligned device pointer");
+
+  const halo_attn_params_t& p = plan->params;
+  const MetaLayout& L = plan->layout;
+  const uint8_t* m = static_cast<const uint8_t*>(device_meta);
+  const int D = p.head_dim;
+  float* part_o = static_cast<float*>(workspace);
+  float* part_lse = plan->n_part_rows
+                        ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
+                                                   align256((size_t)plan->n_part_rows * D * sizeof(float)))
+                        : nullptr;
+  AttnArgs args{q, k_pool, v_pool, o, lse, part_o, part_lse,
+                reinterpret_cast<const int32_t*>(m + L.seg_page_off),
+                reinterpret_cast<const int32_t*>(m + L.seg_len),
+                reinterpret_cast<const int32_t*>(m + L.page_ids),
+                reinterpret_cast<const Item*>(m + L.items),
+                reinterpret_cast<const Span*>(m + L.spans),
+                reinterpret_cast<const Row*>(m + L.rows),
+                plan->n_items, p.num_kv_heads, p.sm_scale * kLog2e};
+  MergeArgs margs{part_o, part_lse,
+                  reinterpret_cast<const int32_t*>(m + L.merge_rows),
+                  reinterpret_cast<const int32_t*>(m + L.merge_indptr),
+                  reinterpret_cast<const int32_t*>(m + L.merge_parts),
+                  o, lse, plan->n_merge};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();   // clear any stale error of the caller
+  const bool out_f32 = p.out_dtype == HALO_F32;
+  if (p.kv_dtype == HALO_BF16) {
+    if (D == 128) {
+      if (out_f32) launch_attention<__bf16, 128, float>(args, margs, st);
+      else launch_attention<__bf16, 128, __bf16>(args, margs, st);
+    } else {
+      if (out_f32) launch_attention<__bf16, 64, float>(args, margs, st);
+      else launch_attention<__bf16, 64, __bf16>(args, margs, st);
+    }
+  } else {
+    if (D == 128) launch_attention<float, 128, float>(args, margs, st);
+    else launch_attention<float, 64, float>(args, margs, st);
+  }
+  return hip_check("attention launch");
+}
+
+}  // namespace
+
+extern "C" halo_status_t halo_plan_upload(const halo_plan_t* plan, void* device_meta,
+                                          size_t device_meta_bytes, void* stream) {
+  clear_error();
+  if (!plan || !device_meta) return fail(HALO_ERR_INVALID_ARGUMENT, "plan and device_meta must not be NULL");
+  if (device_meta_bytes < plan->layout.total)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "device_meta needs " + std::to_string(plan->layout.total) + " bytes");
+  if ((reinterpret_cast<uintptr_t>(device_meta) & 255) != 0)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "device_meta must be 256-byte aligned");
+  hipError_t e = hipMemcpyAsync(device_meta, plan->meta.data(), plan->layout.total, hipMemcpyHostToDevice,
+                                static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(HALO_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+  return HALO_OK;
+}
+
+extern "C" halo_status_t halo_prefix_attn_decode(const halo_plan_t* plan, const void* device_meta,
+                                                 const void* q, const void* k_pool, const void* v_pool,
+                                                 void* o, float* lse, void* workspace,
+                                                 size_t workspace_bytes, void* stream) {
+  return run_attention(plan, false, device_meta, q, k_pool, v_pool, o, lse, workspace, workspace_bytes,
+                       stream);
+}
+
+extern "C" halo_status_t halo_prefix_attn_prefill(const halo_plan_t* plan, const void* device_meta,
+                                                  const void* q, const void* k_pool, const void* v_pool,
+                                                  void* o, float* lse, void* workspace,
+                                                  size_t workspace_bytes, void* stream) {
+  return run_attention(plan, true, device_meta, q, k_pool, v_pool, o, lse, workspace, workspace_bytes,
+                       stream);
+}
+
+extern "C" halo_status_t halo_kv_page_gather(const void* pool, const halo_attn_params_t* params,
+                                             halo_pool_kind_t pool_kind, const int32_t* page_ids,
+                                             const int32_t* seq_page_indptr, const int32_t* seq_len,
+                                             const int64_t* out_token_offset, int32_t num_seqs, void* out,
+                                             int32_t* error_flag, void* stream) {
+  clear_error();
+  if (!params) return fail(HALO_ERR_INVALID_ARGUMENT, "params must not be NULL");
+  if (num_seqs < 0) return fail(HALO_ERR_INVALID_ARGUMENT, "num_seqs must be >= 0");
+  if (num_seqs == 0) return HALO_OK;
+  if (!pool || !page_ids || !seq_page_indptr || !seq_len || !out_token_offset || !out)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "pool, page_ids, seq_page_indptr, seq_len, out_token_offset, out "
+                                           "must not be NULL");
+  if (params->head_dim != 64 && params->head_dim != 128)
+    return fail(HALO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (params->page_size != 16) return fail(HALO_ERR_UNSUPPORTED, "page_size must be 16");
+  if (params->num_kv_heads < 1) return fail(HALO_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
+  if (pool_kind != HALO_POOL_K && pool_kind != HALO_POOL_V)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "pool_kind must be HALO_POOL_K or HALO_POOL_V");
+  GatherArgs g{pool, page_ids, seq_page_indptr, seq_len, out_token_offset, out, error_flag,
+               params->num_pool_pages, num_seqs, params->num_kv_heads, params->head_dim,
+               pool_kind == HALO_POOL_V ? 1 : 0};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const int blocks = 2048;
+  if (params->kv_dtype == HALO_BF16)
+    hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st, g);
+  else if (params->kv_dtype == HALO_F32)
+    hipLaunchKernelGGL(gather_kernel<uint32_t>, dim3(blocks), dim3(256), 0, st, g);
+  else
+    return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
+  return hip_check("gather launch");
+}

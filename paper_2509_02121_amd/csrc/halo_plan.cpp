@@ -1,0 +1,488 @@
+// Host planner: validates a prefix forest and turns it into wavefront work
+// items for the gfx950 kernels. Pure host C++ (no HIP calls), so it can be
+// exercised and sanitized on a machine without a GPU.
+//
+// Decode (arXiv 2509.02121 §2, intra-batch prefix sharing): a segment on the
+// path of two or more requests is "shared". Its query rows -- every (request,
+// q head) pair of one kv head -- are stacked 16 to a work item, so each of the
+// segment's pages is read for 16 rows at a time instead of once per request
+// (the grouped prefix pass). Segments on one path only are "private"; each
+// request's private keys are split into chunks (the suffix pass). Every item
+// over a subset of a row's keys writes a partial (o, lse); rows with several
+// partials are combined by the log-sum-exp merge, rows with exactly one write
+// their final result directly.
+//
+// Prefill (§4.1, prefix caching): each item holds 16 (query, head) rows of one
+// request and walks all of that request's keys, the cached prefix first and
+// its own chunk last, causally; results are final.
+
+#include <stdlib.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "halo_internal.h"
+
+namespace halo {
+
+namespace {
+thread_local std::string g_last_error;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int env_int(const char* name, int dflt, int lo, int hi) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  long x = strtol(v, nullptr, 10);
+  if (x < lo) x = lo;
+  if (x > hi) x = hi;
+  return (int)x;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+}  // namespace
+
+halo_status_t fail(halo_status_t st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+const char* last_error() { return g_last_error.c_str(); }
+
+}  // namespace halo
+
+using namespace halo;
+
+namespace {
+
+halo_status_t validate(const halo_attn_params_t* p, const halo_forest_t* f) {
+  if (!p || !f) return fail(HALO_ERR_INVALID_ARGUMENT, "params and forest must not be NULL");
+  if (p->num_kv_heads < 1 || p->num_q_heads < 1)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "num_q_heads and num_kv_heads must be >= 1");
+  if (p->num_q_heads % p->num_kv_heads != 0)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "num_q_heads must be a multiple of num_kv_heads");
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(HALO_ERR_UNSUPPORTED, "head_dim must be 64 or 128, got " + std::to_string(p->head_dim));
+  if (p->page_size != 16)
+    return fail(HALO_ERR_UNSUPPORTED, "page_size must be 16, got " + std::to_string(p->page_size));
+  if (p->kv_dtype != HALO_F32 && p->kv_dtype != HALO_BF16)
+    return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
+  if (p->out_dtype != HALO_F32 && p->out_dtype != p->kv_dtype)
+    return fail(HALO_ERR_UNSUPPORTED, "out_dtype must be HALO_F32 or equal to kv_dtype");
+  if (p->num_pool_pages < 0 || p->num_pool_pages > (int64_t)std::numeric_limits<int32_t>::max())
+    return fail(HALO_ERR_INVALID_ARGUMENT, "num_pool_pages must be in [0, 2^31)");
+  if (!std::isfinite(p->sm_scale)) return fail(HALO_ERR_INVALID_ARGUMENT, "sm_scale must be finite");
+  if (f->num_segments < 0 || f->num_requests < 0)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "num_segments and num_requests must be >= 0");
+  const int S = f->num_segments, R = f->num_requests;
+  if (S > 0 && (!f->seg_len || !f->seg_page_indptr))
+    return fail(HALO_ERR_INVALID_ARGUMENT, "seg_len / seg_page_indptr must not be NULL");
+  if (!f->req_seg_indptr) return fail(HALO_ERR_INVALID_ARGUMENT, "req_seg_indptr must not be NULL");
+  if (S == 0 && f->seg_page_indptr == nullptr) {
+    // fine: no segments at all
+  } else if (f->seg_page_indptr[0] != 0) {
+    return fail(HALO_ERR_INVALID_ARGUMENT, "seg_page_indptr[0] must be 0");
+  }
+  for (int s = 0; s < S; ++s) {
+    const int32_t len = f->seg_len[s];
+    if (len < 0) return fail(HALO_ERR_INVALID_ARGUMENT, "seg_len[" + std::to_string(s) + "] < 0");
+    const int64_t np = (int64_t)f->seg_page_indptr[s + 1] - f->seg_page_indptr[s];
+    if (np != ceil_div(len, p->page_size))
+      return fail(HALO_ERR_INVALID_ARGUMENT,
+                  "segment " + std::to_string(s) + " lists " + std::to_string(np) +
+                      " pages but its length " + std::to_string(len) + " needs " +
+                      std::to_string(ceil_div(len, p->page_size)));
+  }
+  const int64_t total_pages = S ? f->seg_page_indptr[S] : 0;
+  if (total_pages > 0 && !f->seg_page_ids)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "seg_page_ids must not be NULL");
+  for (int64_t i = 0; i < total_pages; ++i) {
+    const int32_t pg = f->seg_page_ids[i];
+    if (pg < 0 || pg >= p->num_pool_pages)
+      return fail(HALO_ERR_INVALID_ARGUMENT, "page id " + std::to_string(pg) + " at slot " +
+                                                 std::to_string(i) + " outside [0, num_pool_pages)");
+  }
+  if (f->req_seg_indptr[0] != 0) return fail(HALO_ERR_INVALID_ARGUMENT, "req_seg_indptr[0] must be 0");
+  for (int r = 0; r < R; ++r)
+    if (f->req_seg_indptr[r + 1] < f->req_seg_indptr[r])
+      return fail(HALO_ERR_INVALID_ARGUMENT, "req_seg_indptr must be nondecreasing");
+  const int64_t total_refs = f->req_seg_indptr[R];
+  if (total_refs > 0 && !f->req_seg_ids)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "req_seg_ids must not be NULL");
+  std::vector<int32_t> seen(S, -1);
+  for (int r = 0; r < R; ++r) {
+    for (int32_t i = f->req_seg_indptr[r]; i < f->req_seg_indptr[r + 1]; ++i) {
+      const int32_t s = f->req_seg_ids[i];
+      if (s < 0 || s >= S)
+        return fail(HALO_ERR_INVALID_ARGUMENT, "request " + std::to_string(r) + " names segment " +
+                                                   std::to_string(s) + " outside [0, num_segments)");
+      if (seen[s] == r)
+        return fail(HALO_ERR_INVALID_ARGUMENT,
+                    "request " + std::to_string(r) + " lists segment " + std::to_string(s) + " twice");
+      seen[s] = r;
+    }
+  }
+  if (f->q_len) {
+    std::vector<int32_t> refs(S, 0);
+    for (int64_t i = 0; i < total_refs; ++i) refs[f->req_seg_ids[i]]++;
+    for (int r = 0; r < R; ++r) {
+      const int32_t n = f->q_len[r];
+      if (n < 0) return fail(HALO_ERR_INVALID_ARGUMENT, "q_len must be >= 0");
+      const int32_t a = f->req_seg_indptr[r], b = f->req_seg_indptr[r + 1];
+      if (a == b) {
+        if (n != 0)
+          return fail(HALO_ERR_INVALID_ARGUMENT,
+                      "prefill request " + std::to_string(r) + " has queries but an empty path");
+        continue;
+      }
+      const int32_t last = f->req_seg_ids[b - 1];
+      if (f->seg_len[last] != n)
+        return fail(HALO_ERR_INVALID_ARGUMENT, "prefill request " + std::to_string(r) +
+                                                   ": last segment length " +
+                                                   std::to_string(f->seg_len[last]) +
+                                                   " != q_len " + std::to_string(n));
+      if (refs[last] != 1)
+        return fail(HALO_ERR_INVALID_ARGUMENT, "prefill request " + std::to_string(r) +
+                                                   ": its chunk segment appears in another path");
+    }
+  }
+  return HALO_OK;
+}
+
+// Split [0, len) into pieces of at most `chunk` keys (chunk % 32 == 0).
+void pieces(int32_t seg, int32_t len, int32_t chunk, std::vector<Span>& out) {
+  for (int32_t kb = 0; kb < len; kb += chunk)
+    out.push_back(Span{seg, kb, std::min(len, kb + chunk), 0});
+}
+
+}  // namespace
+
+extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
+                                          const halo_forest_t* forest, halo_plan_t** plan_out,
+                                          size_t* device_meta_bytes, size_t* workspace_bytes) {
+  clear_error();
+  if (!plan_out) return fail(HALO_ERR_INVALID_ARGUMENT, "plan must not be NULL");
+  *plan_out = nullptr;
+  halo_status_t st = validate(params, forest);
+  if (st != HALO_OK) return st;
+  const halo_attn_params_t& p = *params;
+  const halo_forest_t& f = *forest;
+  const int S = f.num_segments, R = f.num_requests;
+  const int Hq = p.num_q_heads, Hkv = p.num_kv_heads, G = Hq / Hkv;
+  const bool prefill = f.q_len != nullptr;
+
+  int64_t n_q_rows = R;
+  std::vector<int64_t> tok0(R + 1, 0);
+  if (prefill) {
+    for (int r = 0; r < R; ++r) tok0[r + 1] = tok0[r] + f.q_len[r];
+    n_q_rows = tok0[R];
+  } else {
+    for (int r = 0; r <= R; ++r) tok0[r] = r;
+  }
+  if (n_q_rows * Hq > (int64_t)std::numeric_limits<int32_t>::max())
+    return fail(HALO_ERR_INVALID_ARGUMENT, "query rows * num_q_heads must be < 2^31");
+
+  halo_plan* plan = new (std::nothrow) halo_plan();
+  if (!plan) return fail(HALO_ERR_INVALID_ARGUMENT, "out of host memory");
+  plan->params = p;
+  plan->prefill = prefill;
+  plan->num_segments = S;
+  plan->num_requests = R;
+  plan->num_query_rows = n_q_rows;
+
+  auto path_begin = [&](int r) { return f.req_seg_indptr[r]; };
+  auto path_end = [&](int r) { return f.req_seg_indptr[r + 1]; };
+
+  std::vector<int32_t> refs(S, 0);
+  for (int r = 0; r < R; ++r)
+    for (int32_t i = path_begin(r); i < path_end(r); ++i) refs[f.req_seg_ids[i]]++;
+  for (int s = 0; s < S; ++s) plan->distinct_kv_tokens += f.seg_len[s];
+
+  // Work items as (rows, spans) before part ids are assigned.
+  struct Proto {
+    std::vector<Row> rows;
+    std::vector<Span> spans;
+    int32_t kv_head;
+    int64_t keys;
+    bool shared;
+  };
+  std::vector<Proto> protos;
+
+  if (!prefill) {
+    const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, 1 << 20) / 32 * 32;
+    const int kc_private = env_int("HALO_KC_PRIVATE", 256, 32, 1 << 20) / 32 * 32;
+    for (int r = 0; r < R; ++r) {
+      int64_t keys = 0;
+      for (int32_t i = path_begin(r); i < path_end(r); ++i) keys += f.seg_len[f.req_seg_ids[i]];
+      plan->visible_pairs += keys * Hq;
+    }
+    // Grouped prefix pass: shared segments, all their rows stacked.
+    std::vector<std::vector<int32_t>> seg_reqs(S);
+    for (int r = 0; r < R; ++r)
+      for (int32_t i = path_begin(r); i < path_end(r); ++i) seg_reqs[f.req_seg_ids[i]].push_back(r);
+    for (int s = 0; s < S; ++s) {
+      if (refs[s] < 2 || f.seg_len[s] == 0) continue;
+      std::vector<Span> sp;
+      pieces(s, f.seg_len[s], kc_shared, sp);
+      for (int g = 0; g < Hkv; ++g) {
+        std::vector<Row> rows;
+        for (int32_t r : seg_reqs[s])
+          for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0});
+        // chunk-major, row block innermost: waves that read the same pages
+        // sit next to each other (same workgroup when possible).
+        for (const Span& piece : sp)
+          for (size_t rb = 0; rb < rows.size(); rb += kRowsPerItem) {
+            Proto pr;
+            pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + kRowsPerItem));
+            pr.spans = {piece};
+            pr.kv_head = g;
+            pr.keys = piece.key_end - piece.key_begin;
+            pr.shared = true;
+            protos.push_back(std::move(pr));
+          }
+      }
+    }
+    // Suffix pass: each request's private keys, in chunks.
+    for (int r = 0; r < R; ++r) {
+      std::vector<Span> sp;
+      for (int32_t i = path_begin(r); i < path_end(r); ++i) {
+        const int32_t s = f.req_seg_ids[i];
+        if (refs[s] == 1 && f.seg_len[s] > 0) pieces(s, f.seg_len[s], kc_private, sp);
+      }
+      // pack consecutive pieces into chunks of at most kc_private keys
+      std::vector<std::vector<Span>> chunks;
+      int64_t cur = 0;
+      for (const Span& piece : sp) {
+        const int64_t n = piece.key_end - piece.key_begin;
+        if (chunks.empty() || cur + n > kc_private) {
+          chunks.emplace_back();
+          cur = 0;
+        }
+        chunks.back().push_back(piece);
+        cur += n;
+      }
+      for (int g = 0; g < Hkv; ++g)
+        for (auto& ch : chunks) {
+          int64_t keys = 0;
+          for (auto& x : ch) keys += x.key_end - x.key_begin;
+          for (int j0 = 0; j0 < G; j0 += kRowsPerItem) {
+            Proto pr;
+            for (int j = j0; j < std::min(G, j0 + kRowsPerItem); ++j)
+              pr.rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0});
+            pr.spans = ch;
+            pr.kv_head = g;
+            pr.keys = keys;
+            pr.shared = false;
+            protos.push_back(std::move(pr));
+          }
+        }
+    }
+  } else {
+    for (int r = 0; r < R; ++r) {
+      const int32_t n = f.q_len[r];
+      if (n == 0) continue;
+      const int32_t a = path_begin(r), b = path_end(r);
+      const int32_t chunk_seg = f.req_seg_ids[b - 1];
+      int64_t prefix_keys = 0;
+      std::vector<Span> prefix_spans;
+      for (int32_t i = a; i < b - 1; ++i) {
+        const int32_t s = f.req_seg_ids[i];
+        if (f.seg_len[s] > 0) prefix_spans.push_back(Span{s, 0, f.seg_len[s], 0});
+        prefix_keys += f.seg_len[s];
+      }
+      plan->visible_pairs += ((int64_t)n * prefix_keys + (int64_t)n * (n + 1) / 2) * Hq;
+      for (int g = 0; g < Hkv; ++g) {
+        std::vector<Row> rows;
+        for (int32_t i = 0; i < n; ++i)
+          for (int j = 0; j < G; ++j)
+            rows.push_back(Row{(int32_t)((tok0[r] + i) * Hq + g * G + j), i});
+        for (size_t rb = 0; rb < rows.size(); rb += kRowsPerItem) {
+          Proto pr;
+          pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + kRowsPerItem));
+          int32_t qmax = 0;
+          for (auto& x : pr.rows) qmax = std::max(qmax, x.qpos);
+          pr.spans = prefix_spans;
+          pr.spans.push_back(Span{chunk_seg, 0, std::min(n, qmax + 1), 1});
+          pr.kv_head = g;
+          pr.keys = prefix_keys + qmax + 1;
+          pr.shared = false;
+          protos.push_back(std::move(pr));
+        }
+      }
+    }
+  }
+
+  // Parts per output row; items whose rows all have a single part write
+  // their final result directly.
+  std::vector<int32_t> n_parts(n_q_rows * Hq, 0);
+  for (auto& pr : protos)
+    for (auto& row : pr.rows) n_parts[row.q_row]++;
+  std::vector<char> is_final(protos.size(), 0);
+  for (size_t i = 0; i < protos.size(); ++i) {
+    bool all_one = true;
+    for (auto& row : protos[i].rows) all_one &= (n_parts[row.q_row] == 1);
+    is_final[i] = prefill || all_one;
+  }
+
+  // Longest items first (stable: sharing neighbours stay together).
+  std::vector<size_t> order(protos.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](size_t a, size_t b) { return protos[a].keys > protos[b].keys; });
+
+  std::vector<Item> items;
+  std::vector<Span> spans;
+  std::vector<Row> rows;
+  std::vector<std::vector<int32_t>> row_parts(prefill ? 0 : n_q_rows * Hq);
+  int64_t part_rows = 0;
+  for (size_t oi : order) {
+    Proto& pr = protos[oi];
+    Item it{};
+    it.row_begin = (int32_t)rows.size();
+    it.n_rows = (int32_t)pr.rows.size();
+    it.span_begin = (int32_t)spans.size();
+    it.n_spans = (int32_t)pr.spans.size();
+    it.kv_head = pr.kv_head;
+    it.keys = (int32_t)std::min<int64_t>(pr.keys, std::numeric_limits<int32_t>::max());
+    if (is_final[oi]) {
+      it.part_base = -1;
+    } else {
+      if (part_rows + it.n_rows > (int64_t)std::numeric_limits<int32_t>::max()) {
+        delete plan;
+        return fail(HALO_ERR_INVALID_ARGUMENT, "too many partial rows");
+      }
+      it.part_base = (int32_t)part_rows;
+      for (int i = 0; i < it.n_rows; ++i) row_parts[pr.rows[i].q_row].push_back((int32_t)(part_rows + i));
+      part_rows += it.n_rows;
+    }
+    if (pr.shared) plan->n_shared_items++;
+    rows.insert(rows.end(), pr.rows.begin(), pr.rows.end());
+    spans.insert(spans.end(), pr.spans.begin(), pr.spans.end());
+    items.push_back(it);
+  }
+
+  // Merge list: every decode row no final item writes -- rows with several
+  // partials, rows whose single partial comes from an item that also holds
+  // multi-part rows, and rows with no keys at all (O = 0, LSE = -inf).
+  std::vector<int32_t> merge_rows, merge_indptr{0}, merge_parts;
+  if (!prefill) {
+    for (int64_t qr = 0; qr < n_q_rows * Hq; ++qr) {
+      if (n_parts[qr] == 1 && row_parts[qr].empty()) continue;   // written by a final item
+      merge_rows.push_back((int32_t)qr);
+      merge_parts.insert(merge_parts.end(), row_parts[qr].begin(), row_parts[qr].end());
+      merge_indptr.push_back((int32_t)merge_parts.size());
+    }
+  }
+
+  plan->n_items = (int32_t)items.size();
+  plan->n_spans = (int32_t)spans.size();
+  plan->n_rows = (int32_t)rows.size();
+  plan->n_merge_parts = (int32_t)merge_parts.size();
+  plan->n_merge = (int32_t)merge_rows.size();
+  plan->n_part_rows = part_rows;
+  const size_t D = (size_t)p.head_dim;
+  plan->workspace_bytes =
+      part_rows ? align_up(part_rows * D * sizeof(float), 256) + align_up(part_rows * sizeof(float), 256) : 0;
+
+  // Pack the device metadata image.
+  MetaLayout L;
+  size_t off = 0;
+  auto place = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  const int64_t total_pages = S ? f.seg_page_indptr[S] : 0;
+  plan->n_pages = (int32_t)total_pages;
+  L.seg_page_off = place(sizeof(int32_t) * std::max(S, 1));
+  L.seg_len = place(sizeof(int32_t) * std::max(S, 1));
+  L.page_ids = place(sizeof(int32_t) * std::max<int64_t>(total_pages, 1));
+  L.items = place(sizeof(Item) * std::max<size_t>(items.size(), 1));
+  L.spans = place(sizeof(Span) * std::max<size_t>(spans.size(), 1));
+  L.rows = place(sizeof(Row) * std::max<size_t>(rows.size(), 1));
+  L.merge_rows = place(sizeof(int32_t) * std::max<size_t>(merge_rows.size(), 1));
+  L.merge_indptr = place(sizeof(int32_t) * merge_indptr.size());
+  L.merge_parts = place(sizeof(int32_t) * std::max<size_t>(merge_parts.size(), 1));
+  L.total = off;
+  plan->layout = L;
+  plan->meta.assign(L.total, 0);
+  uint8_t* m = plan->meta.data();
+  if (S) {
+    memcpy(m + L.seg_page_off, f.seg_page_indptr, sizeof(int32_t) * S);
+    memcpy(m + L.seg_len, f.seg_len, sizeof(int32_t) * S);
+  }
+  if (total_pages) memcpy(m + L.page_ids, f.seg_page_ids, sizeof(int32_t) * total_pages);
+  if (!items.empty()) memcpy(m + L.items, items.data(), sizeof(Item) * items.size());
+  if (!spans.empty()) memcpy(m + L.spans, spans.data(), sizeof(Span) * spans.size());
+  if (!rows.empty()) memcpy(m + L.rows, rows.data(), sizeof(Row) * rows.size());
+  if (!merge_rows.empty()) memcpy(m + L.merge_rows, merge_rows.data(), sizeof(int32_t) * merge_rows.size());
+  memcpy(m + L.merge_indptr, merge_indptr.data(), sizeof(int32_t) * merge_indptr.size());
+  if (!merge_parts.empty())
+    memcpy(m + L.merge_parts, merge_parts.data(), sizeof(int32_t) * merge_parts.size());
+
+  *plan_out = plan;
+  if (device_meta_bytes) *device_meta_bytes = L.total;
+  if (workspace_bytes) *workspace_bytes = plan->workspace_bytes;
+  return HALO_OK;
+}
+
+extern "C" void halo_plan_destroy(halo_plan_t* plan) { delete plan; }
+
+extern "C" halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st) {
+  clear_error();
+  if (!plan || !st) return fail(HALO_ERR_INVALID_ARGUMENT, "plan and stats must not be NULL");
+  st->is_prefill = plan->prefill ? 1 : 0;
+  st->num_items = plan->n_items;
+  st->num_shared_items = plan->n_shared_items;
+  st->num_merge_rows = plan->n_merge;
+  st->num_partial_rows = plan->n_part_rows;
+  st->num_query_rows = plan->num_query_rows;
+  st->distinct_kv_tokens = plan->distinct_kv_tokens;
+  st->visible_pairs = plan->visible_pairs;
+  return HALO_OK;
+}
+
+extern "C" halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void** image,
+                                           halo_plan_layout_t* out) {
+  clear_error();
+  if (!plan || !image || !out) return fail(HALO_ERR_INVALID_ARGUMENT, "plan, image and layout must not be NULL");
+  const MetaLayout& L = plan->layout;
+  *image = plan->meta.data();
+  out->seg_page_off = L.seg_page_off;
+  out->seg_len = L.seg_len;
+  out->page_ids = L.page_ids;
+  out->items = L.items;
+  out->spans = L.spans;
+  out->rows = L.rows;
+  out->merge_rows = L.merge_rows;
+  out->merge_indptr = L.merge_indptr;
+  out->merge_parts = L.merge_parts;
+  out->total_bytes = L.total;
+  out->n_items = plan->n_items;
+  out->n_spans = plan->n_spans;
+  out->n_rows = plan->n_rows;
+  out->n_merge = plan->n_merge;
+  out->n_merge_parts = plan->n_merge_parts;
+  out->n_pages = plan->n_pages;
+  return HALO_OK;
+}
+
+extern "C" const char* halo_status_string(halo_status_t s) {
+  switch (s) {
+    case HALO_OK: return "HALO_OK";
+    case HALO_ERR_INVALID_ARGUMENT: return "HALO_ERR_INVALID_ARGUMENT";
+    case HALO_ERR_UNSUPPORTED: return "HALO_ERR_UNSUPPORTED";
+    case HALO_ERR_WORKSPACE_TOO_SMALL: return "HALO_ERR_WORKSPACE_TOO_SMALL";
+    case HALO_ERR_HIP: return "HALO_ERR_HIP";
+  }
+  return "HALO_ERR_UNKNOWN";
+}
+
+extern "C" const char* halo_last_error_message(void) { return halo::last_error(); }

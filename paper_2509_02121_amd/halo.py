@@ -1,0 +1,301 @@
+"""Python binding of libhalo_attn.so (ctypes; argument marshalling only).
+
+Every step of the attention path runs in the library's HIP kernels. This
+module turns torch tensors into device pointers, numpy arrays into the host
+forest, and status codes into exceptions. There is no CPU fallback: without
+the built library every call raises.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+from .build import LIB_PATH
+
+HALO_OK = 0
+HALO_ERR_INVALID_ARGUMENT = 1
+HALO_ERR_UNSUPPORTED = 2
+HALO_ERR_WORKSPACE_TOO_SMALL = 3
+HALO_ERR_HIP = 4
+
+HALO_F32 = 0
+HALO_BF16 = 1
+HALO_POOL_K = 0
+HALO_POOL_V = 1
+
+_I32P = ctypes.POINTER(ctypes.c_int32)
+
+
+class AttnParams(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_pool_pages", ctypes.c_int64), ("kv_dtype", ctypes.c_int),
+                ("out_dtype", ctypes.c_int), ("sm_scale", ctypes.c_float)]
+
+
+class Forest(ctypes.Structure):
+    _fields_ = [("num_segments", ctypes.c_int32), ("seg_len", _I32P),
+                ("seg_page_indptr", _I32P), ("seg_page_ids", _I32P),
+                ("num_requests", ctypes.c_int32), ("req_seg_indptr", _I32P),
+                ("req_seg_ids", _I32P), ("q_len", _I32P)]
+
+
+class PlanStats(ctypes.Structure):
+    _fields_ = [("is_prefill", ctypes.c_int32), ("num_items", ctypes.c_int32),
+                ("num_shared_items", ctypes.c_int32), ("num_merge_rows", ctypes.c_int32),
+                ("num_partial_rows", ctypes.c_int64), ("num_query_rows", ctypes.c_int64),
+                ("distinct_kv_tokens", ctypes.c_int64), ("visible_pairs", ctypes.c_int64)]
+
+
+class PlanLayout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in (
+        "seg_page_off", "seg_len", "page_ids", "items", "spans", "rows", "merge_rows",
+        "merge_indptr", "merge_parts", "total_bytes")] + [(n, ctypes.c_int32) for n in (
+            "n_items", "n_spans", "n_rows", "n_merge", "n_merge_parts", "n_pages")]
+
+
+EXPORTED_SYMBOLS = (
+    "halo_plan_create", "halo_plan_upload", "halo_plan_destroy", "halo_plan_get_stats",
+    "halo_plan_inspect",
+    "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_kv_page_gather",
+    "halo_status_string", "halo_last_error_message",
+)
+
+
+class HaloError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{_status_name(status)}: {message}")
+        self.status = status
+
+
+_LIB = None
+
+
+def _status_name(status):
+    names = {0: "HALO_OK", 1: "HALO_ERR_INVALID_ARGUMENT", 2: "HALO_ERR_UNSUPPORTED",
+             3: "HALO_ERR_WORKSPACE_TOO_SMALL", 4: "HALO_ERR_HIP"}
+    return names.get(status, f"status {status}")
+
+
+def _hip_runtimes_mapped():
+    try:
+        with open("/proc/self/maps") as f:
+            paths = {line.split()[-1] for line in f if "libamdhip64" in line}
+    except OSError:
+        return set()
+    return {os.path.realpath(p) for p in paths}
+
+
+def load_library(require_gpu=False):
+    """Load the built library (once). With require_gpu, torch is imported
+    first so the process maps a single HIP runtime (torch's), and a GPU must
+    be visible."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if require_gpu:
+        import torch
+        if not torch.cuda.is_available():
+            raise RuntimeError("no GPU visible to torch")
+        torch.cuda.init()
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2509_02121_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    lib.halo_plan_create.argtypes = [ctypes.POINTER(AttnParams), ctypes.POINTER(Forest),
+                                     ctypes.POINTER(vp), ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    lib.halo_plan_create.restype = ctypes.c_int
+    lib.halo_plan_upload.argtypes = [vp, vp, sz, vp]
+    lib.halo_plan_upload.restype = ctypes.c_int
+    lib.halo_plan_destroy.argtypes = [vp]
+    lib.halo_plan_destroy.restype = None
+    lib.halo_plan_get_stats.argtypes = [vp, ctypes.POINTER(PlanStats)]
+    lib.halo_plan_get_stats.restype = ctypes.c_int
+    lib.halo_plan_inspect.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(PlanLayout)]
+    lib.halo_plan_inspect.restype = ctypes.c_int
+    for name in ("halo_prefix_attn_decode", "halo_prefix_attn_prefill"):
+        fn = getattr(lib, name)
+        fn.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        fn.restype = ctypes.c_int
+    lib.halo_kv_page_gather.argtypes = [vp, ctypes.POINTER(AttnParams), ctypes.c_int, vp, vp, vp, vp,
+                                        ctypes.c_int32, vp, vp, vp]
+    lib.halo_kv_page_gather.restype = ctypes.c_int
+    lib.halo_status_string.argtypes = [ctypes.c_int]
+    lib.halo_status_string.restype = ctypes.c_char_p
+    lib.halo_last_error_message.argtypes = []
+    lib.halo_last_error_message.restype = ctypes.c_char_p
+    if require_gpu:
+        runtimes = _hip_runtimes_mapped()
+        if len(runtimes) > 1:
+            raise RuntimeError(f"several HIP runtimes mapped: {sorted(runtimes)}")
+    _LIB = lib
+    return lib
+
+
+def _check(status):
+    if status != HALO_OK:
+        msg = _LIB.halo_last_error_message().decode()
+        raise HaloError(status, msg)
+
+
+def _dtype_code(dtype):
+    import torch
+    if dtype == torch.float32:
+        return HALO_F32
+    if dtype == torch.bfloat16:
+        return HALO_BF16
+    raise ValueError(f"unsupported dtype {dtype}")
+
+
+def make_params(num_q_heads, num_kv_heads, head_dim, kv_dtype, num_pool_pages, sm_scale,
+                out_dtype=None, page_size=16):
+    """AttnParams from Python values (dtypes as torch dtypes)."""
+    return AttnParams(num_q_heads, num_kv_heads, head_dim, page_size, int(num_pool_pages),
+                      _dtype_code(kv_dtype), _dtype_code(out_dtype if out_dtype is not None else kv_dtype),
+                      float(sm_scale))
+
+
+def _i32(a):
+    return None if a is None else np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(_I32P)
+
+
+class Plan:
+    """A validated forest plus the work lists of one batch step (host)."""
+
+    def __init__(self, params, seg_len, seg_page_indptr, seg_page_ids, req_seg_indptr,
+                 req_seg_ids, q_len=None):
+        lib = load_library()
+        self.params = params
+        keep = [_i32(x) for x in (seg_len, seg_page_indptr, seg_page_ids, req_seg_indptr,
+                                  req_seg_ids, q_len)]
+        seg_len_a, indptr_a, ids_a, rindptr_a, rids_a, qlen_a = keep
+        forest = Forest(len(seg_len_a), _ptr(seg_len_a), _ptr(indptr_a), _ptr(ids_a),
+                        len(rindptr_a) - 1, _ptr(rindptr_a), _ptr(rids_a), _ptr(qlen_a))
+        handle = ctypes.c_void_p()
+        meta = ctypes.c_size_t()
+        ws = ctypes.c_size_t()
+        self._handle = None
+        _check(lib.halo_plan_create(ctypes.byref(params), ctypes.byref(forest), ctypes.byref(handle),
+                                    ctypes.byref(meta), ctypes.byref(ws)))
+        self._handle = handle
+        self._keep = keep
+        self.device_meta_bytes = meta.value
+        self.workspace_bytes = ws.value
+        self.is_prefill = q_len is not None
+
+    @classmethod
+    def from_csr(cls, params, csr):
+        return cls(params, csr["seg_len"], csr["seg_page_indptr"], csr["seg_page_ids"],
+                   csr["req_seg_indptr"], csr["req_seg_ids"], csr.get("q_len"))
+
+    def stats(self):
+        st = PlanStats()
+        _check(_LIB.halo_plan_get_stats(self._handle, ctypes.byref(st)))
+        return {f: getattr(st, f) for f, _ in PlanStats._fields_}
+
+    def inspect(self):
+        """The host metadata image decoded into numpy arrays (a copy)."""
+        img = ctypes.c_void_p()
+        lay = PlanLayout()
+        _check(_LIB.halo_plan_inspect(self._handle, ctypes.byref(img), ctypes.byref(lay)))
+        raw = np.frombuffer(ctypes.string_at(img.value, lay.total_bytes), dtype=np.uint8)
+
+        def arr(off, count, width=1):
+            a = raw[off:off + 4 * count * width].view(np.int32)
+            return a.reshape(count, width) if width > 1 else a.copy()
+
+        S = len(self._keep[0])
+        return dict(
+            seg_page_off=arr(lay.seg_page_off, S), seg_len=arr(lay.seg_len, S),
+            page_ids=arr(lay.page_ids, lay.n_pages),
+            items=arr(lay.items, lay.n_items, 8).copy(), spans=arr(lay.spans, lay.n_spans, 4).copy(),
+            rows=arr(lay.rows, lay.n_rows, 2).copy(), merge_rows=arr(lay.merge_rows, lay.n_merge),
+            merge_indptr=arr(lay.merge_indptr, lay.n_merge + 1),
+            merge_parts=arr(lay.merge_parts, lay.n_merge_parts), total_bytes=lay.total_bytes)
+
+    def upload(self, device_meta, stream=None):
+        _check(_LIB.halo_plan_upload(self._handle, device_meta.data_ptr(),
+                                     device_meta.numel() * device_meta.element_size(),
+                                     _stream_handle(stream)))
+
+    def close(self):
+        if self._handle is not None and _LIB is not None:
+            _LIB.halo_plan_destroy(self._handle)
+        self._handle = None
+
+    def __del__(self):
+        self.close()
+
+
+def _stream_handle(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _run(fn, plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream):
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(fn(plan._handle, device_meta.data_ptr(), q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(),
+              o.data_ptr(), lse.data_ptr() if lse is not None else None, ws_ptr, ws_bytes,
+              _stream_handle(stream)))
+
+
+def prefix_attn_decode(plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream=None):
+    """halo_prefix_attn_decode on torch tensors (all on one GPU)."""
+    _run(_LIB.halo_prefix_attn_decode, plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream)
+
+
+def prefix_attn_prefill(plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream=None):
+    """halo_prefix_attn_prefill on torch tensors (all on one GPU)."""
+    _run(_LIB.halo_prefix_attn_prefill, plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream)
+
+
+def kv_page_gather(pool, params, pool_kind, page_ids, seq_page_indptr, seq_len, out_token_offset,
+                   out, error_flag=None, stream=None):
+    """halo_kv_page_gather on torch tensors (int arrays on the GPU)."""
+    load_library()
+    _check(_LIB.halo_kv_page_gather(pool.data_ptr(), ctypes.byref(params), int(pool_kind),
+                                    page_ids.data_ptr(), seq_page_indptr.data_ptr(), seq_len.data_ptr(),
+                                    out_token_offset.data_ptr(), int(seq_page_indptr.numel() - 1),
+                                    out.data_ptr(),
+                                    error_flag.data_ptr() if error_flag is not None else None,
+                                    _stream_handle(stream)))
+
+
+class PrefixAttention:
+    """Plan + uploaded metadata + workspace for one forest on one GPU.
+
+    run() enqueues the whole path (attention items, then the merge) on the
+    current stream and returns (o, lse).
+    """
+
+    def __init__(self, params, csr, device="cuda"):
+        import torch
+        load_library(require_gpu=True)
+        self.plan = Plan.from_csr(params, csr)
+        self.device = torch.device(device)
+        self.meta = torch.empty(max(self.plan.device_meta_bytes, 256), dtype=torch.uint8, device=self.device)
+        self.workspace = (torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=self.device)
+                          if self.plan.workspace_bytes else None)
+        self.plan.upload(self.meta)
+        self.out_dtype = {HALO_F32: torch.float32, HALO_BF16: torch.bfloat16}[params.out_dtype]
+
+    def alloc_outputs(self, q):
+        import torch
+        o = torch.empty(q.shape, dtype=self.out_dtype, device=q.device)
+        lse = torch.empty(q.shape[:2], dtype=torch.float32, device=q.device)
+        return o, lse
+
+    def run(self, q, k_pool, v_pool, o=None, lse=None, stream=None):
+        if o is None:
+            o, lse_new = self.alloc_outputs(q)
+            lse = lse if lse is not None else lse_new
+        fn = prefix_attn_prefill if self.plan.is_prefill else prefix_attn_decode
+        fn(self.plan, self.meta, q, k_pool, v_pool, o, lse, self.workspace, stream)
+        return o, lse

@@ -1,0 +1,285 @@
+"""CPU checks of the C ABI: the library loads and exports every declared
+symbol, the header is valid C and C++, and the host planner builds work
+lists that cover every visible (row, key) pair exactly once and rejects
+malformed input with the documented status. No GPU work is launched."""
+
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2509_02121_amd import halo
+from workloads import build_workload, make_config, random_forest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "halo_attn.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return set(re.findall(r"\b(halo_[a-z_]+)\s*\(", text))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return halo.load_library()
+
+
+def test_library_exports_every_declared_symbol(lib):
+    declared = _declared_functions()
+    assert declared == set(halo.EXPORTED_SYMBOLS)
+    out = subprocess.run(["nm", "-D", "--defined-only", halo.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\b(halo_[a-z_]+)\b", out))
+    missing = declared - exported
+    assert not missing, missing
+    for name in declared:
+        assert getattr(lib, name) is not None
+
+
+@pytest.mark.parametrize("lang,std", [("c", "-std=c99"), ("c++", "-std=c++11")])
+def test_header_compiles(tmp_path, lang, std):
+    src = tmp_path / ("t.c" if lang == "c" else "t.cpp")
+    src.write_text('#include "halo_attn.h"\nint main(void){return (int)HALO_OK;}\n')
+    cc = "gcc" if lang == "c" else "g++"
+    subprocess.run([cc, std, "-Wall", "-Werror", "-pedantic", "-I", os.path.dirname(HEADER),
+                    "-fsyntax-only", str(src)], check=True)
+
+
+def test_status_strings(lib):
+    assert lib.halo_status_string(0) == b"HALO_OK"
+    assert lib.halo_status_string(3) == b"HALO_ERR_WORKSPACE_TOO_SMALL"
+
+
+# ------------------------------------------------------------------ planner
+
+def _params(w, out_dtype=None):
+    return halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages,
+                            w.scale, out_dtype)
+
+
+def _expected_intervals(w):
+    """Every (q_row, segment) a row must see, with the key count it sees
+    there (all of the segment, or up to and including its own position in
+    its prefill chunk)."""
+    hq = w.num_q_heads
+    rows, segs, his = [], [], []
+    if not w.is_prefill:
+        for r, path in enumerate(w.req_paths):
+            for s in path:
+                if w.seg_len[s] > 0:
+                    for h in range(hq):
+                        rows.append(r * hq + h); segs.append(s); his.append(int(w.seg_len[s]))
+    else:
+        tok = 0
+        for r, path in enumerate(w.req_paths):
+            n = int(w.q_len[r])
+            qrow = (tok + np.arange(n)[:, None]) * hq + np.arange(hq)[None, :]
+            for s in path[:-1]:
+                if w.seg_len[s] > 0:
+                    rows.extend(qrow.ravel().tolist()); segs.extend([s] * qrow.size)
+                    his.extend([int(w.seg_len[s])] * qrow.size)
+            rows.extend(qrow.ravel().tolist()); segs.extend([path[-1]] * qrow.size)
+            his.extend(np.repeat(np.arange(1, n + 1), hq).tolist())
+            tok += n
+    return np.array(rows, np.int64), np.array(segs, np.int64), np.array(his, np.int64)
+
+
+def _check_plan(w, plan):
+    """Decode the plan's work lists and check that, for every output row,
+    the key ranges of the items covering it tile exactly the keys the row
+    must see (each once), and that partial rows and merge lists agree."""
+    m = plan.inspect()
+    hq, hkv = w.num_q_heads, w.num_kv_heads
+    group = hq // hkv
+    items, spans, rows = m["items"], m["spans"], m["rows"]
+    for sp in spans:
+        seg, kb, ke, causal = sp
+        assert kb % 32 == 0 and 0 <= kb < ke <= w.seg_len[seg]
+    for s in range(len(w.seg_len)):
+        off = m["seg_page_off"][s]
+        assert np.array_equal(m["page_ids"][off:off + len(w.seg_pages[s])], w.seg_pages[s])
+    assert ((items[:, 1] >= 1) & (items[:, 1] <= 16) & (items[:, 3] >= 1)).all()
+    # every (item, row) pair
+    it_rep = np.repeat(np.arange(len(items)), items[:, 1])
+    row_idx = items[it_rep, 0] + (np.arange(len(it_rep)) - np.repeat(np.cumsum(items[:, 1]) - items[:, 1],
+                                                                     items[:, 1]))
+    q_row = rows[row_idx, 0].astype(np.int64)
+    qpos = rows[row_idx, 1].astype(np.int64)
+    assert ((q_row % hq) // group == items[it_rep, 4]).all(), "row outside the item's kv head"
+    part = np.where(items[it_rep, 5] >= 0, items[it_rep, 5] + (row_idx - items[it_rep, 0]), -1)
+    # every (item, row, span) interval
+    ns = items[it_rep, 3]
+    ir = np.repeat(np.arange(len(it_rep)), ns)
+    sp_idx = items[it_rep[ir], 2] + (np.arange(len(ir)) - np.repeat(np.cumsum(ns) - ns, ns))
+    seg, kb, ke, causal = (spans[sp_idx, k].astype(np.int64) for k in range(4))
+    qp = qpos[ir]
+    assert (ke[causal == 1] >= qp[causal == 1] + 1).all(), "causal span cut short"
+    hi = np.where(causal == 1, np.minimum(ke, qp + 1), ke)
+    keep = hi > kb
+    g_row, g_seg, g_lo, g_hi = q_row[ir][keep], seg[keep], kb[keep], hi[keep]
+    order = np.lexsort((g_lo, g_seg, g_row))
+    g_row, g_seg, g_lo, g_hi = g_row[order], g_seg[order], g_lo[order], g_hi[order]
+    new_group = np.ones(len(g_row), bool)
+    new_group[1:] = (g_row[1:] != g_row[:-1]) | (g_seg[1:] != g_seg[:-1])
+    assert (g_lo[new_group] == 0).all(), "a range does not start at key 0"
+    cont = ~new_group
+    assert (g_lo[1:][cont[1:]] == g_hi[:-1][cont[1:]]).all(), "gap or overlap between key ranges"
+    last = np.ones(len(g_row), bool)
+    last[:-1] = new_group[1:]
+    got = np.stack([g_row[last], g_seg[last], g_hi[last]], 1)
+    er, es, eh = _expected_intervals(w)
+    exp = np.stack([er, es, eh], 1)
+    exp = exp[np.lexsort((exp[:, 1], exp[:, 0]))]
+    assert np.array_equal(got, exp), "coverage differs from the rows' visible keys"
+    # partial rows unique; merge lists = the partials of each multiply-covered row
+    parts = part[part >= 0]
+    assert len(np.unique(parts)) == len(parts)
+    cover = np.bincount(q_row, minlength=w.q.shape[0] * hq)
+    assert (part[cover[q_row] > 1] >= 0).all(), "multiply covered rows need partials"
+    final_rows = q_row[part == -1]
+    assert (cover[final_rows] == 1).all()
+    mrows = m["merge_rows"]
+    # a row is written either by its one final item or by the merge, never both
+    assert set(mrows.tolist()) == set(range(w.q.shape[0] * hq)) - set(final_rows.tolist())
+    by_row = {}
+    for r_, p_ in zip(q_row[part >= 0].tolist(), parts.tolist()):
+        by_row.setdefault(r_, set()).add(p_)
+    for i, r_ in enumerate(mrows.tolist()):
+        got_parts = set(m["merge_parts"][m["merge_indptr"][i]:m["merge_indptr"][i + 1]].tolist())
+        assert got_parts == by_row.get(r_, set())
+    st = plan.stats()
+    assert st["visible_pairs"] == int(eh.sum())
+    assert st["num_items"] == len(items)
+    return m
+
+
+@pytest.mark.parametrize("index", [0, 1, 3])
+def test_plan_covers_configs(lib, index):
+    w = make_config(index)
+    plan = halo.Plan.from_csr(_params(w), w.forest_csr())
+    m = _check_plan(w, plan)
+    if not w.is_prefill:
+        assert plan.stats()["num_shared_items"] > 0
+        assert plan.workspace_bytes > 0
+    else:
+        assert plan.workspace_bytes == 0 and len(m["merge_rows"]) == 0
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_plan_covers_random_forests(lib, seed):
+    rng = np.random.default_rng(seed)
+    prefill = seed % 2 == 1
+    hkv = int(rng.choice([1, 2]))
+    hq = hkv * int(rng.choice([1, 2, 4, 8]))
+    seg_len, paths, q_len = random_forest(rng, int(rng.integers(1, 12)), max_len=90,
+                                          prefill=prefill, max_q=50)
+    w = build_workload("rf", seed, hq, hkv, 64, torch.float32, seg_len, paths, q_len,
+                       poison=False)
+    plan = halo.Plan.from_csr(_params(w), w.forest_csr())
+    _check_plan(w, plan)
+
+
+def test_plan_empty_batch_and_empty_segments(lib):
+    w = build_workload("e", 1, 4, 2, 64, torch.float32, [0, 0, 5], [[0, 1], [0], [2], []],
+                       poison=False)
+    plan = halo.Plan.from_csr(_params(w), w.forest_csr())
+    m = _check_plan(w, plan)
+    # requests 0, 1 and 3 see no key: their rows go through the merge with zero parts
+    for r in (0, 1, 3):
+        for h in range(4):
+            i = list(m["merge_rows"]).index(r * 4 + h)
+            assert m["merge_indptr"][i] == m["merge_indptr"][i + 1]
+
+
+def _csr(seg_len, pages, paths, q_len=None):
+    ind = np.zeros(len(seg_len) + 1, np.int32)
+    ind[1:] = np.cumsum([len(p) for p in pages])
+    rind = np.zeros(len(paths) + 1, np.int32)
+    rind[1:] = np.cumsum([len(p) for p in paths])
+    return dict(seg_len=np.array(seg_len, np.int32), seg_page_indptr=ind,
+                seg_page_ids=np.concatenate([np.array(p, np.int32) for p in pages]) if pages else
+                np.zeros(0, np.int32),
+                req_seg_indptr=rind,
+                req_seg_ids=np.concatenate([np.array(p, np.int32) for p in paths]) if paths else
+                np.zeros(0, np.int32),
+                q_len=None if q_len is None else np.array(q_len, np.int32))
+
+
+GOOD = dict(seg_len=[20, 3], pages=[[0, 1], [2]], paths=[[0, 1], [0]])
+
+
+@pytest.mark.parametrize("mutate,status,needle", [
+    (lambda p, c: setattr(p, "num_q_heads", 5), 1, "multiple"),
+    (lambda p, c: setattr(p, "head_dim", 96), 2, "head_dim"),
+    (lambda p, c: setattr(p, "page_size", 32), 2, "page_size"),
+    (lambda p, c: setattr(p, "kv_dtype", 7), 2, "kv_dtype"),
+    (lambda p, c: setattr(p, "out_dtype", 1), 2, "out_dtype"),     # bf16 out from f32 kv
+    (lambda p, c: setattr(p, "sm_scale", float("inf")), 1, "sm_scale"),
+    (lambda p, c: c["seg_page_ids"].__setitem__(1, 99), 1, "outside"),
+    (lambda p, c: c["seg_page_ids"].__setitem__(0, -1), 1, "outside"),
+    (lambda p, c: c["seg_len"].__setitem__(0, 40), 1, "needs"),
+    (lambda p, c: c["seg_len"].__setitem__(1, -2), 1, "< 0"),
+    (lambda p, c: c["req_seg_ids"].__setitem__(0, 5), 1, "outside"),
+    (lambda p, c: c["req_seg_ids"].__setitem__(1, 0), 1, "twice"),
+])
+def test_plan_rejects_malformed_input(lib, mutate, status, needle):
+    params = halo.AttnParams(4, 2, 64, 16, 3, halo.HALO_F32, halo.HALO_F32, 0.125)
+    csr = _csr(GOOD["seg_len"], GOOD["pages"], GOOD["paths"])
+    halo.Plan.from_csr(params, csr)       # the unmutated forest is accepted
+    mutate(params, csr)
+    with pytest.raises(halo.HaloError) as e:
+        halo.Plan.from_csr(params, csr)
+    assert e.value.status == status
+    assert needle in str(e.value)
+
+
+@pytest.mark.parametrize("q_len,paths,needle", [
+    ([3, 2], [[0, 1], [0, 2]], "q_len"),        # chunk 1 has 3 tokens, request 1's chunk has 2: ok
+    ([4, 2], [[0, 1], [0, 2]], "!= q_len"),
+    ([3, 2], [[0, 1], [1, 2]], "another path"),
+    ([1, 0], [[], [0, 2]], "empty path"),
+])
+def test_prefill_validation(lib, q_len, paths, needle):
+    params = halo.AttnParams(4, 2, 64, 16, 4, halo.HALO_F32, halo.HALO_F32, 0.125)
+    csr = _csr([20, 3, 2], [[0, 1], [2], [3]], paths, q_len)
+    if needle == "q_len":
+        halo.Plan.from_csr(params, csr)
+        return
+    with pytest.raises(halo.HaloError) as e:
+        halo.Plan.from_csr(params, csr)
+    assert e.value.status == 1 and needle in str(e.value)
+
+
+def test_run_calls_reject_bad_arguments_without_touching_the_gpu(lib):
+    """Argument checks fail before any HIP call (null pointers, plan kind,
+    workspace size), so they are testable on a machine with no GPU."""
+    import ctypes
+    params = halo.AttnParams(4, 2, 64, 16, 3, halo.HALO_F32, halo.HALO_F32, 0.125)
+    plan = halo.Plan.from_csr(params, _csr(GOOD["seg_len"], GOOD["pages"], GOOD["paths"]))
+    assert plan.workspace_bytes > 0
+    fake = 1 << 20      # never dereferenced: every call below fails validation first
+    rc = lib.halo_prefix_attn_prefill(plan._handle, fake, fake, fake, fake, fake, None, fake,
+                                      plan.workspace_bytes, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT
+    assert b"decode" in lib.halo_last_error_message()
+    rc = lib.halo_prefix_attn_decode(plan._handle, fake, fake, fake, fake, fake, None, fake,
+                                     plan.workspace_bytes - 1, None)
+    assert rc == halo.HALO_ERR_WORKSPACE_TOO_SMALL
+    rc = lib.halo_prefix_attn_decode(plan._handle, fake, None, fake, fake, fake, None, fake,
+                                     plan.workspace_bytes, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT
+    rc = lib.halo_prefix_attn_decode(None, fake, fake, fake, fake, fake, None, fake, 0, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT
+    rc = lib.halo_prefix_attn_decode(plan._handle, fake + 8, fake, fake, fake, fake, None, fake,
+                                     plan.workspace_bytes, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # device_meta not 256-byte aligned
+    p2 = halo.AttnParams(4, 2, 96, 16, 3, halo.HALO_F32, halo.HALO_F32, 0.125)
+    rc = lib.halo_kv_page_gather(fake, ctypes.byref(p2), 0, fake, fake, fake, fake, 1, fake, None, None)
+    assert rc == halo.HALO_ERR_UNSUPPORTED
+    rc = lib.halo_kv_page_gather(fake, ctypes.byref(params), 0, fake, fake, fake, fake, 0, fake, None, None)
+    assert rc == halo.HALO_OK      # nothing to do
