@@ -292,6 +292,23 @@ class PrefixAttention:
         lse = torch.empty(q.shape[:2], dtype=torch.float32, device=q.device)
         return o, lse
 
+    def bind(self, q, k_pool, v_pool, o, lse, stream=None):
+        """A zero-argument callable that enqueues run(q, k_pool, v_pool, o,
+        lse) with every pointer converted once (for tight timing loops).
+        The tensors must stay alive while the callable is used."""
+        fn = _LIB.halo_prefix_attn_prefill if self.plan.is_prefill else _LIB.halo_prefix_attn_decode
+        ws = self.workspace
+        args = (self.plan._handle, self.meta.data_ptr(), q.data_ptr(), k_pool.data_ptr(),
+                v_pool.data_ptr(), o.data_ptr(), lse.data_ptr() if lse is not None else None,
+                ws.data_ptr() if ws is not None else None,
+                ws.numel() if ws is not None else 0, _stream_handle(stream))
+
+        def call():
+            st = fn(*args)
+            if st != HALO_OK:
+                _check(st)
+        return call
+
     def run(self, q, k_pool, v_pool, o=None, lse=None, stream=None):
         if o is None:
             o, lse_new = self.alloc_outputs(q)
