@@ -16,8 +16,11 @@
  *   o    = sum_j softmax(s)_j v_j,   lse = ln sum_j exp(s_j)
  *   q head h reads kv head h / (num_q_heads / num_kv_heads).
  *
- * Memory layouts (all row-major, element type = kv_dtype unless stated):
- *   k_pool  [num_pool_pages][num_kv_heads][page_size][head_dim]   token-major
+ * Memory layouts (all row-major, element type = kv_dtype unless stated;
+ * E = 16 / sizeof(element): 8 for bf16, 4 for fp32):
+ *   k_pool  [num_pool_pages][num_kv_heads][head_dim/E][page_size][E]
+ *           token t, dim c of a (page, head) tile at ((c/E)*page_size + t)*E + c%E
+ *           (16-byte units, so the 16 tokens of one unit column are contiguous)
  *   v_pool  [num_pool_pages][num_kv_heads][head_dim][page_size]   dim-major
  *   q, o    decode:  [num_requests][num_q_heads][head_dim]
  *           prefill: [sum q_len][num_q_heads][head_dim], request r's rows
@@ -180,7 +183,8 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
  * each int32 array inside the image, and the element counts:
  *   items:  n_items  x {row_begin, n_rows, span_begin, n_spans, kv_head,
  *                       part_base (-1: final rows), keys, unused}
- *   spans:  n_spans  x {segment, key_begin, key_end, causal}
+ *   spans:  n_spans  x {segment, key_begin, key_end, causal, page-table offset,
+ *                       unused x 3}; a span covers at most 1024 keys
  *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position}
  *   merge_rows [n_merge], merge_indptr [n_merge + 1], merge_parts: partial
  *   row ids combined into each listed output row.

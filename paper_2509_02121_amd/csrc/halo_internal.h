@@ -30,13 +30,17 @@ struct Item {
 };
 
 // A contiguous range of keys of one segment, [key_begin, key_end).
-// key_begin is a multiple of kKeysPerStep.
+// key_begin is a multiple of kKeysPerStep and a span covers at most
+// kMaxSpanKeys keys, so its page ids fit one 64-lane register.
 struct Span {
   int32_t seg;
   int32_t key_begin;
   int32_t key_end;
   int32_t causal;      // 1: key j visible to a row iff j <= row.qpos
+  int32_t page_off;    // index in page_ids of the page holding key_begin
+  int32_t pad[3];
 };
+constexpr int kMaxSpanKeys = 1024;
 
 // One query row: its row index into q / o (token * H_q + head) and its
 // position inside the prefill chunk (for the causal span).

@@ -2,13 +2,14 @@
 //
 // attn_items_kernel: one wavefront per work item (<= 16 query rows against a
 //   list of key spans). Per step of 32 keys (two 16-token pages):
-//     S^T = K Q^T  on v_mfma_f32_16x16x32_bf16 (4 MFMAs per 16 keys at d=128)
+//     S^T = K Q^T  on v_mfma_f32_16x16x32_bf16 (one 16-key tile per page,
+//                  4 MFMAs per tile at d=128)
 //     online softmax in the log2 domain (row max / sum over the 4 lane groups)
 //     O^T += V^T P^T on the same MFMA (8 MFMAs at d=128)
-//   K tiles are token-major and V tiles dim-major in the page pools, so both
-//   MFMA A operands are one 16-byte load per lane straight from memory. Keys
-//   inside a 32-key step are permuted so that the softmax output of the QK
-//   product is already laid out as the PV B operand (no lane exchange).
+//   K pages are stored in 16-byte units ([d/E][16][E]) and V pages dim-major
+//   ([d][16]), so every MFMA A operand is a direct load from one page: 1 KB
+//   contiguous per wave for K, 512 B for V. The QK output layout is already
+//   the PV B operand (no lane exchange).
 // merge_kernel: exact log-sum-exp combination of partial results over
 //   disjoint key ranges (the merge that makes shared == unshared).
 // gather_kernel: bit copy of paged tokens into a dense token-major buffer.
@@ -49,6 +50,31 @@ __device__ __forceinline__ f32x8_t load8(const float* p) {
 }
 
 template <typename F> __device__ __forceinline__ F zero_frag() { return F{}; }
+
+// K fragment: dims d0..d0+7 of key t in a K tile stored as [D/E][16][E]
+// (E elements per 16-byte unit).
+__device__ __forceinline__ bf16x8_t load_k8(const __bf16* tile, int t, int d0) {
+  return load8(tile + ((d0 >> 3) * 16 + t) * 8);
+}
+__device__ __forceinline__ f32x8_t load_k8(const float* tile, int t, int d0) {
+  const uint4 lo = *reinterpret_cast<const uint4*>(tile + ((d0 >> 2) * 16 + t) * 4);
+  const uint4 hi = *reinterpret_cast<const uint4*>(tile + (((d0 >> 2) + 1) * 16 + t) * 4);
+  struct Pair { uint4 a, b; } v{lo, hi};
+  return __builtin_bit_cast(f32x8_t, v);
+}
+
+// V fragment: keys 4u..4u+3 of dim d from page tiles p0 (slots 0..3) and p1
+// (slots 4..7), V tiles stored dim-major as [D][16].
+__device__ __forceinline__ bf16x8_t load_v8(const __bf16* p0, const __bf16* p1, int off) {
+  const uint2 a = *reinterpret_cast<const uint2*>(p0 + off);
+  const uint2 b = *reinterpret_cast<const uint2*>(p1 + off);
+  return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
+}
+__device__ __forceinline__ f32x8_t load_v8(const float* p0, const float* p1, int off) {
+  struct Pair { uint4 a, b; } v{*reinterpret_cast<const uint4*>(p0 + off),
+                                *reinterpret_cast<const uint4*>(p1 + off)};
+  return __builtin_bit_cast(f32x8_t, v);
+}
 
 // D(16x16) += A(16x32) B(32x16). bf16: one MFMA. fp32: the same 32-deep
 // contraction as eight 16x16x4 MFMAs, slot j of every lane in the j-th one,
@@ -109,21 +135,50 @@ struct AttnArgs {
   float scale_log2;   // sm_scale * log2(e)
 };
 
+// A span's keys and its page ids, one page per lane (a span has at most 64
+// pages), so a step finds its page ids with two lane reads instead of
+// dependent memory loads.
+struct SpanState {
+  int kb, ke, causal;
+  int vpid;      // lane l: page id of the span's l-th page
+  bool valid;
+};
+
+// Position of one 32-key step.
+struct StepPos {
+  int t0;          // first key of the step (segment-local, multiple of 32)
+  int key_end;     // end of its span
+  int causal;
+  int pid0, pid1;  // page ids of the step's two pages (pid1 == pid0 if absent)
+  bool has1;
+  bool valid;
+};
+
+// Operand registers of one step: K for the two 16-key QK tiles, V^T for
+// the NB output blocks.
+template <typename F, int NS, int NB>
+struct StepRegs {
+  F k[2][NS];
+  F v[NB];
+};
+
 // One work item on one wavefront. Lane l: col = l % 16, grp = l / 16.
-//  * QK: A = K rows (A row = col), B = Q^T (B column = query row col);
-//    result lane (col, grp) holds S[row col][keys of slot j], j = 4X + i.
-//  * A 32-key step spans pages P0, P1. Slot j of lane group grp is the key
-//    16*(grp/2) + 8*(grp%2) + j of the step, so a lane's 8 V^T values are 8
-//    consecutive keys of one page (one 16-byte load), and A row r of the QK
-//    tile X is key 16*(r/8) + 8*((r/4)%2) + 4X + r%4.
-//  * PV: A = V^T rows (A row = d index col of block b), B = P^T; result lane
-//    (col, grp) holds O^T[d = 16b + 4grp + i][row col].
+//  * QK, one MFMA tile X per page of the 32-key step: A = K rows (A row =
+//    key col of page X), B = Q^T (B column = query row col); the result lane
+//    (col, grp) holds S[row col][key 16X + 4grp + i] in register i.
+//  * PV: B = P^T with slot j = 4X + i, the same key as above; A = V^T rows
+//    (A row = dim 16b + col), slot j = V[page X][key 4grp + i][dim]. The
+//    result lane (col, grp) holds O^T[d = 16b + 4grp + i][row col].
+//  * Loads are software-pipelined: the operands of step i+1 are in flight
+//    while step i is computed, and the next span's page ids are loaded when
+//    its predecessor starts.
 template <typename T, int D, typename TO>
 __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int lane) {
   using F = typename FragOf<T>::type;
   constexpr int NS = D / 32;   // QK steps over d
   constexpr int NB = D / 16;   // PV output blocks over d
   constexpr int64_t kTile = 16 * D;   // elements of one (page, head) tile
+  using Regs = StepRegs<F, NS, NB>;
   const int col = lane & 15;
   const int grp = lane >> 4;
 
@@ -140,10 +195,66 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
   const int64_t page_stride = (int64_t)a.num_kv_heads * kTile;
   const T* kbase = static_cast<const T*>(a.k_pool) + (int64_t)it.kv_head * kTile;
   const T* vbase = static_cast<const T*>(a.v_pool) + (int64_t)it.kv_head * kTile;
-  const int krow_page = col >> 3;
-  const int krow_key = ((col >> 2) & 1) * 8 + (col & 3);
-  const int slot_page = grp >> 1;
-  const int slot_key = (grp & 1) * 8;
+  const int v_off = col * 16 + 4 * grp;   // V^T[dim col][key 4grp] in a tile
+
+  auto load_span = [&](int si) {
+    SpanState st;
+    st.valid = si < it.n_spans;
+    st.kb = st.ke = st.causal = 0;
+    st.vpid = 0;
+    if (st.valid) {
+      const Span sp = a.spans[it.span_begin + si];
+      st.kb = sp.key_begin;
+      st.ke = sp.key_end;
+      st.causal = sp.causal;
+      const int np = (sp.key_end - sp.key_begin + 15) >> 4;
+      st.vpid = lane < np ? a.page_ids[sp.page_off + lane] : 0;
+    }
+    return st;
+  };
+  auto step_at = [&](const SpanState& st, int t0) {
+    StepPos p;
+    p.valid = st.valid;
+    p.t0 = t0;
+    p.key_end = st.ke;
+    p.causal = st.causal;
+    const int j = (t0 - st.kb) >> 4;
+    p.has1 = t0 + 16 < st.ke;
+    p.pid0 = __builtin_amdgcn_readlane(st.vpid, j);
+    p.pid1 = p.has1 ? __builtin_amdgcn_readlane(st.vpid, j + 1) : p.pid0;
+    return p;
+  };
+  auto fetch = [&](const StepPos& p, Regs& r) {
+    const T* k0 = kbase + (int64_t)p.pid0 * page_stride;
+    const T* k1 = kbase + (int64_t)p.pid1 * page_stride;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      r.k[0][s] = load_k8(k0, col, 32 * s + 8 * grp);
+      r.k[1][s] = load_k8(k1, col, 32 * s + 8 * grp);
+    }
+    const T* v0 = vbase + (int64_t)p.pid0 * page_stride;
+    const T* v1 = vbase + (int64_t)p.pid1 * page_stride;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) r.v[b] = load_v8(v0, v1, v_off + b * 256);
+  };
+
+  // Span cursor: cur is being walked, nxt is loaded one span ahead.
+  int si = 0;
+  SpanState cur = load_span(0);
+  SpanState nxt = load_span(1);
+  int t_next = cur.kb;   // first key of the next step to issue
+  auto advance = [&]() {
+    // position of the next step to issue, moving to the next span if needed
+    if (t_next >= cur.ke) {
+      cur = nxt;
+      ++si;
+      nxt = load_span(si + 1);
+      t_next = cur.kb;
+    }
+    StepPos p = step_at(cur, t_next);
+    t_next += kKeysPerStep;
+    return p;
+  };
 
   float m = kNegInf;
   float lsum = 0.f;
@@ -151,82 +262,72 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int si = 0; si < it.n_spans; ++si) {
-    const Span sp = a.spans[it.span_begin + si];
-    const int32_t* pids = a.page_ids + a.seg_page_off[sp.seg];
-    for (int t0 = sp.key_begin; t0 < sp.key_end; t0 += kKeysPerStep) {
-      const bool has1 = t0 + 16 < sp.key_end;
-      const int pid0 = pids[t0 >> 4];
-      const int pid1 = has1 ? pids[(t0 >> 4) + 1] : pid0;
-
-      // K operand: two 16-key tiles of this step.
-      F kf[2][NS];
-      {
-        const bool ok = krow_page == 0 || has1;
-        const int pid = krow_page ? pid1 : pid0;
-        const T* kp = kbase + (int64_t)pid * page_stride + krow_key * D + 8 * grp;
+  auto compute = [&](const StepPos& p, Regs& r) {
+    f32x4_t sacc[2];
 #pragma unroll
-        for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 2; ++x) {
+      sacc[x] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int s = 0; s < NS; ++s) kf[x][s] = ok ? load8(kp + 4 * x * D + 32 * s) : zero_frag<F>();
-      }
-      // V^T operand: rows d = 16b + col, 8 consecutive keys of one page.
-      F vf[NB];
-      {
-        const bool ok = slot_page == 0 || has1;
-        const int pid = slot_page ? pid1 : pid0;
-        const T* vp = vbase + (int64_t)pid * page_stride + col * 16 + slot_key;
+      for (int s = 0; s < NS; ++s) sacc[x] = mma(r.k[x][s], qf[s], sacc[x]);
+    }
+    // slot j = 4X + i holds key t0 + 16X + 4grp + i
+    float sv[8];
+    if (p.t0 + kKeysPerStep <= p.key_end && !p.causal) {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) vf[b] = ok ? load8(vp + b * 256) : zero_frag<F>();
-      }
-
-      f32x4_t sacc[2];
-#pragma unroll
-      for (int x = 0; x < 2; ++x) {
-        sacc[x] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < NS; ++s) sacc[x] = mma(kf[x][s], qf[s], sacc[x]);
-      }
-
-      const int key0 = t0 + 16 * slot_page + slot_key;   // key of slot 0
-      float sv[8];
-      float mt = kNegInf;
+      for (int j = 0; j < 8; ++j) sv[j] = sacc[j >> 2][j & 3] * a.scale_log2;
+    } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const int key = key0 + j;
-        const bool vis = key < sp.key_end && (!sp.causal || key <= row.qpos);
+        const int key = p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3);
+        const bool vis = key < p.key_end && (!p.causal || key <= row.qpos);
         sv[j] = vis ? sacc[j >> 2][j & 3] * a.scale_log2 : kNegInf;
-        mt = fmaxf(mt, sv[j]);
       }
-      mt = fmaxf(mt, __shfl_xor(mt, 16));
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      const float m_new = fmaxf(m, mt);
-      const float m_use = m_new == kNegInf ? 0.f : m_new;
-      const float alpha = exp2f(m - m_use);
-      float p[8];
-      float psum = 0.f;
+      // Keys past the span end may be NaN page tails (or a repeated page):
+      // zero V there, since P = 0 times NaN would still poison the sum.
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        p[j] = exp2f(sv[j] - m_use);
-        psum += p[j];
-      }
-      lsum = lsum * alpha + psum;
-      m = m_new;
-      // Keys past the span end may be NaN page tails: zero V there (P is 0,
-      // but 0 * NaN would still poison the sum).
-      if (key0 + 8 > sp.key_end) {
+      for (int j = 0; j < 8; ++j)
+        if (p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3) >= p.key_end)
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (key0 + j >= sp.key_end)
+          for (int b = 0; b < NB; ++b) r.v[b][j] = (T)0.f;
+    }
+    float mt = sv[0];
 #pragma unroll
-            for (int b = 0; b < NB; ++b) vf[b][j] = (T)0.f;
-      }
-      const F pf = to_frag(p, (F*)nullptr);
+    for (int j = 1; j < 8; ++j) mt = fmaxf(mt, sv[j]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16));
+    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    const float m_new = fmaxf(m, mt);
+    const float m_use = m_new == kNegInf ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m - m_use);
+    float pr[8];
+    float psum = 0.f;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        acc[b] *= alpha;
-        acc[b] = mma(vf[b], pf, acc[b]);
-      }
+    for (int j = 0; j < 8; ++j) {
+      pr[j] = __builtin_amdgcn_exp2f(sv[j] - m_use);
+      psum += pr[j];
+    }
+    lsum = lsum * alpha + psum;
+    m = m_new;
+    const F pf = to_frag(pr, (F*)nullptr);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      acc[b] *= alpha;
+      acc[b] = mma(r.v[b], pf, acc[b]);
+    }
+  };
+
+  if (cur.valid) {
+    Regs ra, rb;
+    StepPos pa = advance();
+    fetch(pa, ra);
+    while (true) {
+      StepPos pb = advance();
+      fetch(pb.valid ? pb : pa, rb);
+      compute(pa, ra);
+      if (!pb.valid) break;
+      pa = advance();
+      fetch(pa.valid ? pa : pb, ra);
+      compute(pb, rb);
+      if (!pa.valid) break;
     }
   }
 
@@ -322,7 +423,7 @@ struct GatherArgs {
 // unchanged.
 template <typename W>
 __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
-  __shared__ W tile[128 * 17];
+  __shared__ W tile[16 * (128 + 1)];
   const int D = a.head_dim;
   const int64_t total_tiles = (int64_t)a.seq_page_indptr[a.num_seqs] * a.num_kv_heads;
   const W* pool = static_cast<const W*>(a.pool);
@@ -346,23 +447,26 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
     const int n = min(16, len - t0);
     const int64_t out_tok = a.out_token_offset[lo] + t0;
     const W* src = pool + ((int64_t)pid * a.num_kv_heads + h) * 16 * D;
-    if (!a.v_layout) {
-      for (int e = threadIdx.x; e < n * D; e += blockDim.x) {
-        const int tok = e / D, c = e - tok * D;
-        out[((out_tok + tok) * a.num_kv_heads + h) * D + c] = src[e];
+    // Read the whole (page, head) tile coalesced, in its stored order, and
+    // place element (token t, dim c) at tile[t][c] (row stride D + 1).
+    constexpr int E = 16 / (int)sizeof(W);
+    for (int e = threadIdx.x; e < 16 * D; e += blockDim.x) {
+      int t, c;
+      if (!a.v_layout) {           // K: [D/E][16][E]
+        c = (e / (16 * E)) * E + e % E;
+        t = (e / E) % 16;
+      } else {                     // V: [D][16]
+        c = e >> 4;
+        t = e & 15;
       }
-    } else {
-      for (int e = threadIdx.x; e < 16 * D; e += blockDim.x) {
-        const int c = e >> 4, tok = e & 15;
-        tile[c * 17 + tok] = src[e];
-      }
-      __syncthreads();
-      for (int e = threadIdx.x; e < n * D; e += blockDim.x) {
-        const int tok = e / D, c = e - tok * D;
-        out[((out_tok + tok) * a.num_kv_heads + h) * D + c] = tile[c * 17 + tok];
-      }
-      __syncthreads();
+      tile[t * (D + 1) + c] = src[e];
     }
+    __syncthreads();
+    for (int e = threadIdx.x; e < n * D; e += blockDim.x) {
+      const int tok = e / D, c = e - tok * D;
+      out[((out_tok + tok) * a.num_kv_heads + h) * D + c] = tile[tok * (D + 1) + c];
+    }
+    __syncthreads();
   }
 }
 

@@ -159,7 +159,7 @@ halo_status_t validate(const halo_attn_params_t* p, const halo_forest_t* f) {
 // Split [0, len) into pieces of at most `chunk` keys (chunk % 32 == 0).
 void pieces(int32_t seg, int32_t len, int32_t chunk, std::vector<Span>& out) {
   for (int32_t kb = 0; kb < len; kb += chunk)
-    out.push_back(Span{seg, kb, std::min(len, kb + chunk), 0});
+    out.push_back(Span{seg, kb, std::min(len, kb + chunk), 0, 0, {0, 0, 0}});
 }
 
 }  // namespace
@@ -216,8 +216,8 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   std::vector<Proto> protos;
 
   if (!prefill) {
-    const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, 1 << 20) / 32 * 32;
-    const int kc_private = env_int("HALO_KC_PRIVATE", 256, 32, 1 << 20) / 32 * 32;
+    const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, kMaxSpanKeys) / 32 * 32;
+    const int kc_private = env_int("HALO_KC_PRIVATE", 256, 32, kMaxSpanKeys) / 32 * 32;
     for (int r = 0; r < R; ++r) {
       int64_t keys = 0;
       for (int32_t i = path_begin(r); i < path_end(r); ++i) keys += f.seg_len[f.req_seg_ids[i]];
@@ -294,7 +294,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       std::vector<Span> prefix_spans;
       for (int32_t i = a; i < b - 1; ++i) {
         const int32_t s = f.req_seg_ids[i];
-        if (f.seg_len[s] > 0) prefix_spans.push_back(Span{s, 0, f.seg_len[s], 0});
+        if (f.seg_len[s] > 0) prefix_spans.push_back(Span{s, 0, f.seg_len[s], 0, 0, {0, 0, 0}});
         prefix_keys += f.seg_len[s];
       }
       plan->visible_pairs += ((int64_t)n * prefix_keys + (int64_t)n * (n + 1) / 2) * Hq;
@@ -309,7 +309,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
           int32_t qmax = 0;
           for (auto& x : pr.rows) qmax = std::max(qmax, x.qpos);
           pr.spans = prefix_spans;
-          pr.spans.push_back(Span{chunk_seg, 0, std::min(n, qmax + 1), 1});
+          pr.spans.push_back(Span{chunk_seg, 0, std::min(n, qmax + 1), 1, 0, {0, 0, 0}});
           pr.kv_head = g;
           pr.keys = prefix_keys + qmax + 1;
           pr.shared = false;
@@ -348,7 +348,6 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     it.row_begin = (int32_t)rows.size();
     it.n_rows = (int32_t)pr.rows.size();
     it.span_begin = (int32_t)spans.size();
-    it.n_spans = (int32_t)pr.spans.size();
     it.kv_head = pr.kv_head;
     it.keys = (int32_t)std::min<int64_t>(pr.keys, std::numeric_limits<int32_t>::max());
     if (is_final[oi]) {
@@ -364,7 +363,16 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     }
     if (pr.shared) plan->n_shared_items++;
     rows.insert(rows.end(), pr.rows.begin(), pr.rows.end());
-    spans.insert(spans.end(), pr.spans.begin(), pr.spans.end());
+    // Split spans at kMaxSpanKeys and resolve their page-table offsets.
+    for (const Span& sp : pr.spans)
+      for (int32_t kb = sp.key_begin; kb < sp.key_end; kb += kMaxSpanKeys) {
+        Span piece = sp;
+        piece.key_begin = kb;
+        piece.key_end = std::min(sp.key_end, kb + kMaxSpanKeys);
+        piece.page_off = f.seg_page_indptr[sp.seg] + kb / p.page_size;
+        spans.push_back(piece);
+      }
+    it.n_spans = (int32_t)spans.size() - it.span_begin;
     items.push_back(it);
   }
 

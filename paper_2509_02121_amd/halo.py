@@ -213,7 +213,7 @@ class Plan:
         return dict(
             seg_page_off=arr(lay.seg_page_off, S), seg_len=arr(lay.seg_len, S),
             page_ids=arr(lay.page_ids, lay.n_pages),
-            items=arr(lay.items, lay.n_items, 8).copy(), spans=arr(lay.spans, lay.n_spans, 4).copy(),
+            items=arr(lay.items, lay.n_items, 8).copy(), spans=arr(lay.spans, lay.n_spans, 8).copy(),
             rows=arr(lay.rows, lay.n_rows, 2).copy(), merge_rows=arr(lay.merge_rows, lay.n_merge),
             merge_indptr=arr(lay.merge_indptr, lay.n_merge + 1),
             merge_parts=arr(lay.merge_parts, lay.n_merge_parts), total_bytes=lay.total_bytes)

@@ -98,8 +98,9 @@ def _check_plan(w, plan):
     group = hq // hkv
     items, spans, rows = m["items"], m["spans"], m["rows"]
     for sp in spans:
-        seg, kb, ke, causal = sp
-        assert kb % 32 == 0 and 0 <= kb < ke <= w.seg_len[seg]
+        seg, kb, ke, causal, page_off = sp[:5]
+        assert kb % 32 == 0 and 0 <= kb < ke <= w.seg_len[seg] and ke - kb <= 1024
+        assert page_off == m["seg_page_off"][seg] + kb // 16
     for s in range(len(w.seg_len)):
         off = m["seg_page_off"][s]
         assert np.array_equal(m["page_ids"][off:off + len(w.seg_pages[s])], w.seg_pages[s])

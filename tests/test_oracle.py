@@ -378,14 +378,15 @@ def test_pool_pages_hold_the_logical_tokens():
     for s in range(len(w.seg_len)):
         n = int(w.seg_len[s])
         pages = np.asarray(w.seg_pages[s])
-        k_np = np.stack([kp[pages[t // 16], :, t % 16, :] for t in range(n)])
+        k_np = np.stack([kp[pages[t // 16], :, :, t % 16, :].reshape(kp.shape[1], -1)
+                         for t in range(n)])
         v_np = np.stack([vp[pages[t // 16], :, :, t % 16] for t in range(n)])
         k, v = w.segment_kv(s)
         assert np.array_equal(k.numpy(), k_np) and np.array_equal(v.numpy(), v_np)
         assert not np.isnan(k_np).any()
         tail = n % 16
         if tail:
-            assert np.isnan(kp[pages[-1], :, tail:, :]).all()
+            assert np.isnan(kp[pages[-1], :, :, tail:, :]).all()
             assert np.isnan(vp[pages[-1], :, :, tail:]).all()
 
 
@@ -401,7 +402,7 @@ def test_page_placement_does_not_change_oracle_output():
         k, v = a.segment_kv(s)
         for t in range(seg_len[s]):
             p = int(b.seg_pages[s][t // 16])
-            b.k_pool[p, :, t % 16, :] = k[t]
+            b.k_pool[p, :, :, t % 16, :] = k[t].reshape(b.k_pool.shape[1], -1, b.k_pool.shape[-1])
             b.v_pool[p, :, :, t % 16] = v[t]
     for w in (a, b):
         w.q = a.q.clone()

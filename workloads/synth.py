@@ -7,8 +7,10 @@ replicated agentic workflows of arXiv 2509.02121 §1 and §2 ("Context reuse";
 intra-batch prefix sharing), whose KV cache is paged (§7, PagedAttention).
 
 Page pools (the layout the library reads):
-  k_pool: [P, H_kv, page_size, d]   token-major inside a (page, head) tile
-  v_pool: [P, H_kv, d, page_size]   dim-major inside a (page, head) tile
+  k_pool: [P, H_kv, d/E, page_size, E]  16-byte units of E elements (E = 8
+                                        for bf16, 4 for fp32), token-major
+                                        inside each unit column
+  v_pool: [P, H_kv, d, page_size]       dim-major inside a (page, head) tile
 Unused pages and the tail slots of a segment's last page are NaN when
 ``poison`` is set, so any read of them shows up in the results.
 
@@ -86,9 +88,9 @@ class Workload:
         """
         length = int(self.seg_len[s])
         pages = torch.as_tensor(np.asarray(self.seg_pages[s], np.int64))
-        kp = self.k_pool[pages.to(self.k_pool.device)].cpu()   # [n, H, ps, d]
+        kp = self.k_pool[pages.to(self.k_pool.device)].cpu()   # [n, H, d/E, ps, E]
         vp = self.v_pool[pages.to(self.v_pool.device)].cpu()   # [n, H, d, ps]
-        k = kp.permute(0, 2, 1, 3).reshape(-1, self.num_kv_heads, self.head_dim)
+        k = kp.permute(0, 3, 1, 2, 4).reshape(-1, self.num_kv_heads, self.head_dim)
         v = vp.permute(0, 3, 1, 2).reshape(-1, self.num_kv_heads, self.head_dim)
         return k[:length].contiguous(), v[:length].contiguous()
 
@@ -103,6 +105,11 @@ class Workload:
         """Bytes of distinct K+V tokens (each segment once)."""
         elt = torch.finfo(self.dtype).bits // 8
         return int(np.sum(self.seg_len)) * 2 * self.num_kv_heads * self.head_dim * elt
+
+
+def unit_elems(dtype):
+    """Elements per 16-byte unit of the K page layout."""
+    return 16 // torch.empty(0, dtype=dtype).element_size()
 
 
 def _fp32_scale(head_dim):
@@ -154,7 +161,8 @@ def build_workload(name, seed, num_q_heads, num_kv_heads, head_dim, dtype,
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
     h, d, ps = num_kv_heads, head_dim, page_size
-    k_pool = _fill_normal((capacity, h, ps, d), gen, device, value_scale, dtype)
+    e = unit_elems(dtype)
+    k_pool = _fill_normal((capacity, h, d // e, ps, e), gen, device, value_scale, dtype)
     v_pool = _fill_normal((capacity, h, d, ps), gen, device, value_scale, dtype)
     if q_len is None:
         rows = len(req_paths)
@@ -174,7 +182,7 @@ def build_workload(name, seed, num_q_heads, num_kv_heads, head_dim, dtype,
             tail = int(n) % ps
             if tail and n_pages[s]:
                 p = int(seg_pages[s][-1])
-                k_pool[p, :, tail:, :] = float("nan")
+                k_pool[p, :, :, tail:, :] = float("nan")
                 v_pool[p, :, :, tail:] = float("nan")
 
     return Workload(name=name, seed=int(seed), num_q_heads=num_q_heads,
