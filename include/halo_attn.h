@@ -36,8 +36,9 @@
  * Python binding). Run calls allocate nothing and enqueue work on the
  * caller's HIP stream (passed as void*, a hipStream_t); HALO_OK means
  * "validated and enqueued". A plan is host memory owned by the library from
- * halo_plan_create until halo_plan_destroy; it is immutable, so several
- * streams may run one plan concurrently if each has its own workspace.
+ * halo_plan_create until halo_plan_destroy; it is immutable, and its
+ * uploaded device_meta is only read by runs, so several streams may run one
+ * plan concurrently if each has its own workspace.
  *
  * Errors. Every call returns a halo_status_t; halo_last_error_message()
  * gives a thread-local description of the last failure. Structural checks
@@ -111,9 +112,9 @@ halo_status_t halo_plan_create(const halo_attn_params_t* params,
                                size_t* device_meta_bytes,
                                size_t* workspace_bytes);
 
-/* Copy the plan's metadata (page ids, work lists) into device_meta, a
- * caller-owned device buffer of at least device_meta_bytes, asynchronously
- * on stream. The plan must stay alive until the copy has completed. */
+/* Copy the plan's metadata (page ids, work lists) into device_meta, a caller-owned 256-byte aligned device buffer of at least
+ * device_meta_bytes, asynchronously on stream. The plan must stay alive
+ * until the copy has completed. */
 halo_status_t halo_plan_upload(const halo_plan_t* plan, void* device_meta,
                                size_t device_meta_bytes, void* stream);
 
@@ -127,7 +128,8 @@ void halo_plan_destroy(halo_plan_t* plan);
  * device_meta. Shared segments are read once per group of stacked query
  * rows (the grouped prefix pass, §2 intra-batch prefix sharing); partial
  * results over disjoint key ranges are combined with the exact log-sum-exp
- * rule, so the result equals unshared attention (§3 "Scope"). */
+ * rule, so the result equals unshared attention (§3 "Scope"). Launches:
+ * wide items (if any), narrow items, then the merge (if any rows are split). */
 halo_status_t halo_prefix_attn_decode(const halo_plan_t* plan, const void* device_meta,
                                       const void* q, const void* k_pool, const void* v_pool,
                                       void* o, float* lse,
@@ -167,13 +169,15 @@ halo_status_t halo_kv_page_gather(const void* pool, const halo_attn_params_t* pa
 /* Plan statistics for callers and benchmarks (host memory, no device work). */
 typedef struct {
   int32_t is_prefill;
-  int32_t num_items;          /* wavefront work items */
-  int32_t num_shared_items;   /* of which cover a segment shared by >= 2 requests */
+  int32_t num_items;          /* narrow work items (one wavefront, <= 16 rows) */
+  int32_t num_shared_items;   /* items (narrow or wide) over a segment shared by >= 2 requests */
   int32_t num_merge_rows;     /* output rows combined from several partials */
   int64_t num_partial_rows;   /* partial (o, lse) rows written to the workspace */
   int64_t num_query_rows;     /* rows of q / o */
   int64_t distinct_kv_tokens; /* sum of segment lengths, each segment once */
   int64_t visible_pairs;      /* sum over query rows and q heads of visible keys */
+  int32_t num_wide_items;     /* wide work items (one 4-wave workgroup, <= 256 rows) */
+  int32_t wide_row_blocks;    /* 16-row MFMA blocks per wave in wide items (0: none) */
 } halo_plan_stats_t;
 
 halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* stats);
@@ -181,18 +185,19 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
 /* Read-only view of the metadata image halo_plan_upload copies to the device,
  * for inspection and host-side testing of the work lists. Byte offsets of
  * each int32 array inside the image, and the element counts:
- *   items:  n_items  x {row_begin, n_rows, span_begin, n_spans, kv_head,
- *                       part_base (-1: final rows), keys, unused}
+ *   items, wide_items: n_items / n_wide x {row_begin, n_rows, span_begin,
+ *                       n_spans, kv_head, part_base (-1: final rows), keys, unused}
  *   spans:  n_spans  x {segment, key_begin, key_end, causal, page-table offset,
  *                       unused x 3}; a span covers at most 1024 keys
- *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position}
+ *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position,
+ *                       merge entry or -1, unused}
  *   merge_rows [n_merge], merge_indptr [n_merge + 1], merge_parts: partial
  *   row ids combined into each listed output row.
  * *image stays valid until halo_plan_destroy. */
 typedef struct {
-  uint64_t seg_page_off, seg_len, page_ids, items, spans, rows;
+  uint64_t seg_page_off, seg_len, page_ids, items, wide_items, spans, rows;
   uint64_t merge_rows, merge_indptr, merge_parts, total_bytes;
-  int32_t n_items, n_spans, n_rows, n_merge, n_merge_parts, n_pages;
+  int32_t n_items, n_wide, n_spans, n_rows, n_merge, n_merge_parts, n_pages;
 } halo_plan_layout_t;
 
 halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void** image,

@@ -12,6 +12,8 @@ namespace halo {
 
 // Rows of one wavefront work item: at most 16 query rows (one MFMA N tile).
 constexpr int kRowsPerItem = 16;
+// A wide item holds up to 4 waves x wide_rb row blocks x 16 rows.
+constexpr int kMaxWideRows = 256;
 // Keys consumed per inner step: two pages of 16 (one K=32 MFMA for P*V).
 constexpr int kKeysPerStep = 32;
 
@@ -42,11 +44,15 @@ struct Span {
 };
 constexpr int kMaxSpanKeys = 1024;
 
-// One query row: its row index into q / o (token * H_q + head) and its
-// position inside the prefill chunk (for the causal span).
+// One query row: its row index into q / o (token * H_q + head), its
+// position inside the prefill chunk (for the causal span) and, for a row
+// whose keys are split over several items, its merge-list entry.
 struct Row {
   int32_t q_row;
   int32_t qpos;
+  int32_t merge_idx;   // entry in the merge list, or -1 when the row is final here
+                       // (inspection only; the merge kernel walks the list)
+  int32_t pad;
 };
 
 // Offsets (bytes) of the arrays packed in the device metadata buffer.
@@ -54,7 +60,8 @@ struct MetaLayout {
   size_t seg_page_off = 0;   // int32 [S]  first page slot of each segment
   size_t seg_len = 0;        // int32 [S]
   size_t page_ids = 0;       // int32 [total pages]
-  size_t items = 0;          // Item  [n_items]
+  size_t items = 0;          // Item  [n_items]     narrow (one wavefront)
+  size_t wide_items = 0;     // Item  [n_wide]      wide (one 4-wave workgroup)
   size_t spans = 0;          // Span  [n_spans]
   size_t rows = 0;           // Row   [n_rows]
   size_t merge_rows = 0;     // int32 [n_merge] output row (q_row) per merge entry
@@ -72,6 +79,8 @@ struct halo_plan {
   int32_t num_requests = 0;
   int64_t num_query_rows = 0;
   int32_t n_items = 0;
+  int32_t n_wide = 0;
+  int32_t wide_rb = 0;       // MFMA row blocks per wave in wide items (1, 2, 4)
   int32_t n_shared_items = 0;
   int32_t n_merge = 0;
   int32_t n_spans = 0;

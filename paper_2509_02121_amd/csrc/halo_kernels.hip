@@ -11,7 +11,10 @@
 //   contiguous per wave for K, 512 B for V. The QK output layout is already
 //   the PV B operand (no lane exchange).
 // merge_kernel: exact log-sum-exp combination of partial results over
-//   disjoint key ranges (the merge that makes shared == unshared).
+//   disjoint key ranges (the merge that makes shared == unshared), in its own
+//   launch so the kernel boundary makes every partial visible (an in-kernel
+//   last-arriver merge needs agent-scope release/acquire, i.e. L2
+//   write-back and invalidate, which measured 4x slower on this path).
 // gather_kernel: bit copy of paged tokens into a dense token-major buffer.
 
 #include <hip/hip_runtime.h>
@@ -28,6 +31,8 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLn2 = 0.69314718055994530942f;
@@ -41,12 +46,10 @@ template <> struct FragOf<__bf16> { using type = bf16x8_t; };
 template <> struct FragOf<float> { using type = f32x8_t; };
 
 __device__ __forceinline__ bf16x8_t load8(const __bf16* p) {
-  return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
+  return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4_t*>(p));
 }
 __device__ __forceinline__ f32x8_t load8(const float* p) {
-  const uint4* q = reinterpret_cast<const uint4*>(p);
-  struct Pair { uint4 a, b; } v{q[0], q[1]};
-  return __builtin_bit_cast(f32x8_t, v);
+  return *reinterpret_cast<const f32x8_t*>(p);
 }
 
 template <typename F> __device__ __forceinline__ F zero_frag() { return F{}; }
@@ -57,23 +60,24 @@ __device__ __forceinline__ bf16x8_t load_k8(const __bf16* tile, int t, int d0) {
   return load8(tile + ((d0 >> 3) * 16 + t) * 8);
 }
 __device__ __forceinline__ f32x8_t load_k8(const float* tile, int t, int d0) {
-  const uint4 lo = *reinterpret_cast<const uint4*>(tile + ((d0 >> 2) * 16 + t) * 4);
-  const uint4 hi = *reinterpret_cast<const uint4*>(tile + (((d0 >> 2) + 1) * 16 + t) * 4);
-  struct Pair { uint4 a, b; } v{lo, hi};
-  return __builtin_bit_cast(f32x8_t, v);
+  typedef float f32x4v __attribute__((ext_vector_type(4)));
+  const f32x4v lo = *reinterpret_cast<const f32x4v*>(tile + ((d0 >> 2) * 16 + t) * 4);
+  const f32x4v hi = *reinterpret_cast<const f32x4v*>(tile + (((d0 >> 2) + 1) * 16 + t) * 4);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // V fragment: keys 4u..4u+3 of dim d from page tiles p0 (slots 0..3) and p1
 // (slots 4..7), V tiles stored dim-major as [D][16].
 __device__ __forceinline__ bf16x8_t load_v8(const __bf16* p0, const __bf16* p1, int off) {
-  const uint2 a = *reinterpret_cast<const uint2*>(p0 + off);
-  const uint2 b = *reinterpret_cast<const uint2*>(p1 + off);
-  return __builtin_bit_cast(bf16x8_t, make_uint4(a.x, a.y, b.x, b.y));
+  const u32x2_t a = *reinterpret_cast<const u32x2_t*>(p0 + off);
+  const u32x2_t b = *reinterpret_cast<const u32x2_t*>(p1 + off);
+  return __builtin_bit_cast(bf16x8_t, u32x4_t{a.x, a.y, b.x, b.y});
 }
 __device__ __forceinline__ f32x8_t load_v8(const float* p0, const float* p1, int off) {
-  struct Pair { uint4 a, b; } v{*reinterpret_cast<const uint4*>(p0 + off),
-                                *reinterpret_cast<const uint4*>(p1 + off)};
-  return __builtin_bit_cast(f32x8_t, v);
+  typedef float f32x4v __attribute__((ext_vector_type(4)));
+  const f32x4v lo = *reinterpret_cast<const f32x4v*>(p0 + off);
+  const f32x4v hi = *reinterpret_cast<const f32x4v*>(p1 + off);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // D(16x16) += A(16x32) B(32x16). bf16: one MFMA. fp32: the same 32-deep
@@ -127,10 +131,12 @@ struct AttnArgs {
   const int32_t* seg_page_off;
   const int32_t* seg_len;
   const int32_t* page_ids;
-  const Item* items;
+  const Item* items;        // narrow items (one wavefront each)
+  const Item* wide_items;   // wide items (one 4-wave workgroup each)
   const Span* spans;
   const Row* rows;
   int32_t n_items;
+  int32_t n_wide;
   int32_t num_kv_heads;
   float scale_log2;   // sm_scale * log2(e)
 };
@@ -153,6 +159,20 @@ struct StepPos {
   bool has1;
   bool valid;
 };
+
+// Field-wise choice between two step positions (a conditional on the
+// structs themselves would select their addresses and keep them in memory).
+__device__ __forceinline__ StepPos pick(bool c, const StepPos& x, const StepPos& y) {
+  StepPos r;
+  r.t0 = c ? x.t0 : y.t0;
+  r.key_end = c ? x.key_end : y.key_end;
+  r.causal = c ? x.causal : y.causal;
+  r.pid0 = c ? x.pid0 : y.pid0;
+  r.pid1 = c ? x.pid1 : y.pid1;
+  r.has1 = c ? x.has1 : y.has1;
+  r.valid = c ? x.valid : y.valid;
+  return r;
+}
 
 // Operand registers of one step: K for the two 16-key QK tiles, V^T for
 // the NB output blocks.
@@ -182,7 +202,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
   const int col = lane & 15;
   const int grp = lane >> 4;
 
-  Row row{-1, 0};
+  Row row{-1, 0, -1, 0};
   if (col < it.n_rows) row = a.rows[it.row_begin + col];
 
   F qf[NS];
@@ -321,11 +341,11 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
     fetch(pa, ra);
     while (true) {
       StepPos pb = advance();
-      fetch(pb.valid ? pb : pa, rb);
+      fetch(pick(pb.valid, pb, pa), rb);
       compute(pa, ra);
       if (!pb.valid) break;
       pa = advance();
-      fetch(pa.valid ? pa : pb, ra);
+      fetch(pick(pa.valid, pa, pb), ra);
       compute(pb, rb);
       if (!pa.valid) break;
     }
@@ -333,16 +353,18 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
 
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
-  if (col >= it.n_rows) return;
+  const bool has_row = col < it.n_rows;
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   const float lse2 = lsum > 0.f ? m + __log2f(lsum) : kNegInf;
   if (it.part_base >= 0) {
-    const int64_t prow = (int64_t)it.part_base + col;
-    float* dst = a.part_o + prow * D + 4 * grp;
+    if (has_row) {
+      const int64_t prow = (int64_t)it.part_base + col;
+      float* dst = a.part_o + prow * D + 4 * grp;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[b] * inv);
-    if (grp == 0) a.part_lse[prow] = lse2;
-  } else {
+      for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[b] * inv);
+      if (grp == 0) a.part_lse[prow] = lse2;
+    }
+  } else if (has_row) {
     TO* dst = static_cast<TO*>(a.o) + (int64_t)row.q_row * D + 4 * grp;
 #pragma unroll
     for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[b] * inv);
@@ -351,11 +373,260 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
 }
 
 template <typename T, int D, typename TO>
-__global__ __launch_bounds__(256) void attn_items_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_items_kernel(AttnArgs a) {
   const int item_id = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
   if (item_id >= a.n_items) return;
   const Item it = a.items[item_id];
   run_item<T, D, TO>(a, it, threadIdx.x & 63);
+}
+
+
+// ---------------------------------------------------------------- wide items
+// A wide item holds up to 4 * RB * 16 query rows of one kv head against a
+// span list: a workgroup of 4 waves, RB MFMA row blocks per wave, all rows
+// sharing the key stream. Each 32-key step's four tiles (K and V of its two
+// pages) are read once per workgroup with coalesced 16-byte loads, two steps
+// ahead through registers, into an LDS double buffer; every wave then reads
+// its MFMA operands from LDS (1 KB contiguous per K read, 512 B per V read).
+// Used for the grouped prefix pass (many rows share one segment, §2
+// intra-batch prefix sharing) and for chunked prefill (§4.1).
+//
+// Softmax rescaling is lazy: a row's reference maximum only moves when a
+// step's maximum exceeds it by more than kRescaleLog2 (so weights stay below
+// 2^kRescaleLog2); the result is the same softmax, and the accumulator
+// rescale runs only on the rare steps where some row moves.
+constexpr float kRescaleLog2 = 8.f;
+
+template <int D>
+struct WideGeom {
+  static constexpr int kTileBytes = 16 * D * 2;           // one bf16 (page, head) tile
+  static constexpr int kStepBytes = 4 * kTileBytes;       // K page0, K page1, V page0, V page1
+  static constexpr int kChunksPerTile = kTileBytes / 16;  // 16-byte chunks
+  static constexpr int kPerThread = 4 * kChunksPerTile / 256;
+};
+
+template <int D, int RB, typename TO>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(RB >= 4 ? 1 : 2)))
+void attn_wide_kernel(AttnArgs a) {
+  using T = __bf16;
+  using F = bf16x8_t;
+  using G = WideGeom<D>;
+  constexpr int NS = D / 32;
+  constexpr int NB = D / 16;
+  constexpr int64_t kTile = 16 * D;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * G::kStepBytes];
+
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 15;
+  const int grp = lane >> 4;
+  const int item_id = blockIdx.x;
+  if (item_id >= a.n_wide) return;
+  const Item it = a.wide_items[item_id];
+
+  // This lane's rows: row block rb of this wave, column col.
+  Row row[RB];
+  F qf[RB][NS];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = (wave * RB + rb) * 16 + col;
+    row[rb] = r < it.n_rows ? a.rows[it.row_begin + r] : Row{-1, 0, -1, 0};
+    const T* qp = static_cast<const T*>(a.q) + (int64_t)(row[rb].q_row < 0 ? 0 : row[rb].q_row) * D + 8 * grp;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qf[rb][s] = row[rb].q_row >= 0 ? load8(qp + 32 * s) : zero_frag<F>();
+  }
+
+  const int64_t page_stride = (int64_t)a.num_kv_heads * kTile;
+  const T* kbase = static_cast<const T*>(a.k_pool) + (int64_t)it.kv_head * kTile;
+  const T* vbase = static_cast<const T*>(a.v_pool) + (int64_t)it.kv_head * kTile;
+
+  // ---- span cursor (identical, wave-uniform, in every wave)
+  auto load_span = [&](int si) {
+    SpanState st;
+    st.valid = si < it.n_spans;
+    st.kb = st.ke = st.causal = 0;
+    st.vpid = 0;
+    if (st.valid) {
+      const Span sp = a.spans[it.span_begin + si];
+      st.kb = sp.key_begin;
+      st.ke = sp.key_end;
+      st.causal = sp.causal;
+      const int np = (sp.key_end - sp.key_begin + 15) >> 4;
+      st.vpid = lane < np ? a.page_ids[sp.page_off + lane] : 0;
+    }
+    return st;
+  };
+  int si = 0;
+  SpanState cur = load_span(0);
+  SpanState nxt = load_span(1);
+  int t_next = cur.kb;
+  auto advance = [&]() {
+    if (t_next >= cur.ke) {
+      cur = nxt;
+      ++si;
+      nxt = load_span(si + 1);
+      t_next = cur.kb;
+    }
+    StepPos p;
+    p.valid = cur.valid;
+    p.t0 = t_next;
+    p.key_end = cur.ke;
+    p.causal = cur.causal;
+    const int j = (t_next - cur.kb) >> 4;
+    p.has1 = t_next + 16 < cur.ke;
+    p.pid0 = __builtin_amdgcn_readlane(cur.vpid, j);
+    p.pid1 = p.has1 ? __builtin_amdgcn_readlane(cur.vpid, j + 1) : p.pid0;
+    t_next += kKeysPerStep;
+    return p;
+  };
+
+  // ---- staging: thread t moves chunks t + 256k of the step (k < kPerThread)
+  struct Stage { u32x4_t v[G::kPerThread]; };
+  auto stage_load = [&](const StepPos& p, Stage& st) {
+#pragma unroll
+    for (int k = 0; k < G::kPerThread; ++k) {
+      const int c = threadIdx.x + 256 * k;
+      const int tile = c / G::kChunksPerTile;        // 0,1: K pages; 2,3: V pages
+      const int off = (c % G::kChunksPerTile) * 8;   // elements
+      const int pid = (tile & 1) ? p.pid1 : p.pid0;
+      const T* src = ((tile < 2) ? kbase : vbase) + (int64_t)pid * page_stride + off;
+      st.v[k] = *reinterpret_cast<const u32x4_t*>(src);
+    }
+  };
+  auto stage_write = [&](const Stage& st, int buf) {
+#pragma unroll
+    for (int k = 0; k < G::kPerThread; ++k) {
+      const int c = threadIdx.x + 256 * k;
+      *reinterpret_cast<u32x4_t*>(lds + buf * G::kStepBytes + c * 16) = st.v[k];
+    }
+  };
+
+  float m[RB], lsum[RB];
+  f32x4_t acc[RB][NB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    m[rb] = kNegInf;
+    lsum[rb] = 0.f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[rb][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto compute = [&](const StepPos& p, int buf) {
+    const uint8_t* base = lds + buf * G::kStepBytes;
+    f32x4_t sacc[RB][2];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) sacc[rb][0] = sacc[rb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const F kf = __builtin_bit_cast(
+            F, *reinterpret_cast<const u32x4_t*>(base + x * G::kTileBytes + ((4 * s + grp) * 16 + col) * 16));
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) sacc[rb][x] = mma(kf, qf[rb][s], sacc[rb][x]);
+      }
+    const bool full = p.t0 + kKeysPerStep <= p.key_end && !p.causal;
+    F pf[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float sv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int key = p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3);
+        const bool vis = full || (key < p.key_end && (!p.causal || key <= row[rb].qpos));
+        sv[j] = vis ? sacc[rb][j >> 2][j & 3] * a.scale_log2 : kNegInf;
+      }
+      float mt = sv[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) mt = fmaxf(mt, sv[j]);
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const bool move = mt > m[rb] + kRescaleLog2;
+      if (__any(move)) {
+        const float m_new = move ? mt : m[rb];
+        const float alpha = m[rb] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[rb] - m_new);
+        lsum[rb] *= alpha;
+#pragma unroll
+        for (int b = 0; b < NB; ++b) acc[rb][b] *= alpha;
+        m[rb] = m_new;
+      }
+      const float m_use = m[rb] == kNegInf ? 0.f : m[rb];
+      float pr[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        pr[j] = __builtin_amdgcn_exp2f(sv[j] - m_use);
+        lsum[rb] += pr[j];
+      }
+      pf[rb] = to_frag(pr, (F*)nullptr);
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int voff = ((16 * b + col) * 16 + 4 * grp) * 2;
+      const u32x2_t v0 = *reinterpret_cast<const u32x2_t*>(base + 2 * G::kTileBytes + voff);
+      const u32x2_t v1 = *reinterpret_cast<const u32x2_t*>(base + 3 * G::kTileBytes + voff);
+      F vf = __builtin_bit_cast(F, u32x4_t{v0.x, v0.y, v1.x, v1.y});
+      if (!full) {
+        // keys past the span end may be NaN page tails: zero V there
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3) >= p.key_end) vf[j] = (T)0.f;
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[rb][b] = mma(vf, pf[rb], acc[rb][b]);
+    }
+  };
+
+  // ---- pipeline: LDS buffers 0/1, register stages r0/r1, two steps ahead
+  StepPos p0 = advance();
+  StepPos p1 = advance();
+  if (p0.valid) {
+    Stage r0, r1;
+    stage_load(p0, r0);
+    stage_load(pick(p1.valid, p1, p0), r1);
+    stage_write(r0, 0);
+    __syncthreads();
+    while (true) {
+      StepPos p2 = advance();
+      stage_load(pick(p2.valid, p2, p0), r0);
+      compute(p0, 0);
+      if (!p1.valid) break;
+      stage_write(r1, 1);
+      __syncthreads();
+      StepPos p3 = advance();
+      stage_load(pick(p3.valid, p3, p1), r1);
+      compute(p1, 1);
+      if (!p2.valid) break;
+      stage_write(r0, 0);
+      __syncthreads();
+      p0 = p2;
+      p1 = p3;
+    }
+  }
+
+  // ---- epilogue
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    float l = lsum[rb];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    const int r = (wave * RB + rb) * 16 + col;
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    const float lse2 = l > 0.f ? m[rb] + __log2f(l) : kNegInf;
+    if (it.part_base >= 0) {
+      if (r < it.n_rows) {
+        const int64_t prow = (int64_t)it.part_base + r;
+        float* dst = a.part_o + prow * D + 4 * grp;
+#pragma unroll
+        for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[rb][b] * inv);
+        if (grp == 0) a.part_lse[prow] = lse2;
+      }
+    } else if (r < it.n_rows) {
+      TO* dst = static_cast<TO*>(a.o) + (int64_t)row[rb].q_row * D + 4 * grp;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[rb][b] * inv);
+      if (grp == 0 && a.lse) a.lse[row[rb].q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- merge
@@ -371,30 +642,56 @@ struct MergeArgs {
   int32_t n_merge;
 };
 
-// Rows with several partials (o_i normalized, lse_i in log2):
-//   M = max_i lse_i, w_i = 2^(lse_i - M), O = sum w_i o_i / sum w_i,
-//   LSE = (M + log2 sum w_i) * ln 2.  Rows with no parts: O = 0, LSE = -inf.
+// Output rows whose keys were split over several items. Partials hold the
+// normalized o_i and lse_i (log2) of disjoint key sets:
+//   M = max_i lse_i,  w_i = 2^(lse_i - M),  O = sum w_i o_i / sum w_i,
+//   LSE = (M + log2 sum w_i) * ln 2
+// which is exact in real arithmetic (shared == unshared, §3 "Scope"). One
+// group of D/4 threads per row, 4 dims per thread; the partial ids and
+// LSEs of up to 8 parts are fetched together so the loads overlap.
 template <int D, typename TO>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
   constexpr int TPR = D / 4;
   constexpr int RPB = 256 / TPR;
+  constexpr int kBatch = 8;
   const int r = blockIdx.x * RPB + threadIdx.x / TPR;
   const int t = threadIdx.x % TPR;
   if (r >= a.n_merge) return;
   const int q_row = a.merge_rows[r];
   const int p0 = a.merge_indptr[r], p1 = a.merge_indptr[r + 1];
   float mx = kNegInf;
-  for (int p = p0; p < p1; ++p) mx = fmaxf(mx, a.part_lse[a.merge_parts[p]]);
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  if (mx != kNegInf) {
-    for (int p = p0; p < p1; ++p) {
-      const int pr = a.merge_parts[p];
-      const float w = exp2f(a.part_lse[pr] - mx);
-      const float4 v = *reinterpret_cast<const float4*>(a.part_o + (int64_t)pr * D + 4 * t);
-      wsum += w;
-      acc += w * f32x4_t{v.x, v.y, v.z, v.w};
+  // online over batches of parts: rescale when the running max moves
+  for (int pb = p0; pb < p1; pb += kBatch) {
+    int pid[kBatch];
+    float l[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) pid[k] = pb + k < p1 ? a.merge_parts[pb + k] : -1;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) l[k] = pid[k] >= 0 ? a.part_lse[pid[k]] : kNegInf;
+    f32x4_t v[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const float4 x = pid[k] >= 0 ? *reinterpret_cast<const float4*>(a.part_o + (int64_t)pid[k] * D + 4 * t)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+      v[k] = f32x4_t{x.x, x.y, x.z, x.w};
     }
+    float bm = kNegInf;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) bm = fmaxf(bm, l[k]);
+    const float m_new = fmaxf(mx, bm);
+    if (m_new == kNegInf) continue;
+    const float alpha = mx == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mx - m_new);
+    acc *= alpha;
+    wsum *= alpha;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const float w = __builtin_amdgcn_exp2f(l[k] - m_new);   // 0 for absent parts
+      wsum += w;
+      acc += w * v[k];
+    }
+    mx = m_new;
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 4 * t, acc * inv);
@@ -482,8 +779,18 @@ halo_status_t hip_check(const char* what) {
   return HALO_OK;
 }
 
+template <int D, typename TO>
+void launch_wide(const AttnArgs& args, int rb, hipStream_t stream) {
+  if (rb == 1) hipLaunchKernelGGL((attn_wide_kernel<D, 1, TO>), dim3(args.n_wide), dim3(256), 0, stream, args);
+  else if (rb == 2) hipLaunchKernelGGL((attn_wide_kernel<D, 2, TO>), dim3(args.n_wide), dim3(256), 0, stream, args);
+  else hipLaunchKernelGGL((attn_wide_kernel<D, 4, TO>), dim3(args.n_wide), dim3(256), 0, stream, args);
+}
+
 template <typename T, int D, typename TO>
-void launch_attention(const AttnArgs& args, const MergeArgs& margs, hipStream_t stream) {
+void launch_attention(const AttnArgs& args, const MergeArgs& margs, int wide_rb, hipStream_t stream) {
+  if (args.n_wide > 0) {
+    if constexpr (sizeof(T) == 2) launch_wide<D, TO>(args, wide_rb, stream);
+  }
   if (args.n_items > 0) {
     const int blocks = (args.n_items + 3) / 4;
     hipLaunchKernelGGL((attn_items_kernel<T, D, TO>), dim3(blocks), dim3(256), 0, stream, args);
@@ -528,9 +835,10 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                 reinterpret_cast<const int32_t*>(m + L.seg_len),
                 reinterpret_cast<const int32_t*>(m + L.page_ids),
                 reinterpret_cast<const Item*>(m + L.items),
+                reinterpret_cast<const Item*>(m + L.wide_items),
                 reinterpret_cast<const Span*>(m + L.spans),
                 reinterpret_cast<const Row*>(m + L.rows),
-                plan->n_items, p.num_kv_heads, p.sm_scale * kLog2e};
+                plan->n_items, plan->n_wide, p.num_kv_heads, p.sm_scale * kLog2e};
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),
                   reinterpret_cast<const int32_t*>(m + L.merge_indptr),
@@ -541,15 +849,15 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
   const bool out_f32 = p.out_dtype == HALO_F32;
   if (p.kv_dtype == HALO_BF16) {
     if (D == 128) {
-      if (out_f32) launch_attention<__bf16, 128, float>(args, margs, st);
-      else launch_attention<__bf16, 128, __bf16>(args, margs, st);
+      if (out_f32) launch_attention<__bf16, 128, float>(args, margs, plan->wide_rb, st);
+      else launch_attention<__bf16, 128, __bf16>(args, margs, plan->wide_rb, st);
     } else {
-      if (out_f32) launch_attention<__bf16, 64, float>(args, margs, st);
-      else launch_attention<__bf16, 64, __bf16>(args, margs, st);
+      if (out_f32) launch_attention<__bf16, 64, float>(args, margs, plan->wide_rb, st);
+      else launch_attention<__bf16, 64, __bf16>(args, margs, plan->wide_rb, st);
     }
   } else {
-    if (D == 128) launch_attention<float, 128, float>(args, margs, st);
-    else launch_attention<float, 64, float>(args, margs, st);
+    if (D == 128) launch_attention<float, 128, float>(args, margs, plan->wide_rb, st);
+    else launch_attention<float, 64, float>(args, margs, plan->wide_rb, st);
   }
   return hip_check("attention launch");
 }

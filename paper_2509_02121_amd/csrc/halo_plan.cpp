@@ -212,6 +212,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     int32_t kv_head;
     int64_t keys;
     bool shared;
+    bool wide;
   };
   std::vector<Proto> protos;
 
@@ -223,28 +224,68 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       for (int32_t i = path_begin(r); i < path_end(r); ++i) keys += f.seg_len[f.req_seg_ids[i]];
       plan->visible_pairs += keys * Hq;
     }
-    // Grouped prefix pass: shared segments, all their rows stacked.
+    // Grouped prefix pass: shared segments, all their rows stacked. With
+    // bf16 inputs the rows go to wide items (a 4-wave workgroup reading each
+    // page once for up to 256 rows); the row-block count per wave follows the
+    // row-weighted size of the shared groups, and the key chunk shrinks until
+    // there are enough workgroups to cover the GPU.
     std::vector<std::vector<int32_t>> seg_reqs(S);
     for (int r = 0; r < R; ++r)
       for (int32_t i = path_begin(r); i < path_end(r); ++i) seg_reqs[f.req_seg_ids[i]].push_back(r);
+    // Wide items pay off once the shared work is large: below ~16M
+    // (row, key) pairs the grouped pass is a small fraction of the call and
+    // narrow items (more of them, no LDS barriers) finish sooner.
+    double shared_work = 0, wsum = 0, wrows = 0;
+    for (int s = 0; s < S; ++s)
+      if (refs[s] >= 2 && f.seg_len[s] > 0) {
+        const double w = (double)f.seg_len[s] * refs[s];
+        shared_work += w * G * Hkv;
+        wsum += w;
+        wrows += w * (double)refs[s] * G;
+      }
+    const int wide_env = env_int("HALO_WIDE", -1, 0, 1);
+    const bool wide = p.kv_dtype == HALO_BF16 &&
+                      (wide_env == 1 || (wide_env == -1 && shared_work >= 16.0 * (1 << 20)));
+    int rows_per = kRowsPerItem;
+    int kc = kc_shared;
+    if (wide) {
+      const double avg_rows = wsum > 0 ? wrows / wsum : 0;
+      int rb = avg_rows >= 128 ? 2 : 1;
+      rb = env_int("HALO_WIDE_RB", rb, 1, 4);
+      if (rb == 3) rb = 4;
+      plan->wide_rb = rb;
+      rows_per = 64 * rb;
+      const int min_items = env_int("HALO_WIDE_MIN_ITEMS", 512, 1, 1 << 30);
+      kc = kMaxSpanKeys;
+      while (kc > 128) {
+        int64_t n = 0;
+        for (int s = 0; s < S; ++s)
+          if (refs[s] >= 2 && f.seg_len[s] > 0)
+            n += ceil_div(f.seg_len[s], kc) * ceil_div((int64_t)refs[s] * G, rows_per) * Hkv;
+        if (n >= min_items) break;
+        kc /= 2;
+      }
+      kc = env_int("HALO_KC_WIDE", kc, 32, kMaxSpanKeys) / 32 * 32;
+    }
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
       std::vector<Span> sp;
-      pieces(s, f.seg_len[s], kc_shared, sp);
+      pieces(s, f.seg_len[s], kc, sp);
       for (int g = 0; g < Hkv; ++g) {
         std::vector<Row> rows;
         for (int32_t r : seg_reqs[s])
-          for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0});
-        // chunk-major, row block innermost: waves that read the same pages
-        // sit next to each other (same workgroup when possible).
+          for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, 0});
+        // chunk-major, row group innermost: items reading the same pages
+        // are neighbours in the launch order.
         for (const Span& piece : sp)
-          for (size_t rb = 0; rb < rows.size(); rb += kRowsPerItem) {
+          for (size_t rb = 0; rb < rows.size(); rb += rows_per) {
             Proto pr;
-            pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + kRowsPerItem));
+            pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
             pr.spans = {piece};
             pr.kv_head = g;
             pr.keys = piece.key_end - piece.key_begin;
             pr.shared = true;
+            pr.wide = wide;
             protos.push_back(std::move(pr));
           }
       }
@@ -275,16 +316,23 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
           for (int j0 = 0; j0 < G; j0 += kRowsPerItem) {
             Proto pr;
             for (int j = j0; j < std::min(G, j0 + kRowsPerItem); ++j)
-              pr.rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0});
+              pr.rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, 0});
             pr.spans = ch;
             pr.kv_head = g;
             pr.keys = keys;
             pr.shared = false;
+            pr.wide = false;
             protos.push_back(std::move(pr));
           }
         }
     }
   } else {
+    // Prefill: bf16 rows go to wide items of 64 * rb (query, head) rows.
+    const bool wide = p.kv_dtype == HALO_BF16 && env_int("HALO_WIDE", 1, 0, 1) == 1;
+    int rb = env_int("HALO_WIDE_RB", 2, 1, 4);
+    if (rb == 3) rb = 4;
+    plan->wide_rb = wide ? rb : 0;
+    const int rows_per = wide ? 64 * rb : kRowsPerItem;
     for (int r = 0; r < R; ++r) {
       const int32_t n = f.q_len[r];
       if (n == 0) continue;
@@ -302,10 +350,10 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         std::vector<Row> rows;
         for (int32_t i = 0; i < n; ++i)
           for (int j = 0; j < G; ++j)
-            rows.push_back(Row{(int32_t)((tok0[r] + i) * Hq + g * G + j), i});
-        for (size_t rb = 0; rb < rows.size(); rb += kRowsPerItem) {
+            rows.push_back(Row{(int32_t)((tok0[r] + i) * Hq + g * G + j), i, -1, 0});
+        for (size_t rb = 0; rb < rows.size(); rb += rows_per) {
           Proto pr;
-          pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + kRowsPerItem));
+          pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
           int32_t qmax = 0;
           for (auto& x : pr.rows) qmax = std::max(qmax, x.qpos);
           pr.spans = prefix_spans;
@@ -313,6 +361,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
           pr.kv_head = g;
           pr.keys = prefix_keys + qmax + 1;
           pr.shared = false;
+          pr.wide = wide;
           protos.push_back(std::move(pr));
         }
       }
@@ -324,6 +373,24 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   std::vector<int32_t> n_parts(n_q_rows * Hq, 0);
   for (auto& pr : protos)
     for (auto& row : pr.rows) n_parts[row.q_row]++;
+  // Rows that see no key at all get an item with no spans, which writes
+  // O = 0 and LSE = -inf.
+  if (!prefill) {
+    std::vector<std::vector<Row>> empty(Hkv);
+    for (int64_t qr = 0; qr < n_q_rows * Hq; ++qr)
+      if (n_parts[qr] == 0) empty[(qr % Hq) / G].push_back(Row{(int32_t)qr, 0, -1, 0});
+    for (int g = 0; g < Hkv; ++g)
+    for (size_t i = 0; i < empty[g].size(); i += kRowsPerItem) {
+      Proto pr;
+      pr.rows.assign(empty[g].begin() + i, empty[g].begin() + std::min(empty[g].size(), i + kRowsPerItem));
+      pr.kv_head = g;
+      pr.keys = 0;
+      pr.shared = false;
+      pr.wide = false;
+      for (auto& row : pr.rows) n_parts[row.q_row] = 1;
+      protos.push_back(std::move(pr));
+    }
+  }
   std::vector<char> is_final(protos.size(), 0);
   for (size_t i = 0; i < protos.size(); ++i) {
     bool all_one = true;
@@ -337,7 +404,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   std::stable_sort(order.begin(), order.end(),
                    [&](size_t a, size_t b) { return protos[a].keys > protos[b].keys; });
 
-  std::vector<Item> items;
+  std::vector<Item> items, witems;
   std::vector<Span> spans;
   std::vector<Row> rows;
   std::vector<std::vector<int32_t>> row_parts(prefill ? 0 : n_q_rows * Hq);
@@ -373,23 +440,35 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         spans.push_back(piece);
       }
     it.n_spans = (int32_t)spans.size() - it.span_begin;
-    items.push_back(it);
+    (pr.wide ? witems : items).push_back(it);
   }
 
-  // Merge list: every decode row no final item writes -- rows with several
-  // partials, rows whose single partial comes from an item that also holds
-  // multi-part rows, and rows with no keys at all (O = 0, LSE = -inf).
+  // Merge list: every decode row no final item writes, i.e. every row with
+  // partial results (several, or one from an item that also holds
+  // multi-part rows); the merge kernel combines them after the attention
+  // kernels.
   std::vector<int32_t> merge_rows, merge_indptr{0}, merge_parts;
   if (!prefill) {
+    std::vector<int32_t> merge_of(n_q_rows * Hq, -1);
     for (int64_t qr = 0; qr < n_q_rows * Hq; ++qr) {
-      if (n_parts[qr] == 1 && row_parts[qr].empty()) continue;   // written by a final item
+      if (row_parts[qr].empty()) continue;   // written by a final item
+      merge_of[qr] = (int32_t)merge_rows.size();
       merge_rows.push_back((int32_t)qr);
       merge_parts.insert(merge_parts.end(), row_parts[qr].begin(), row_parts[qr].end());
       merge_indptr.push_back((int32_t)merge_parts.size());
     }
+    for (const std::vector<Item>* list : {&items, &witems})
+      for (const Item& it : *list)
+        if (it.part_base >= 0)
+          for (int32_t k = 0; k < it.n_rows; ++k) {
+            Row& row = rows[it.row_begin + k];
+            row.merge_idx = merge_of[row.q_row];
+          }
   }
 
   plan->n_items = (int32_t)items.size();
+  plan->n_wide = (int32_t)witems.size();
+  if (plan->n_wide == 0) plan->wide_rb = 0;
   plan->n_spans = (int32_t)spans.size();
   plan->n_rows = (int32_t)rows.size();
   plan->n_merge_parts = (int32_t)merge_parts.size();
@@ -413,6 +492,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   L.seg_len = place(sizeof(int32_t) * std::max(S, 1));
   L.page_ids = place(sizeof(int32_t) * std::max<int64_t>(total_pages, 1));
   L.items = place(sizeof(Item) * std::max<size_t>(items.size(), 1));
+  L.wide_items = place(sizeof(Item) * std::max<size_t>(witems.size(), 1));
   L.spans = place(sizeof(Span) * std::max<size_t>(spans.size(), 1));
   L.rows = place(sizeof(Row) * std::max<size_t>(rows.size(), 1));
   L.merge_rows = place(sizeof(int32_t) * std::max<size_t>(merge_rows.size(), 1));
@@ -428,6 +508,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   }
   if (total_pages) memcpy(m + L.page_ids, f.seg_page_ids, sizeof(int32_t) * total_pages);
   if (!items.empty()) memcpy(m + L.items, items.data(), sizeof(Item) * items.size());
+  if (!witems.empty()) memcpy(m + L.wide_items, witems.data(), sizeof(Item) * witems.size());
   if (!spans.empty()) memcpy(m + L.spans, spans.data(), sizeof(Span) * spans.size());
   if (!rows.empty()) memcpy(m + L.rows, rows.data(), sizeof(Row) * rows.size());
   if (!merge_rows.empty()) memcpy(m + L.merge_rows, merge_rows.data(), sizeof(int32_t) * merge_rows.size());
@@ -448,6 +529,8 @@ extern "C" halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_
   if (!plan || !st) return fail(HALO_ERR_INVALID_ARGUMENT, "plan and stats must not be NULL");
   st->is_prefill = plan->prefill ? 1 : 0;
   st->num_items = plan->n_items;
+  st->num_wide_items = plan->n_wide;
+  st->wide_row_blocks = plan->wide_rb;
   st->num_shared_items = plan->n_shared_items;
   st->num_merge_rows = plan->n_merge;
   st->num_partial_rows = plan->n_part_rows;
@@ -467,6 +550,7 @@ extern "C" halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void**
   out->seg_len = L.seg_len;
   out->page_ids = L.page_ids;
   out->items = L.items;
+  out->wide_items = L.wide_items;
   out->spans = L.spans;
   out->rows = L.rows;
   out->merge_rows = L.merge_rows;
@@ -474,6 +558,7 @@ extern "C" halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void**
   out->merge_parts = L.merge_parts;
   out->total_bytes = L.total;
   out->n_items = plan->n_items;
+  out->n_wide = plan->n_wide;
   out->n_spans = plan->n_spans;
   out->n_rows = plan->n_rows;
   out->n_merge = plan->n_merge;

@@ -45,14 +45,15 @@ class PlanStats(ctypes.Structure):
     _fields_ = [("is_prefill", ctypes.c_int32), ("num_items", ctypes.c_int32),
                 ("num_shared_items", ctypes.c_int32), ("num_merge_rows", ctypes.c_int32),
                 ("num_partial_rows", ctypes.c_int64), ("num_query_rows", ctypes.c_int64),
-                ("distinct_kv_tokens", ctypes.c_int64), ("visible_pairs", ctypes.c_int64)]
+                ("distinct_kv_tokens", ctypes.c_int64), ("visible_pairs", ctypes.c_int64),
+                ("num_wide_items", ctypes.c_int32), ("wide_row_blocks", ctypes.c_int32)]
 
 
 class PlanLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
-        "seg_page_off", "seg_len", "page_ids", "items", "spans", "rows", "merge_rows",
+        "seg_page_off", "seg_len", "page_ids", "items", "wide_items", "spans", "rows", "merge_rows",
         "merge_indptr", "merge_parts", "total_bytes")] + [(n, ctypes.c_int32) for n in (
-            "n_items", "n_spans", "n_rows", "n_merge", "n_merge_parts", "n_pages")]
+            "n_items", "n_wide", "n_spans", "n_rows", "n_merge", "n_merge_parts", "n_pages")]
 
 
 EXPORTED_SYMBOLS = (
@@ -213,8 +214,9 @@ class Plan:
         return dict(
             seg_page_off=arr(lay.seg_page_off, S), seg_len=arr(lay.seg_len, S),
             page_ids=arr(lay.page_ids, lay.n_pages),
-            items=arr(lay.items, lay.n_items, 8).copy(), spans=arr(lay.spans, lay.n_spans, 8).copy(),
-            rows=arr(lay.rows, lay.n_rows, 2).copy(), merge_rows=arr(lay.merge_rows, lay.n_merge),
+            items=arr(lay.items, lay.n_items, 8).copy(),
+            wide_items=arr(lay.wide_items, lay.n_wide, 8).copy(), spans=arr(lay.spans, lay.n_spans, 8).copy(),
+            rows=arr(lay.rows, lay.n_rows, 4).copy(), merge_rows=arr(lay.merge_rows, lay.n_merge),
             merge_indptr=arr(lay.merge_indptr, lay.n_merge + 1),
             merge_parts=arr(lay.merge_parts, lay.n_merge_parts), total_bytes=lay.total_bytes)
 

@@ -96,7 +96,9 @@ def _check_plan(w, plan):
     m = plan.inspect()
     hq, hkv = w.num_q_heads, w.num_kv_heads
     group = hq // hkv
-    items, spans, rows = m["items"], m["spans"], m["rows"]
+    items = np.concatenate([m["items"].reshape(-1, 8), m["wide_items"].reshape(-1, 8)])
+    n_narrow = len(m["items"])
+    spans, rows = m["spans"], m["rows"]
     for sp in spans:
         seg, kb, ke, causal, page_off = sp[:5]
         assert kb % 32 == 0 and 0 <= kb < ke <= w.seg_len[seg] and ke - kb <= 1024
@@ -104,7 +106,9 @@ def _check_plan(w, plan):
     for s in range(len(w.seg_len)):
         off = m["seg_page_off"][s]
         assert np.array_equal(m["page_ids"][off:off + len(w.seg_pages[s])], w.seg_pages[s])
-    assert ((items[:, 1] >= 1) & (items[:, 1] <= 16) & (items[:, 3] >= 1)).all()
+    assert ((items[:, 1] >= 1) & (items[:, 3] >= 0)).all()
+    assert ((items[:, 3] >= 1) | (items[:, 5] == -1)).all(), "no-span items are final"
+    assert (items[:n_narrow, 1] <= 16).all() and (items[n_narrow:, 1] <= 256).all()
     # every (item, row) pair
     it_rep = np.repeat(np.arange(len(items)), items[:, 1])
     row_idx = items[it_rep, 0] + (np.arange(len(it_rep)) - np.repeat(np.cumsum(items[:, 1]) - items[:, 1],
@@ -147,6 +151,10 @@ def _check_plan(w, plan):
     mrows = m["merge_rows"]
     # a row is written either by its one final item or by the merge, never both
     assert set(mrows.tolist()) == set(range(w.q.shape[0] * hq)) - set(final_rows.tolist())
+    midx = rows[row_idx, 2]
+    assert (midx[part == -1] == -1).all(), "final rows carry no merge entry"
+    pos = {int(r_): i for i, r_ in enumerate(mrows.tolist())}
+    assert all(midx[k] == pos[int(q_row[k])] for k in np.nonzero(part >= 0)[0]), "merge entry mismatch"
     by_row = {}
     for r_, p_ in zip(q_row[part >= 0].tolist(), parts.tolist()):
         by_row.setdefault(r_, set()).add(p_)
@@ -155,7 +163,7 @@ def _check_plan(w, plan):
         assert got_parts == by_row.get(r_, set())
     st = plan.stats()
     assert st["visible_pairs"] == int(eh.sum())
-    assert st["num_items"] == len(items)
+    assert st["num_items"] == n_narrow and st["num_wide_items"] == len(items) - n_narrow
     return m
 
 
@@ -190,11 +198,16 @@ def test_plan_empty_batch_and_empty_segments(lib):
                        poison=False)
     plan = halo.Plan.from_csr(_params(w), w.forest_csr())
     m = _check_plan(w, plan)
-    # requests 0, 1 and 3 see no key: their rows go through the merge with zero parts
-    for r in (0, 1, 3):
-        for h in range(4):
-            i = list(m["merge_rows"]).index(r * 4 + h)
-            assert m["merge_indptr"][i] == m["merge_indptr"][i + 1]
+    # requests 0, 1 and 3 see no key: their rows sit in final items with no
+    # spans (which write O = 0, LSE = -inf), never in the merge list
+    empty_rows = {r * 4 + h for r in (0, 1, 3) for h in range(4)}
+    found = set()
+    for it in m["items"]:
+        if it[3] == 0:
+            assert it[5] == -1
+            found |= set(m["rows"][it[0]:it[0] + it[1], 0].tolist())
+    assert found == empty_rows
+    assert not empty_rows & set(m["merge_rows"].tolist())
 
 
 def _csr(seg_len, pages, paths, q_len=None):
