@@ -28,8 +28,9 @@ struct Item {
   int32_t part_base;   // >= 0: partial rows part_base + i in the workspace;
                        // -1: final rows written straight to o / lse
   int32_t keys;        // visible-key estimate (cost, for ordering only)
-  int32_t pad;
+  int32_t flags;       // kItemStream: keys read by this item only (stream them)
 };
+constexpr int32_t kItemStream = 1;
 
 // A contiguous range of keys of one segment, [key_begin, key_end).
 // key_begin is a multiple of kKeysPerStep and a span covers at most
@@ -80,7 +81,9 @@ struct halo_plan {
   int64_t num_query_rows = 0;
   int32_t n_items = 0;
   int32_t n_wide = 0;
-  int32_t wide_rb = 0;       // MFMA row blocks per wave in wide items (1, 2, 4)
+  int32_t wide_rb = 0;       // MFMA row blocks per wave in wide items (1, 2)
+  int32_t wide_group = 1;    // wide items that share pages, kept on one XCD
+  int32_t narrow_group = 1;  // narrow 4-item blocks that share pages, kept on one XCD
   int32_t n_shared_items = 0;
   int32_t n_merge = 0;
   int32_t n_spans = 0;

@@ -54,30 +54,45 @@ __device__ __forceinline__ f32x8_t load8(const float* p) {
 
 template <typename F> __device__ __forceinline__ F zero_frag() { return F{}; }
 
+// 16-byte global load; NT marks data read once (non-temporal: streamed past
+// the caches, measured 7.2 TB/s vs 5.8 TB/s for plain loads on a read stream).
+template <bool NT>
+__device__ __forceinline__ u32x4_t ld16(const void* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  else return *reinterpret_cast<const u32x4_t*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ u32x2_t ld8(const void* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+  else return *reinterpret_cast<const u32x2_t*>(p);
+}
+
 // K fragment: dims d0..d0+7 of key t in a K tile stored as [D/E][16][E]
 // (E elements per 16-byte unit).
+template <bool NT>
 __device__ __forceinline__ bf16x8_t load_k8(const __bf16* tile, int t, int d0) {
-  return load8(tile + ((d0 >> 3) * 16 + t) * 8);
+  return __builtin_bit_cast(bf16x8_t, ld16<NT>(tile + ((d0 >> 3) * 16 + t) * 8));
 }
+template <bool NT>
 __device__ __forceinline__ f32x8_t load_k8(const float* tile, int t, int d0) {
-  typedef float f32x4v __attribute__((ext_vector_type(4)));
-  const f32x4v lo = *reinterpret_cast<const f32x4v*>(tile + ((d0 >> 2) * 16 + t) * 4);
-  const f32x4v hi = *reinterpret_cast<const f32x4v*>(tile + (((d0 >> 2) + 1) * 16 + t) * 4);
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  const u32x4_t lo = ld16<NT>(tile + ((d0 >> 2) * 16 + t) * 4);
+  const u32x4_t hi = ld16<NT>(tile + (((d0 >> 2) + 1) * 16 + t) * 4);
+  return __builtin_bit_cast(f32x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // V fragment: keys 4u..4u+3 of dim d from page tiles p0 (slots 0..3) and p1
 // (slots 4..7), V tiles stored dim-major as [D][16].
+template <bool NT>
 __device__ __forceinline__ bf16x8_t load_v8(const __bf16* p0, const __bf16* p1, int off) {
-  const u32x2_t a = *reinterpret_cast<const u32x2_t*>(p0 + off);
-  const u32x2_t b = *reinterpret_cast<const u32x2_t*>(p1 + off);
+  const u32x2_t a = ld8<NT>(p0 + off);
+  const u32x2_t b = ld8<NT>(p1 + off);
   return __builtin_bit_cast(bf16x8_t, u32x4_t{a.x, a.y, b.x, b.y});
 }
+template <bool NT>
 __device__ __forceinline__ f32x8_t load_v8(const float* p0, const float* p1, int off) {
-  typedef float f32x4v __attribute__((ext_vector_type(4)));
-  const f32x4v lo = *reinterpret_cast<const f32x4v*>(p0 + off);
-  const f32x4v hi = *reinterpret_cast<const f32x4v*>(p1 + off);
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  const u32x4_t lo = ld16<NT>(p0 + off);
+  const u32x4_t hi = ld16<NT>(p1 + off);
+  return __builtin_bit_cast(f32x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // D(16x16) += A(16x32) B(32x16). bf16: one MFMA. fp32: the same 32-deep
@@ -137,9 +152,25 @@ struct AttnArgs {
   const Row* rows;
   int32_t n_items;
   int32_t n_wide;
+  int32_t wide_blocks;     // grid blocks of the wide role (n_wide padded, see xcd_remap)
+  int32_t narrow_blocks;   // grid blocks of the narrow role (4 items each, padded)
+  int32_t wide_group;      // consecutive wide items kept on one XCD
+  int32_t narrow_group;    // consecutive narrow blocks kept on one XCD
   int32_t num_kv_heads;
   float scale_log2;   // sm_scale * log2(e)
 };
+
+// Workgroups are dealt to the 8 XCDs round-robin by block index, and each
+// XCD has its own L2. Blocks that read the same pages (the row groups of one
+// shared chunk) are made consecutive on one XCD: physical block p of a
+// segment (p % 8 = XCD, p / 8 = its turn there) runs logical block
+//   ((p / 8) / S * 8 + p % 8) * S + (p / 8) % S,
+// i.e. groups of S logical blocks go round-robin to XCDs, in order. The
+// segment length is a multiple of 8 S, so this is a permutation.
+__device__ __forceinline__ int xcd_remap(int p, int S) {
+  const int x = p & 7, j = p >> 3;
+  return ((j / S) * 8 + x) * S + j % S;
+}
 
 // A span's keys and its page ids, one page per lane (a span has at most 64
 // pages), so a step finds its page ids with two lane reads instead of
@@ -192,7 +223,7 @@ struct StepRegs {
 //  * Loads are software-pipelined: the operands of step i+1 are in flight
 //    while step i is computed, and the next span's page ids are loaded when
 //    its predecessor starts.
-template <typename T, int D, typename TO>
+template <typename T, int D, typename TO, bool NT>
 __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int lane) {
   using F = typename FragOf<T>::type;
   constexpr int NS = D / 32;   // QK steps over d
@@ -249,13 +280,13 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
     const T* k1 = kbase + (int64_t)p.pid1 * page_stride;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      r.k[0][s] = load_k8(k0, col, 32 * s + 8 * grp);
-      r.k[1][s] = load_k8(k1, col, 32 * s + 8 * grp);
+      r.k[0][s] = load_k8<NT>(k0, col, 32 * s + 8 * grp);
+      r.k[1][s] = load_k8<NT>(k1, col, 32 * s + 8 * grp);
     }
     const T* v0 = vbase + (int64_t)p.pid0 * page_stride;
     const T* v1 = vbase + (int64_t)p.pid1 * page_stride;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) r.v[b] = load_v8(v0, v1, v_off + b * 256);
+    for (int b = 0; b < NB; ++b) r.v[b] = load_v8<NT>(v0, v1, v_off + b * 256);
   };
 
   // Span cursor: cur is being walked, nxt is loaded one span ahead.
@@ -373,11 +404,12 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
 }
 
 template <typename T, int D, typename TO>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_items_kernel(AttnArgs a) {
-  const int item_id = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
+__device__ __forceinline__ void narrow_block(const AttnArgs& a, int block) {
+  const int item_id = __builtin_amdgcn_readfirstlane((int)(block * 4 + (threadIdx.x >> 6)));
   if (item_id >= a.n_items) return;
   const Item it = a.items[item_id];
-  run_item<T, D, TO>(a, it, threadIdx.x & 63);
+  if (it.flags & kItemStream) run_item<T, D, TO, true>(a, it, threadIdx.x & 63);
+  else run_item<T, D, TO, false>(a, it, threadIdx.x & 63);
 }
 
 
@@ -406,8 +438,7 @@ struct WideGeom {
 };
 
 template <int D, int RB, typename TO>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(RB >= 4 ? 1 : 2)))
-void attn_wide_kernel(AttnArgs a) {
+__device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
   using T = __bf16;
   using F = bf16x8_t;
   using G = WideGeom<D>;
@@ -420,8 +451,6 @@ void attn_wide_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int col = lane & 15;
   const int grp = lane >> 4;
-  const int item_id = blockIdx.x;
-  if (item_id >= a.n_wide) return;
   const Item it = a.wide_items[item_id];
 
   // This lane's rows: row block rb of this wave, column col.
@@ -629,6 +658,36 @@ void attn_wide_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- launch
+// One launch runs both roles: the first wide_blocks blocks are wide items
+// (MFMA/LDS-bound grouped prefix or prefill work), the rest hold four narrow
+// items each (mostly HBM-bound suffix streaming), so the two kinds of work
+// overlap on the GPU. RB = 0: no wide role (fp32 inputs).
+// The grid is dealt in rounds of 8 blocks (one per XCD); rounds of the two
+// roles are spread evenly over the launch so every CU mixes MFMA-heavy wide
+// blocks with HBM-heavy narrow ones, and within a role the block index modulo
+// 8 still names the XCD (xcd_remap stays valid).
+template <typename T, int D, typename TO, int RB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 ? 2 : 1)))
+void attn_kernel(AttnArgs a) {
+  const int b = blockIdx.x;
+  const int x = b & 7, r = b >> 3;
+  if constexpr (RB > 0) {
+    const int wr = a.wide_blocks >> 3;
+    const int tr = wr + (a.narrow_blocks >> 3);
+    const int w_before = (int)((int64_t)r * wr / tr);
+    const int w_upto = (int)((int64_t)(r + 1) * wr / tr);
+    if (w_upto > w_before) {
+      const int item = xcd_remap(w_before * 8 + x, a.wide_group);
+      if (item < a.n_wide) wide_item<D, RB, TO>(a, item);
+      return;
+    }
+    narrow_block<T, D, TO>(a, xcd_remap((r - w_upto) * 8 + x, a.narrow_group));
+  } else {
+    narrow_block<T, D, TO>(a, xcd_remap(b, a.narrow_group));
+  }
+}
+
 // ---------------------------------------------------------------- merge
 
 struct MergeArgs {
@@ -779,21 +838,25 @@ halo_status_t hip_check(const char* what) {
   return HALO_OK;
 }
 
-template <int D, typename TO>
-void launch_wide(const AttnArgs& args, int rb, hipStream_t stream) {
-  if (rb == 1) hipLaunchKernelGGL((attn_wide_kernel<D, 1, TO>), dim3(args.n_wide), dim3(256), 0, stream, args);
-  else if (rb == 2) hipLaunchKernelGGL((attn_wide_kernel<D, 2, TO>), dim3(args.n_wide), dim3(256), 0, stream, args);
-  else hipLaunchKernelGGL((attn_wide_kernel<D, 4, TO>), dim3(args.n_wide), dim3(256), 0, stream, args);
-}
+int pad_to(int n, int m) { return (n + m - 1) / m * m; }
 
 template <typename T, int D, typename TO>
-void launch_attention(const AttnArgs& args, const MergeArgs& margs, int wide_rb, hipStream_t stream) {
-  if (args.n_wide > 0) {
-    if constexpr (sizeof(T) == 2) launch_wide<D, TO>(args, wide_rb, stream);
-  }
-  if (args.n_items > 0) {
-    const int blocks = (args.n_items + 3) / 4;
-    hipLaunchKernelGGL((attn_items_kernel<T, D, TO>), dim3(blocks), dim3(256), 0, stream, args);
+void launch_attention(AttnArgs args, const MergeArgs& margs, int wide_rb, hipStream_t stream) {
+  const int rb = sizeof(T) == 2 ? wide_rb : 0;
+  args.wide_blocks = (rb > 0 && args.n_wide > 0) ? pad_to(args.n_wide, 8 * args.wide_group) : 0;
+  args.narrow_blocks = args.n_items > 0 ? pad_to((args.n_items + 3) / 4, 8 * args.narrow_group) : 0;
+  const int grid = args.wide_blocks + args.narrow_blocks;
+  if (grid > 0) {
+    if constexpr (sizeof(T) == 2) {
+      if (rb == 2)
+        hipLaunchKernelGGL((attn_kernel<T, D, TO, 2>), dim3(grid), dim3(256), 0, stream, args);
+      else if (rb == 1)
+        hipLaunchKernelGGL((attn_kernel<T, D, TO, 1>), dim3(grid), dim3(256), 0, stream, args);
+      else
+        hipLaunchKernelGGL((attn_kernel<T, D, TO, 0>), dim3(grid), dim3(256), 0, stream, args);
+    } else {
+      hipLaunchKernelGGL((attn_kernel<T, D, TO, 0>), dim3(grid), dim3(256), 0, stream, args);
+    }
   }
   if (margs.n_merge > 0) {
     constexpr int rpb = 256 / (D / 4);
@@ -838,7 +901,8 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                 reinterpret_cast<const Item*>(m + L.wide_items),
                 reinterpret_cast<const Span*>(m + L.spans),
                 reinterpret_cast<const Row*>(m + L.rows),
-                plan->n_items, plan->n_wide, p.num_kv_heads, p.sm_scale * kLog2e};
+                plan->n_items, plan->n_wide, 0, 0, plan->wide_group, plan->narrow_group,
+                p.num_kv_heads, p.sm_scale * kLog2e};
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),
                   reinterpret_cast<const int32_t*>(m + L.merge_indptr),

@@ -251,10 +251,12 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     if (wide) {
       const double avg_rows = wsum > 0 ? wrows / wsum : 0;
       int rb = avg_rows >= 128 ? 2 : 1;
-      rb = env_int("HALO_WIDE_RB", rb, 1, 4);
-      if (rb == 3) rb = 4;
+      rb = env_int("HALO_WIDE_RB", rb, 1, 2);
       plan->wide_rb = rb;
       rows_per = 64 * rb;
+      // row groups of one shared chunk read the same pages: keep up to 8 of
+      // them on one XCD
+      plan->wide_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / rows_per)));
       const int min_items = env_int("HALO_WIDE_MIN_ITEMS", 512, 1, 1 << 30);
       kc = kMaxSpanKeys;
       while (kc > 128) {
@@ -267,6 +269,14 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       }
       kc = env_int("HALO_KC_WIDE", kc, 32, kMaxSpanKeys) / 32 * 32;
     }
+    if (!wide) {
+      // 16-row items of one shared chunk are consecutive: keep the blocks
+      // holding them on one XCD
+      const double avg_rows = wsum > 0 ? wrows / wsum : 0;
+      plan->narrow_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / (4.0 * kRowsPerItem))));
+    }
+    plan->narrow_group = env_int("HALO_NARROW_GROUP", plan->narrow_group, 1, 64);
+    plan->wide_group = env_int("HALO_WIDE_GROUP", plan->wide_group, 1, 64);
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
       std::vector<Span> sp;
@@ -329,9 +339,9 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   } else {
     // Prefill: bf16 rows go to wide items of 64 * rb (query, head) rows.
     const bool wide = p.kv_dtype == HALO_BF16 && env_int("HALO_WIDE", 1, 0, 1) == 1;
-    int rb = env_int("HALO_WIDE_RB", 2, 1, 4);
-    if (rb == 3) rb = 4;
+    int rb = env_int("HALO_WIDE_RB", 2, 1, 2);
     plan->wide_rb = wide ? rb : 0;
+    plan->wide_group = 1;
     const int rows_per = wide ? 64 * rb : kRowsPerItem;
     for (int r = 0; r < R; ++r) {
       const int32_t n = f.q_len[r];
@@ -417,6 +427,9 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     it.span_begin = (int32_t)spans.size();
     it.kv_head = pr.kv_head;
     it.keys = (int32_t)std::min<int64_t>(pr.keys, std::numeric_limits<int32_t>::max());
+    // Private keys of a decode item are read by no other item: stream them
+    // past the caches.
+    it.flags = (!prefill && !pr.shared && !pr.wide) ? kItemStream : 0;
     if (is_final[oi]) {
       it.part_base = -1;
     } else {
