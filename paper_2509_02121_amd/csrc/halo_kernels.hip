@@ -542,28 +542,47 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
 
   auto compute = [&](const StepPos& p, int buf) {
     const uint8_t* base = lds + buf * G::kStepBytes;
+    // All K fragments of the step first, then the QK products.
+    F kf[2][NS];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        kf[x][s] = __builtin_bit_cast(
+            F, *reinterpret_cast<const u32x4_t*>(base + x * G::kTileBytes + ((4 * s + grp) * 16 + col) * 16));
     f32x4_t sacc[RB][2];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) sacc[rb][0] = sacc[rb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const F kf = __builtin_bit_cast(
-            F, *reinterpret_cast<const u32x4_t*>(base + x * G::kTileBytes + ((4 * s + grp) * 16 + col) * 16));
+      for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) sacc[rb][x] = mma(kf, qf[rb][s], sacc[rb][x]);
-      }
+        for (int rb = 0; rb < RB; ++rb) sacc[rb][x] = mma(kf[x][s], qf[rb][s], sacc[rb][x]);
+    // V fragments are read now so the LDS latency overlaps the softmax.
+    F vf[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int voff = ((16 * b + col) * 16 + 4 * grp) * 2;
+      const u32x2_t v0 = *reinterpret_cast<const u32x2_t*>(base + 2 * G::kTileBytes + voff);
+      const u32x2_t v1 = *reinterpret_cast<const u32x2_t*>(base + 3 * G::kTileBytes + voff);
+      vf[b] = __builtin_bit_cast(F, u32x4_t{v0.x, v0.y, v1.x, v1.y});
+    }
     const bool full = p.t0 + kKeysPerStep <= p.key_end && !p.causal;
     F pf[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       float sv[8];
+      if (full) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int key = p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3);
-        const bool vis = full || (key < p.key_end && (!p.causal || key <= row[rb].qpos));
-        sv[j] = vis ? sacc[rb][j >> 2][j & 3] * a.scale_log2 : kNegInf;
+        for (int j = 0; j < 8; ++j) sv[j] = sacc[rb][j >> 2][j & 3] * a.scale_log2;
+      } else {
+        const int lim = p.causal ? min(p.key_end, row[rb].qpos + 1) : p.key_end;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int key = p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3);
+          sv[j] = key < lim ? sacc[rb][j >> 2][j & 3] * a.scale_log2 : kNegInf;
+        }
       }
       float mt = sv[0];
 #pragma unroll
@@ -588,21 +607,18 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
       }
       pf[rb] = to_frag(pr, (F*)nullptr);
     }
+    if (!full) {
+      // keys past the span end may be NaN page tails: zero V there
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int voff = ((16 * b + col) * 16 + 4 * grp) * 2;
-      const u32x2_t v0 = *reinterpret_cast<const u32x2_t*>(base + 2 * G::kTileBytes + voff);
-      const u32x2_t v1 = *reinterpret_cast<const u32x2_t*>(base + 3 * G::kTileBytes + voff);
-      F vf = __builtin_bit_cast(F, u32x4_t{v0.x, v0.y, v1.x, v1.y});
-      if (!full) {
-        // keys past the span end may be NaN page tails: zero V there
+      for (int j = 0; j < 8; ++j)
+        if (p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3) >= p.key_end)
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3) >= p.key_end) vf[j] = (T)0.f;
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) acc[rb][b] = mma(vf, pf[rb], acc[rb][b]);
+          for (int b = 0; b < NB; ++b) vf[b][j] = (T)0.f;
     }
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) acc[rb][b] = mma(vf[b], pf[rb], acc[rb][b]);
   };
 
   // ---- pipeline: LDS buffers 0/1, register stages r0/r1, two steps ahead

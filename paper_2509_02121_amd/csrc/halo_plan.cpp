@@ -218,7 +218,19 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
 
   if (!prefill) {
     const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, kMaxSpanKeys) / 32 * 32;
-    const int kc_private = env_int("HALO_KC_PRIVATE", 256, 32, kMaxSpanKeys) / 32 * 32;
+    // Private chunks: 512 keys, or 1024 when that still leaves >= 16K items
+    // (fewer partials to write and merge; the sweep over the three decode
+    // workloads favours these).
+    int64_t private_keys = 0;
+    {
+      std::vector<int32_t> rc(S, 0);
+      for (int r = 0; r < R; ++r)
+        for (int32_t i = path_begin(r); i < path_end(r); ++i) rc[f.req_seg_ids[i]]++;
+      for (int s = 0; s < S; ++s)
+        if (rc[s] == 1) private_keys += f.seg_len[s];
+    }
+    const int kc_private_default = private_keys * Hkv / 1024 >= 16384 ? 1024 : 512;
+    const int kc_private = env_int("HALO_KC_PRIVATE", kc_private_default, 32, kMaxSpanKeys) / 32 * 32;
     for (int r = 0; r < R; ++r) {
       int64_t keys = 0;
       for (int32_t i = path_begin(r); i < path_end(r); ++i) keys += f.seg_len[f.req_seg_ids[i]];
