@@ -76,7 +76,7 @@ typedef struct {
   int64_t num_pool_pages;   /* capacity of k_pool / v_pool, in pages */
   halo_dtype_t kv_dtype;    /* element type of q, k_pool, v_pool */
   halo_dtype_t out_dtype;   /* HALO_F32, or equal to kv_dtype */
-  float sm_scale;           /* score scale, normally 1/sqrt(head_dim) */
+  float sm_scale;           /* score scale > 0, normally 1/sqrt(head_dim) */
 } halo_attn_params_t;
 
 /* Prefix forest, HOST arrays in CSR form (§2 intra-batch prefix sharing). */

@@ -522,11 +522,28 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
       st.v[k] = *reinterpret_cast<const u32x4_t*>(src);
     }
   };
+  // LDS image of a step: K tiles of both pages as stored ([D/8][16][8]),
+  // then V as 16-byte cells, one per (dim d, lane group g):
+  //   {page0 keys 4g..4g+3, page1 keys 4g..4g+3}
+  // at cell d * 4 + (g ^ ((d >> 1) & 3)): a wave's V read is then one
+  // conflict-free ds_read_b128 per output block (the XOR spreads the eight
+  // lanes served together over all banks).
   auto stage_write = [&](const Stage& st, int buf) {
+    uint8_t* base = lds + buf * G::kStepBytes;
 #pragma unroll
     for (int k = 0; k < G::kPerThread; ++k) {
       const int c = threadIdx.x + 256 * k;
-      *reinterpret_cast<u32x4_t*>(lds + buf * G::kStepBytes + c * 16) = st.v[k];
+      const int tile = c / G::kChunksPerTile;
+      const int chunk = c % G::kChunksPerTile;
+      if (tile < 2) {
+        *reinterpret_cast<u32x4_t*>(base + tile * G::kTileBytes + chunk * 16) = st.v[k];
+      } else {
+        const int d = chunk >> 1, h = chunk & 1, pg = tile - 2;
+        uint8_t* vb = base + 2 * G::kTileBytes + pg * 8;
+        const int sw = (d >> 1) & 3;
+        *reinterpret_cast<u32x2_t*>(vb + (d * 4 + ((2 * h) ^ sw)) * 16) = u32x2_t{st.v[k].x, st.v[k].y};
+        *reinterpret_cast<u32x2_t*>(vb + (d * 4 + ((2 * h + 1) ^ sw)) * 16) = u32x2_t{st.v[k].z, st.v[k].w};
+      }
     }
   };
 
@@ -563,25 +580,26 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
     F vf[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const int voff = ((16 * b + col) * 16 + 4 * grp) * 2;
-      const u32x2_t v0 = *reinterpret_cast<const u32x2_t*>(base + 2 * G::kTileBytes + voff);
-      const u32x2_t v1 = *reinterpret_cast<const u32x2_t*>(base + 3 * G::kTileBytes + voff);
-      vf[b] = __builtin_bit_cast(F, u32x4_t{v0.x, v0.y, v1.x, v1.y});
+      const int d = 16 * b + col;
+      vf[b] = __builtin_bit_cast(
+          F, *reinterpret_cast<const u32x4_t*>(base + 2 * G::kTileBytes + (d * 4 + (grp ^ ((d >> 1) & 3))) * 16));
     }
     const bool full = p.t0 + kKeysPerStep <= p.key_end && !p.causal;
     F pf[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
+      // raw scores (masked ones -inf); the scale is applied inside the
+      // exponent with one FMA (scale > 0, so it commutes with the max)
       float sv[8];
       if (full) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) sv[j] = sacc[rb][j >> 2][j & 3] * a.scale_log2;
+        for (int j = 0; j < 8; ++j) sv[j] = sacc[rb][j >> 2][j & 3];
       } else {
         const int lim = p.causal ? min(p.key_end, row[rb].qpos + 1) : p.key_end;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int key = p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3);
-          sv[j] = key < lim ? sacc[rb][j >> 2][j & 3] * a.scale_log2 : kNegInf;
+          sv[j] = key < lim ? sacc[rb][j >> 2][j & 3] : kNegInf;
         }
       }
       float mt = sv[0];
@@ -589,6 +607,7 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
       for (int j = 1; j < 8; ++j) mt = fmaxf(mt, sv[j]);
       mt = fmaxf(mt, __shfl_xor(mt, 16));
       mt = fmaxf(mt, __shfl_xor(mt, 32));
+      mt *= a.scale_log2;
       const bool move = mt > m[rb] + kRescaleLog2;
       if (__any(move)) {
         const float m_new = move ? mt : m[rb];
@@ -602,7 +621,7 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
       float pr[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        pr[j] = __builtin_amdgcn_exp2f(sv[j] - m_use);
+        pr[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j], a.scale_log2, -m_use));
         lsum[rb] += pr[j];
       }
       pf[rb] = to_frag(pr, (F*)nullptr);

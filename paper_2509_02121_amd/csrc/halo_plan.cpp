@@ -78,7 +78,8 @@ halo_status_t validate(const halo_attn_params_t* p, const halo_forest_t* f) {
     return fail(HALO_ERR_UNSUPPORTED, "out_dtype must be HALO_F32 or equal to kv_dtype");
   if (p->num_pool_pages < 0 || p->num_pool_pages > (int64_t)std::numeric_limits<int32_t>::max())
     return fail(HALO_ERR_INVALID_ARGUMENT, "num_pool_pages must be in [0, 2^31)");
-  if (!std::isfinite(p->sm_scale)) return fail(HALO_ERR_INVALID_ARGUMENT, "sm_scale must be finite");
+  if (!std::isfinite(p->sm_scale) || !(p->sm_scale > 0.f))
+    return fail(HALO_ERR_INVALID_ARGUMENT, "sm_scale must be finite and > 0");
   if (f->num_segments < 0 || f->num_requests < 0)
     return fail(HALO_ERR_INVALID_ARGUMENT, "num_segments and num_requests must be >= 0");
   const int S = f->num_segments, R = f->num_requests;

@@ -234,6 +234,7 @@ GOOD = dict(seg_len=[20, 3], pages=[[0, 1], [2]], paths=[[0, 1], [0]])
     (lambda p, c: setattr(p, "kv_dtype", 7), 2, "kv_dtype"),
     (lambda p, c: setattr(p, "out_dtype", 1), 2, "out_dtype"),     # bf16 out from f32 kv
     (lambda p, c: setattr(p, "sm_scale", float("inf")), 1, "sm_scale"),
+    (lambda p, c: setattr(p, "sm_scale", -0.5), 1, "sm_scale"),
     (lambda p, c: c["seg_page_ids"].__setitem__(1, 99), 1, "outside"),
     (lambda p, c: c["seg_page_ids"].__setitem__(0, -1), 1, "outside"),
     (lambda p, c: c["seg_len"].__setitem__(0, 40), 1, "needs"),
