@@ -21,7 +21,10 @@
  *   k_pool  [num_pool_pages][num_kv_heads][head_dim/E][page_size][E]
  *           token t, dim c of a (page, head) tile at ((c/E)*page_size + t)*E + c%E
  *           (16-byte units, so the 16 tokens of one unit column are contiguous)
- *   v_pool  [num_pool_pages][num_kv_heads][head_dim][page_size]   dim-major
+ *   v_pool  [num_pool_pages][num_kv_heads][head_dim][page_size]   dim-major;
+ *           the page_size slots of a dim row hold tokens 0-3, 8-11, 4-7,
+ *           12-15 (token t at slot (t & 3) | (t & 4) << 1 | (t & 8) >> 1),
+ *           so the 8 tokens one MFMA lane multiplies are 16 contiguous bytes
  *   q, o    decode:  [num_requests][num_q_heads][head_dim]
  *           prefill: [sum q_len][num_q_heads][head_dim], request r's rows
  *                    follow request r-1's. o has element type out_dtype.
@@ -177,7 +180,7 @@ typedef struct {
   int64_t distinct_kv_tokens; /* sum of segment lengths, each segment once */
   int64_t visible_pairs;      /* sum over query rows and q heads of visible keys */
   int32_t num_wide_items;     /* wide work items (one 4-wave workgroup, <= 256 rows) */
-  int32_t wide_row_blocks;    /* 16-row MFMA blocks per wave in wide items (0: none) */
+  int32_t wide_row_blocks;    /* 1 when the plan has wide items (32 query rows per wave), else 0 */
 } halo_plan_stats_t;
 
 halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* stats);

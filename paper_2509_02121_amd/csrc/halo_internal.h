@@ -12,8 +12,11 @@ namespace halo {
 
 // Rows of one wavefront work item: at most 16 query rows (one MFMA N tile).
 constexpr int kRowsPerItem = 16;
-// A wide item holds up to 4 waves x wide_rb row blocks x 16 rows.
-constexpr int kMaxWideRows = 256;
+// A wide item is one workgroup of kWideWaves waves of 32 query rows each.
+constexpr int kWideWaves = 8;
+constexpr int kMaxWideRows = kWideWaves * 32;
+// Narrow items per workgroup (one per wave): 8 for bf16, 4 for fp32.
+inline int narrow_items_per_block(halo_dtype_t dt) { return dt == HALO_BF16 ? 8 : 4; }
 // Keys consumed per inner step: two pages of 16 (one K=32 MFMA for P*V).
 constexpr int kKeysPerStep = 32;
 
@@ -81,9 +84,10 @@ struct halo_plan {
   int64_t num_query_rows = 0;
   int32_t n_items = 0;
   int32_t n_wide = 0;
-  int32_t wide_rb = 0;       // MFMA row blocks per wave in wide items (1, 2)
+  int32_t wide_rb = 0;       // 1 when the plan has wide items (32 rows per wave), else 0
   int32_t wide_group = 1;    // wide items that share pages, kept on one XCD
-  int32_t narrow_group = 1;  // narrow 4-item blocks that share pages, kept on one XCD
+  int32_t narrow_group = 1;  // narrow blocks that share pages, kept on one XCD
+  int32_t narrow_per_block = 1;  // narrow items per workgroup (one per wave)
   int32_t n_shared_items = 0;
   int32_t n_merge = 0;
   int32_t n_spans = 0;

@@ -31,6 +31,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
@@ -80,19 +81,27 @@ __device__ __forceinline__ f32x8_t load_k8(const float* tile, int t, int d0) {
   return __builtin_bit_cast(f32x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// V fragment: keys 4u..4u+3 of dim d from page tiles p0 (slots 0..3) and p1
-// (slots 4..7), V tiles stored dim-major as [D][16].
+// V fragment: the 8 slot-ordered keys at element offset off of a V tile
+// stored dim-major as [D][16] (one dim row holds tokens 0-3, 8-11, 4-7,
+// 12-15, so slots 8h..8h+7 are the keys one lane multiplies).
 template <bool NT>
-__device__ __forceinline__ bf16x8_t load_v8(const __bf16* p0, const __bf16* p1, int off) {
-  const u32x2_t a = ld8<NT>(p0 + off);
-  const u32x2_t b = ld8<NT>(p1 + off);
-  return __builtin_bit_cast(bf16x8_t, u32x4_t{a.x, a.y, b.x, b.y});
+__device__ __forceinline__ bf16x8_t load_v8(const __bf16* page, int off) {
+  return __builtin_bit_cast(bf16x8_t, ld16<NT>(page + off));
 }
 template <bool NT>
-__device__ __forceinline__ f32x8_t load_v8(const float* p0, const float* p1, int off) {
-  const u32x4_t lo = ld16<NT>(p0 + off);
-  const u32x4_t hi = ld16<NT>(p1 + off);
+__device__ __forceinline__ f32x8_t load_v8(const float* page, int off) {
+  const u32x4_t lo = ld16<NT>(page + off);
+  const u32x4_t hi = ld16<NT>(page + off + 4);
   return __builtin_bit_cast(f32x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// Key (relative to the first key of a 32-key step) behind slot j of a lane
+// in lane group grp. QK tile X (X = j / 4) takes its 16 A rows as keys
+// 8X..8X+7 of page 0 (rows 0-7) and of page 1 (rows 8-15); MFMA output
+// register i of lane group grp is tile row 4 grp + i, i.e. page grp / 2,
+// key 8X + 4 (grp % 2) + i.
+__device__ __forceinline__ int slot_key(int grp, int j) {
+  return 16 * (grp >> 1) + 8 * (j >> 2) + 4 * (grp & 1) + (j & 3);
 }
 
 // D(16x16) += A(16x32) B(32x16). bf16: one MFMA. fp32: the same 32-deep
@@ -105,6 +114,13 @@ __device__ __forceinline__ f32x4_t mma(f32x8_t a, f32x8_t b, f32x4_t c) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
   return c;
+}
+
+// D(32x32) += A(32x16) B(16x32), bf16 operands, fp32 accumulate. Lane
+// (c = lane % 32, h = lane / 32): A row c and B column c, k = 8h..8h+7;
+// result register i holds row 8 (i / 4) + 4h + i % 4, column c.
+__device__ __forceinline__ f32x16_t mma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ bf16x8_t to_frag(const float (&p)[8], bf16x8_t*) {
@@ -133,6 +149,38 @@ __device__ __forceinline__ void store4(__bf16* dst, f32x4_t v) {
   *reinterpret_cast<uint2*>(dst) = __builtin_bit_cast(uint2, r);
 }
 
+// V pages keep the tokens of a dim row in the slot order 0-3, 8-11, 4-7,
+// 12-15 (bits 2 and 3 of the index swapped; the map is its own inverse).
+__device__ __forceinline__ int v_token_at_slot(int s) { return (s & 3) | ((s & 4) << 1) | ((s & 8) >> 1); }
+
+// Reductions over the four 16-lane rows of a wave (lanes l, l^16, l^32,
+// l^48) with the gfx950 row-swap instructions, which stay on the VALU
+// instead of going through the LDS crossbar like a generic shuffle. Each
+// swap leaves, in every lane, the pair {own value, value of lane l^16} (or
+// l^32), in some order; max and sum are symmetric in the pair.
+__device__ __forceinline__ float rows_max(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows_sum(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Reductions over the two 32-lane halves of a wave (lanes l and l^32).
+__device__ __forceinline__ float halves_max(float x) {
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // ---------------------------------------------------------------- attention
 
 struct AttnArgs {
@@ -153,7 +201,8 @@ struct AttnArgs {
   int32_t n_items;
   int32_t n_wide;
   int32_t wide_blocks;     // grid blocks of the wide role (n_wide padded, see xcd_remap)
-  int32_t narrow_blocks;   // grid blocks of the narrow role (4 items each, padded)
+  int32_t narrow_blocks;   // grid blocks of the narrow role (narrow_per_block items each, padded)
+  int32_t narrow_per_block;  // narrow items per block, one per wave (the other waves exit)
   int32_t wide_group;      // consecutive wide items kept on one XCD
   int32_t narrow_group;    // consecutive narrow blocks kept on one XCD
   int32_t num_kv_heads;
@@ -189,6 +238,7 @@ struct StepPos {
   int pid0, pid1;  // page ids of the step's two pages (pid1 == pid0 if absent)
   bool has1;
   bool valid;
+  bool full;       // all 32 keys visible to every row: inside the span, no causal mask
 };
 
 // Field-wise choice between two step positions (a conditional on the
@@ -202,6 +252,7 @@ __device__ __forceinline__ StepPos pick(bool c, const StepPos& x, const StepPos&
   r.pid1 = c ? x.pid1 : y.pid1;
   r.has1 = c ? x.has1 : y.has1;
   r.valid = c ? x.valid : y.valid;
+  r.full = c ? x.full : y.full;
   return r;
 }
 
@@ -223,7 +274,7 @@ struct StepRegs {
 //  * Loads are software-pipelined: the operands of step i+1 are in flight
 //    while step i is computed, and the next span's page ids are loaded when
 //    its predecessor starts.
-template <typename T, int D, typename TO, bool NT>
+template <typename T, int D, typename TO, bool NT, int P>
 __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int lane) {
   using F = typename FragOf<T>::type;
   constexpr int NS = D / 32;   // QK steps over d
@@ -246,7 +297,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
   const int64_t page_stride = (int64_t)a.num_kv_heads * kTile;
   const T* kbase = static_cast<const T*>(a.k_pool) + (int64_t)it.kv_head * kTile;
   const T* vbase = static_cast<const T*>(a.v_pool) + (int64_t)it.kv_head * kTile;
-  const int v_off = col * 16 + 4 * grp;   // V^T[dim col][key 4grp] in a tile
+  const int v_off = col * 16 + 8 * (grp & 1);   // V^T[dim col][slots 8(grp%2)..] in a tile
 
   auto load_span = [&](int si) {
     SpanState st;
@@ -271,22 +322,23 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
     p.causal = st.causal;
     const int j = (t0 - st.kb) >> 4;
     p.has1 = t0 + 16 < st.ke;
+    p.full = t0 + kKeysPerStep <= st.ke && !st.causal;
     p.pid0 = __builtin_amdgcn_readlane(st.vpid, j);
     p.pid1 = p.has1 ? __builtin_amdgcn_readlane(st.vpid, j + 1) : p.pid0;
     return p;
   };
   auto fetch = [&](const StepPos& p, Regs& r) {
-    const T* k0 = kbase + (int64_t)p.pid0 * page_stride;
-    const T* k1 = kbase + (int64_t)p.pid1 * page_stride;
+    // A rows 0-7 come from page 0, rows 8-15 from page 1; a V lane reads
+    // page grp / 2.
+    const T* kq = kbase + (int64_t)(col < 8 ? p.pid0 : p.pid1) * page_stride;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      r.k[0][s] = load_k8<NT>(k0, col, 32 * s + 8 * grp);
-      r.k[1][s] = load_k8<NT>(k1, col, 32 * s + 8 * grp);
+      r.k[0][s] = load_k8<NT>(kq, col & 7, 32 * s + 8 * grp);
+      r.k[1][s] = load_k8<NT>(kq, 8 + (col & 7), 32 * s + 8 * grp);
     }
-    const T* v0 = vbase + (int64_t)p.pid0 * page_stride;
-    const T* v1 = vbase + (int64_t)p.pid1 * page_stride;
+    const T* vq = vbase + (int64_t)(grp < 2 ? p.pid0 : p.pid1) * page_stride;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) r.v[b] = load_v8<NT>(v0, v1, v_off + b * 256);
+    for (int b = 0; b < NB; ++b) r.v[b] = load_v8<NT>(vq, v_off + b * 256);
   };
 
   // Span cursor: cur is being walked, nxt is loaded one span ahead.
@@ -321,7 +373,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
 #pragma unroll
       for (int s = 0; s < NS; ++s) sacc[x] = mma(r.k[x][s], qf[s], sacc[x]);
     }
-    // slot j = 4X + i holds key t0 + 16X + 4grp + i
+    // slot j = 4X + i holds key t0 + slot_key(grp, j)
     float sv[8];
     if (p.t0 + kKeysPerStep <= p.key_end && !p.causal) {
 #pragma unroll
@@ -329,7 +381,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const int key = p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3);
+        const int key = p.t0 + slot_key(grp, j);
         const bool vis = key < p.key_end && (!p.causal || key <= row.qpos);
         sv[j] = vis ? sacc[j >> 2][j & 3] * a.scale_log2 : kNegInf;
       }
@@ -337,15 +389,14 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
       // zero V there, since P = 0 times NaN would still poison the sum.
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        if (p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3) >= p.key_end)
+        if (p.t0 + slot_key(grp, j) >= p.key_end)
 #pragma unroll
           for (int b = 0; b < NB; ++b) r.v[b][j] = (T)0.f;
     }
     float mt = sv[0];
 #pragma unroll
     for (int j = 1; j < 8; ++j) mt = fmaxf(mt, sv[j]);
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    mt = rows_max(mt);
     const float m_new = fmaxf(m, mt);
     const float m_use = m_new == kNegInf ? 0.f : m_new;
     const float alpha = __builtin_amdgcn_exp2f(m - m_use);
@@ -366,24 +417,34 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
     }
   };
 
+  // P register stages rotate: while step s is computed, the next P - 1
+  // steps are in flight. A position past the end re-fetches the current
+  // step's pages (in bounds, never used).
   if (cur.valid) {
-    Regs ra, rb;
-    StepPos pa = advance();
-    fetch(pa, ra);
-    while (true) {
-      StepPos pb = advance();
-      fetch(pick(pb.valid, pb, pa), rb);
-      compute(pa, ra);
-      if (!pb.valid) break;
-      pa = advance();
-      fetch(pick(pa.valid, pa, pb), ra);
-      compute(pb, rb);
-      if (!pa.valid) break;
+    Regs r[P];
+    StepPos ps[P];
+#pragma unroll
+    for (int i = 0; i < P - 1; ++i) {
+      ps[i] = advance();
+      fetch(pick(ps[i].valid, ps[i], ps[0]), r[i]);
+    }
+    bool done = false;
+    while (!done) {
+#pragma unroll
+      for (int s = 0; s < P; ++s) {
+        const int w = (s + P - 1) % P;
+        ps[w] = advance();
+        fetch(pick(ps[w].valid, ps[w], ps[s]), r[w]);
+        compute(ps[s], r[s]);
+        if (!ps[(s + 1) % P].valid) {
+          done = true;
+          break;
+        }
+      }
     }
   }
 
-  lsum += __shfl_xor(lsum, 16);
-  lsum += __shfl_xor(lsum, 32);
+  lsum = rows_sum(lsum);
   const bool has_row = col < it.n_rows;
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   const float lse2 = lsum > 0.f ? m + __log2f(lsum) : kNegInf;
@@ -403,66 +464,100 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
   }
 }
 
+// Waves per workgroup: 8 for bf16 (two per SIMD, so one wave's softmax
+// overlaps another's MFMAs), 4 for fp32, whose operand registers allow only
+// one wave per SIMD.
+template <typename T> constexpr int block_waves() { return sizeof(T) == 2 ? 8 : 4; }
+
+// One narrow item per wave of the block.
 template <typename T, int D, typename TO>
 __device__ __forceinline__ void narrow_block(const AttnArgs& a, int block) {
-  const int item_id = __builtin_amdgcn_readfirstlane((int)(block * 4 + (threadIdx.x >> 6)));
-  if (item_id >= a.n_items) return;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int item_id = block * a.narrow_per_block + wave;
+  if (wave >= a.narrow_per_block || item_id >= a.n_items) return;
   const Item it = a.items[item_id];
-  if (it.flags & kItemStream) run_item<T, D, TO, true>(a, it, threadIdx.x & 63);
-  else run_item<T, D, TO, false>(a, it, threadIdx.x & 63);
+  if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, threadIdx.x & 63);
+  else run_item<T, D, TO, false, 2>(a, it, threadIdx.x & 63);
 }
 
-
 // ---------------------------------------------------------------- wide items
-// A wide item holds up to 4 * RB * 16 query rows of one kv head against a
-// span list: a workgroup of 4 waves, RB MFMA row blocks per wave, all rows
-// sharing the key stream. Each 32-key step's four tiles (K and V of its two
-// pages) are read once per workgroup with coalesced 16-byte loads, two steps
-// ahead through registers, into an LDS double buffer; every wave then reads
-// its MFMA operands from LDS (1 KB contiguous per K read, 512 B per V read).
-// Used for the grouped prefix pass (many rows share one segment, §2
-// intra-batch prefix sharing) and for chunked prefill (§4.1).
+// A wide item holds up to kWideWaves * 32 query rows of one kv head against
+// a span list: a workgroup of kWideWaves waves, 32 rows per wave, all rows
+// sharing the key stream. Used for the grouped prefix pass
+// (many rows share one segment, §2 intra-batch prefix sharing) and for
+// chunked prefill (§4.1).
+//
+// Loads. Each 32-key step's K and V (two pages) are read once per
+// workgroup, by direct global-to-LDS loads into a ring of kWideStages step
+// images, so no registers hold data in transit. A step image is
+// 2 * D/32 + D/16 blocks of 1 KB (16 KB at d = 128); block k is written by
+// one load instruction whose lane L fetches the 16 bytes that lane L of
+// every wave later reads with one ds_read_b128 at L * 16, so every LDS read
+// is sequential and conflict-free. With c = L % 32, h = L / 32:
+//   K block s (dims 16s..16s+15):   page c / 16, key c % 16, unit 2s + h
+//   V block (page g, dims 32b..+31): page g, dim 32b + c, slots 8h..8h+7
+//
+// Products use v_mfma_f32_32x32x16_bf16, the shape that reaches the bf16
+// peak on gfx950 (measured 2.48 PFLOP/s, against 1.39 for 16x16x32):
+//   S^T (32 keys x 32 rows) = K Q^T, 8 products over d = 128; lane (c, h)
+//     holds row c, keys 8 (i / 4) + 4 h + i % 4 in register i;
+//   O^T (32 dims x 32 rows) += V^T P^T per page of the step: the B operand of
+//     page g is registers 8g..8g+7 of that lane, i.e. keys 8j/4 + 4h + j%4 of
+//     page g, which the V slot order keeps in 16 contiguous bytes.
+//
+// Compute. Iteration t issues the MFMAs of P V for step t-1 and of Q K^T for
+// step t+1, and meanwhile runs the softmax of step t on the VALU: the three
+// are independent, so the matrix cores and the VALU overlap inside each
+// wave (and the two waves of a SIMD fill each other's stalls).
 //
 // Softmax rescaling is lazy: a row's reference maximum only moves when a
 // step's maximum exceeds it by more than kRescaleLog2 (so weights stay below
 // 2^kRescaleLog2); the result is the same softmax, and the accumulator
 // rescale runs only on the rare steps where some row moves.
 constexpr float kRescaleLog2 = 8.f;
+constexpr int kWideStages = 6;
 
-template <int D>
-struct WideGeom {
-  static constexpr int kTileBytes = 16 * D * 2;           // one bf16 (page, head) tile
-  static constexpr int kStepBytes = 4 * kTileBytes;       // K page0, K page1, V page0, V page1
-  static constexpr int kChunksPerTile = kTileBytes / 16;  // 16-byte chunks
-  static constexpr int kPerThread = 4 * kChunksPerTile / 256;
-};
+// s_waitcnt with only the vector-memory counter limited (gfx9 encoding:
+// vmcnt low bits [3:0] and high bits [15:14]; expcnt and lgkmcnt at their
+// "no wait" maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-template <int D, int RB, typename TO>
+template <int D, typename TO>
 __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
   using T = __bf16;
   using F = bf16x8_t;
-  using G = WideGeom<D>;
-  constexpr int NS = D / 32;
-  constexpr int NB = D / 16;
+  constexpr int NK = D / 16;                      // 16-dim slices of Q K^T
+  constexpr int NO = D / 32;                      // 32-dim output blocks
+  constexpr int kBlocks = NK + 2 * NO;            // 1 KB blocks per step image
+  constexpr int kStepBytes = kBlocks * 1024;
+  static_assert(kBlocks % kWideWaves == 0, "step blocks must split evenly over the waves");
+  constexpr int kLoadsPerWave = kBlocks / kWideWaves;
+  constexpr int S = kWideStages;
+  static_assert(S >= 5 && S % 2 == 0, "the ring needs >= 5 stages, an even count keeps tile parity static");
   constexpr int64_t kTile = 16 * D;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * G::kStepBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[S][kStepBytes];
 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int col = lane & 15;
-  const int grp = lane >> 4;
+  const int c = lane & 31;
+  const int h = lane >> 5;
   const Item it = a.wide_items[item_id];
+  // waves without rows still load their share of every step image
+  const bool computes = wave * 32 < it.n_rows;
 
-  // This lane's rows: row block rb of this wave, column col.
-  Row row[RB];
-  F qf[RB][NS];
+  // This lane's row: row c of this wave's block.
+  const int r = wave * 32 + c;
+  const Row row = r < it.n_rows ? a.rows[it.row_begin + r] : Row{-1, 0, -1, 0};
+  F qf[NK];
+  {
+    const T* qp = static_cast<const T*>(a.q) + (int64_t)(row.q_row < 0 ? 0 : row.q_row) * D + 8 * h;
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int r = (wave * RB + rb) * 16 + col;
-    row[rb] = r < it.n_rows ? a.rows[it.row_begin + r] : Row{-1, 0, -1, 0};
-    const T* qp = static_cast<const T*>(a.q) + (int64_t)(row[rb].q_row < 0 ? 0 : row[rb].q_row) * D + 8 * grp;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) qf[rb][s] = row[rb].q_row >= 0 ? load8(qp + 32 * s) : zero_frag<F>();
+    for (int s = 0; s < NK; ++s) qf[s] = row.q_row >= 0 ? load8(qp + 16 * s) : zero_frag<F>();
   }
 
   const int64_t page_stride = (int64_t)a.num_kv_heads * kTile;
@@ -503,208 +598,311 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
     p.causal = cur.causal;
     const int j = (t_next - cur.kb) >> 4;
     p.has1 = t_next + 16 < cur.ke;
+    p.full = t_next + kKeysPerStep <= cur.ke && !cur.causal;
     p.pid0 = __builtin_amdgcn_readlane(cur.vpid, j);
     p.pid1 = p.has1 ? __builtin_amdgcn_readlane(cur.vpid, j + 1) : p.pid0;
     t_next += kKeysPerStep;
     return p;
   };
 
-  // ---- staging: thread t moves chunks t + 256k of the step (k < kPerThread)
-  struct Stage { u32x4_t v[G::kPerThread]; };
-  auto stage_load = [&](const StepPos& p, Stage& st) {
+  // ---- loads: this wave writes blocks wave + kWideWaves * k of a step image.
+  // Per lane: K or V, which page of the step, and the element offset inside
+  // that page's tile. Page bases are computed on the scalar unit.
+  int ld_off[kLoadsPerWave];
+  bool ld_v[kLoadsPerWave], ld_p1[kLoadsPerWave];
 #pragma unroll
-    for (int k = 0; k < G::kPerThread; ++k) {
-      const int c = threadIdx.x + 256 * k;
-      const int tile = c / G::kChunksPerTile;        // 0,1: K pages; 2,3: V pages
-      const int off = (c % G::kChunksPerTile) * 8;   // elements
-      const int pid = (tile & 1) ? p.pid1 : p.pid0;
-      const T* src = ((tile < 2) ? kbase : vbase) + (int64_t)pid * page_stride + off;
-      st.v[k] = *reinterpret_cast<const u32x4_t*>(src);
+  for (int k = 0; k < kLoadsPerWave; ++k) {
+    const int blk = wave + kWideWaves * k;
+    ld_v[k] = blk >= NK;
+    if (!ld_v[k]) {
+      ld_p1[k] = c >= 16;
+      ld_off[k] = ((2 * blk + h) * 16 + (c & 15)) * 8;
+    } else {
+      const int g = (blk - NK) / NO, b = (blk - NK) % NO;
+      ld_p1[k] = g == 1;
+      ld_off[k] = (32 * b + c) * 16 + 8 * h;
     }
-  };
-  // LDS image of a step: K tiles of both pages as stored ([D/8][16][8]),
-  // then V as 16-byte cells, one per (dim d, lane group g):
-  //   {page0 keys 4g..4g+3, page1 keys 4g..4g+3}
-  // at cell d * 4 + (g ^ ((d >> 1) & 3)): a wave's V read is then one
-  // conflict-free ds_read_b128 per output block (the XOR spreads the eight
-  // lanes served together over all banks).
-  auto stage_write = [&](const Stage& st, int buf) {
-    uint8_t* base = lds + buf * G::kStepBytes;
-#pragma unroll
-    for (int k = 0; k < G::kPerThread; ++k) {
-      const int c = threadIdx.x + 256 * k;
-      const int tile = c / G::kChunksPerTile;
-      const int chunk = c % G::kChunksPerTile;
-      if (tile < 2) {
-        *reinterpret_cast<u32x4_t*>(base + tile * G::kTileBytes + chunk * 16) = st.v[k];
-      } else {
-        const int d = chunk >> 1, h = chunk & 1, pg = tile - 2;
-        uint8_t* vb = base + 2 * G::kTileBytes + pg * 8;
-        const int sw = (d >> 1) & 3;
-        *reinterpret_cast<u32x2_t*>(vb + (d * 4 + ((2 * h) ^ sw)) * 16) = u32x2_t{st.v[k].x, st.v[k].y};
-        *reinterpret_cast<u32x2_t*>(vb + (d * 4 + ((2 * h + 1) ^ sw)) * 16) = u32x2_t{st.v[k].z, st.v[k].w};
-      }
-    }
-  };
-
-  float m[RB], lsum[RB];
-  f32x4_t acc[RB][NB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    m[rb] = kNegInf;
-    lsum[rb] = 0.f;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) acc[rb][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
-
-  auto compute = [&](const StepPos& p, int buf) {
-    const uint8_t* base = lds + buf * G::kStepBytes;
-    // All K fragments of the step first, then the QK products.
-    F kf[2][NS];
+  // Byte offsets of the step's two pages, forced onto the scalar unit (the
+  // per-lane choice between them is then one select per half).
+  auto uniform64 = [](int64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+  };
+  auto issue = [&](const StepPos& p, uint8_t* img) {
+    const int64_t o0 = uniform64((int64_t)p.pid0 * page_stride);
+    const int64_t o1 = uniform64((int64_t)p.pid1 * page_stride);
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-        kf[x][s] = __builtin_bit_cast(
-            F, *reinterpret_cast<const u32x4_t*>(base + x * G::kTileBytes + ((4 * s + grp) * 16 + col) * 16));
-    f32x4_t sacc[RB][2];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) sacc[rb][0] = sacc[rb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) sacc[rb][x] = mma(kf[x][s], qf[rb][s], sacc[rb][x]);
-    // V fragments are read now so the LDS latency overlaps the softmax.
-    F vf[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int d = 16 * b + col;
-      vf[b] = __builtin_bit_cast(
-          F, *reinterpret_cast<const u32x4_t*>(base + 2 * G::kTileBytes + (d * 4 + (grp ^ ((d >> 1) & 3))) * 16));
+    for (int k = 0; k < kLoadsPerWave; ++k) {
+      const T* base = (ld_v[k] ? vbase : kbase) + ld_off[k];
+      __builtin_amdgcn_global_load_lds(base + (ld_p1[k] ? o1 : o0), img + (wave + kWideWaves * k) * 1024, 16, 0, 0);
     }
-    const bool full = p.t0 + kKeysPerStep <= p.key_end && !p.causal;
-    F pf[RB];
+  };
+
+  float m = kNegInf, lsum = 0.f;
+  f32x16_t acc[NO];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      // raw scores (masked ones -inf); the scale is applied inside the
-      // exponent with one FMA (scale > 0, so it commutes with the max)
-      float sv[8];
-      if (full) {
+  for (int b = 0; b < NO; ++b) acc[b] = f32x16_t{};
+
+  // Key (within the step) of score register i of this lane.
+  auto skey = [&](int i) { return 8 * (i >> 2) + 4 * h + (i & 3); };
+
+  // Q K^T of one step (one accumulation chain over the 16-dim slices).
+  auto qk = [&](const uint8_t* img, f32x16_t& sacc) {
+    const uint8_t* rd = img + lane * 16;
+    F kf[NK];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) sv[j] = sacc[rb][j >> 2][j & 3];
-      } else {
-        const int lim = p.causal ? min(p.key_end, row[rb].qpos + 1) : p.key_end;
+    for (int s = 0; s < NK; ++s) kf[s] = __builtin_bit_cast(F, *reinterpret_cast<const u32x4_t*>(rd + s * 1024));
+    f32x16_t sn = f32x16_t{};
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int key = p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3);
-          sv[j] = key < lim ? sacc[rb][j >> 2][j & 3] : kNegInf;
+    for (int s = 0; s < NK; ++s) sn = mma32(kf[s], qf[s], sn);
+    sacc = sn;
+  };
+
+  // P V of one step. Keys past the span end may be NaN page tails: their V
+  // slots are zeroed (P = 0 times NaN would still poison the sum).
+  auto read_v = [&](const uint8_t* img, F (&vf)[2][NO]) {
+    const uint8_t* rd = img + lane * 16;
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int b = 0; b < NO; ++b)
+        vf[g][b] = __builtin_bit_cast(F, *reinterpret_cast<const u32x4_t*>(rd + (NK + g * NO + b) * 1024));
+  };
+  auto pv = [&](const StepPos& p, const uint8_t* img, const F (&pf)[2]) {
+    F vf[2][NO];
+    read_v(img, vf);
+    if (p.t0 + kKeysPerStep > p.key_end) {
+      const int lim = p.key_end - p.t0;
+#pragma unroll
+      for (int g = 0; g < 2; ++g)
+#pragma unroll
+        for (int b = 0; b < NO; ++b) {
+          u32x4_t w = __builtin_bit_cast(u32x4_t, vf[g][b]);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            // 32-bit word q holds slots 2q, 2q+1 = registers 8g + 2q, 8g + 2q + 1
+            const unsigned keep_lo = skey(8 * g + 2 * q) < lim ? 0xFFFFu : 0u;
+            const unsigned keep_hi = skey(8 * g + 2 * q + 1) < lim ? 0xFFFF0000u : 0u;
+            w[q] &= keep_lo | keep_hi;
+          }
+          vf[g][b] = __builtin_bit_cast(F, w);
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int b = 0; b < NO; ++b) acc[b] = mma32(vf[g][b], pf[g], acc[b]);
+  };
+
+  // Online softmax of one step's scores into P (bf16, RNE), one operand per
+  // page of the step (registers 0-7: page 0, 8-15: page 1).
+  auto softmax = [&](const StepPos& p, const f32x16_t& sacc, F (&pf)[2]) {
+    // raw scores (masked ones -inf); the scale is applied inside the exponent
+    // with one FMA (scale > 0, so it commutes with the max)
+    float sv[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sv[i] = sacc[i];
+    if (p.t0 + kKeysPerStep > p.key_end || p.causal) {
+      const int lim = (p.causal ? min(p.key_end, row.qpos + 1) : p.key_end) - p.t0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sv[i] = skey(i) < lim ? sv[i] : kNegInf;
+    }
+    float mt = sv[0];
+#pragma unroll
+    for (int i = 1; i < 16; ++i) mt = fmaxf(mt, sv[i]);
+    mt = halves_max(mt) * a.scale_log2;
+    const bool move = mt > m + kRescaleLog2;
+    if (__any(move)) {
+      const float m_new = move ? mt : m;
+      const float alpha = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - m_new);
+      lsum *= alpha;
+#pragma unroll
+      for (int b = 0; b < NO; ++b) acc[b] *= alpha;
+      m = m_new;
+    }
+    const float m_use = m == kNegInf ? 0.f : m;
+    float pr[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) pr[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[i], a.scale_log2, -m_use));
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; i += 4) ps += (pr[i] + pr[i + 1]) + (pr[i + 2] + pr[i + 3]);
+    lsum += ps;
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      float half[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) half[j] = pr[8 * g + j];
+      pf[g] = to_frag(half, (F*)nullptr);
+    }
+  };
+
+  // One iteration on full, unmasked steps as a single basic block: the 16
+  // MFMAs (P V of step t-1, Q K^T of step t+1) are interleaved with the
+  // softmax VALU work of step t, so a wave keeps issuing independent VALU
+  // instructions while each MFMA runs. The accumulator rescale, which must
+  // wait for the P V products, is returned (move) and applied afterwards.
+  auto fast_iter = [&](const uint8_t* img_pv, const uint8_t* img_qk, const F (&pf_prev)[2],
+                       const f32x16_t& sacc_cur, f32x16_t& sacc_nxt, F (&pf_cur)[2], float& alpha) {
+    const uint8_t* rk = img_qk + lane * 16;
+    F vf[2][NO], kf[NK];
+    read_v(img_pv, vf);
+#pragma unroll
+    for (int s = 0; s < NK; ++s) kf[s] = __builtin_bit_cast(F, *reinterpret_cast<const u32x4_t*>(rk + s * 1024));
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int b = 0; b < NO; ++b) acc[b] = mma32(vf[g][b], pf_prev[g], acc[b]);
+    f32x16_t sn = f32x16_t{};
+#pragma unroll
+    for (int s = 0; s < NK; ++s) sn = mma32(kf[s], qf[s], sn);
+    // softmax of step t (no masks: full step)
+    float mt = fmaxf(fmaxf(fmaxf(sacc_cur[0], sacc_cur[1]), fmaxf(sacc_cur[2], sacc_cur[3])),
+                     fmaxf(fmaxf(sacc_cur[4], sacc_cur[5]), fmaxf(sacc_cur[6], sacc_cur[7])));
+    mt = fmaxf(mt, fmaxf(fmaxf(fmaxf(sacc_cur[8], sacc_cur[9]), fmaxf(sacc_cur[10], sacc_cur[11])),
+                         fmaxf(fmaxf(sacc_cur[12], sacc_cur[13]), fmaxf(sacc_cur[14], sacc_cur[15]))));
+    mt = halves_max(mt) * a.scale_log2;
+    const bool move = mt > m + kRescaleLog2;
+    const float m_new = move ? mt : m;
+    alpha = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - m_new);
+    m = m_new;
+    const float m_use = m == kNegInf ? 0.f : m;
+    float pr[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) pr[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc_cur[i], a.scale_log2, -m_use));
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; i += 4) ps += (pr[i] + pr[i + 1]) + (pr[i + 2] + pr[i + 3]);
+    lsum = __builtin_fmaf(lsum, alpha, ps);
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      float half[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) half[j] = pr[8 * g + j];
+      pf_cur[g] = to_frag(half, (F*)nullptr);
+    }
+    sacc_nxt = sn;
+    // keep the softmax results in this block (they are consumed only after
+    // the next barrier, and would otherwise sink below the rescale branch)
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const u32x4_t w = __builtin_bit_cast(u32x4_t, pf_cur[g]);
+      asm volatile("" ::"v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]));
+    }
+    asm volatile("" ::"v"(lsum));
+    // schedule: all LDS reads first, then each MFMA followed by VALU work
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NO + NK, 0);
+#pragma unroll
+    for (int k = 0; k < 2 * NO + NK; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    }
+  };
+
+  // ---- pipeline. Step t lives in stage t % S. Iteration t:
+  //   wait for this wave's loads of step t+1 (steps t+2..t+S-3 may still be
+  //   in flight) and retire its LDS reads (lgkmcnt 0); barrier: step t+1 is
+  //   visible to every wave, and step t-2's stage is free (its V was read by
+  //   P V in iteration t-1); issue step t+S-2 into it;
+  //   MFMA: P V of step t-1, Q K^T of step t+1; VALU: softmax of step t.
+  // Score and probability tiles alternate by step parity (S is even, so the
+  // parity of each unrolled position is fixed). Positions past the end
+  // re-load the current step's pages (in bounds, never read) so the count of
+  // loads in flight stays fixed.
+  StepPos ps[S];
+  ps[0] = advance();
+  if (ps[0].valid) {
+#pragma unroll
+    for (int i = 0; i < S - 2; ++i) {
+      if (i > 0) ps[i] = advance();
+      issue(pick(ps[i].valid, ps[i], ps[0]), lds[i]);
+    }
+    f32x16_t sacc[2];
+    F pf[2][2];
+    wait_vmcnt<(S - 3) * kLoadsPerWave>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (computes) qk(lds[0], sacc[0]);
+    bool first = true, done = false;
+    while (!done) {
+#pragma unroll
+      for (int st = 0; st < S; ++st) {
+        const int cur_p = st & 1, nxt_p = cur_p ^ 1;
+        const int nx = (st + 1) % S, pv_st = (st + S - 1) % S, fr = (st + S - 2) % S;
+        wait_vmcnt<(S - 4) * kLoadsPerWave>();
+        wait_lgkmcnt0();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        ps[fr] = advance();
+        issue(pick(ps[fr].valid, ps[fr], ps[st]), lds[fr]);
+        const bool more = ps[nx].valid;
+        const bool fast = !first && more && ps[st].full && ps[pv_st].full;
+        if (computes && fast) {
+          float alpha;
+          fast_iter(lds[pv_st], lds[nx], pf[nxt_p], sacc[cur_p], sacc[nxt_p], pf[cur_p], alpha);
+          if (__any(alpha != 1.f)) {
+#pragma unroll
+            for (int b = 0; b < NO; ++b) acc[b] *= alpha;
+          }
+        } else if (computes) {
+          if (!first) pv(ps[pv_st], lds[pv_st], pf[nxt_p]);
+          if (more) qk(lds[nx], sacc[nxt_p]);
+          softmax(ps[st], sacc[cur_p], pf[cur_p]);
+          if (!more) pv(ps[st], lds[st], pf[cur_p]);
+        }
+        first = false;
+        if (!more) {
+          done = true;
+          break;
         }
       }
-      float mt = sv[0];
-#pragma unroll
-      for (int j = 1; j < 8; ++j) mt = fmaxf(mt, sv[j]);
-      mt = fmaxf(mt, __shfl_xor(mt, 16));
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      mt *= a.scale_log2;
-      const bool move = mt > m[rb] + kRescaleLog2;
-      if (__any(move)) {
-        const float m_new = move ? mt : m[rb];
-        const float alpha = m[rb] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m[rb] - m_new);
-        lsum[rb] *= alpha;
-#pragma unroll
-        for (int b = 0; b < NB; ++b) acc[rb][b] *= alpha;
-        m[rb] = m_new;
-      }
-      const float m_use = m[rb] == kNegInf ? 0.f : m[rb];
-      float pr[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        pr[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j], a.scale_log2, -m_use));
-        lsum[rb] += pr[j];
-      }
-      pf[rb] = to_frag(pr, (F*)nullptr);
-    }
-    if (!full) {
-      // keys past the span end may be NaN page tails: zero V there
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (p.t0 + 16 * (j >> 2) + 4 * grp + (j & 3) >= p.key_end)
-#pragma unroll
-          for (int b = 0; b < NB; ++b) vf[b][j] = (T)0.f;
-    }
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) acc[rb][b] = mma(vf[b], pf[rb], acc[rb][b]);
-  };
-
-  // ---- pipeline: LDS buffers 0/1, register stages r0/r1, two steps ahead
-  StepPos p0 = advance();
-  StepPos p1 = advance();
-  if (p0.valid) {
-    Stage r0, r1;
-    stage_load(p0, r0);
-    stage_load(pick(p1.valid, p1, p0), r1);
-    stage_write(r0, 0);
-    __syncthreads();
-    while (true) {
-      StepPos p2 = advance();
-      stage_load(pick(p2.valid, p2, p0), r0);
-      compute(p0, 0);
-      if (!p1.valid) break;
-      stage_write(r1, 1);
-      __syncthreads();
-      StepPos p3 = advance();
-      stage_load(pick(p3.valid, p3, p1), r1);
-      compute(p1, 1);
-      if (!p2.valid) break;
-      stage_write(r0, 0);
-      __syncthreads();
-      p0 = p2;
-      p1 = p3;
     }
   }
+  // drain the loads still in flight before the workgroup's LDS is released
+  wait_vmcnt<0>();
 
-  // ---- epilogue
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    float l = lsum[rb];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int r = (wave * RB + rb) * 16 + col;
+  // ---- epilogue: lane (c, h) holds dims 32b + 8(i/4) + 4h + i%4 of row c
+  const float l = halves_sum(lsum);
+  if (computes && r < it.n_rows) {
     const float inv = l > 0.f ? 1.f / l : 0.f;
-    const float lse2 = l > 0.f ? m[rb] + __log2f(l) : kNegInf;
+    const float lse2 = l > 0.f ? m + __log2f(l) : kNegInf;
     if (it.part_base >= 0) {
-      if (r < it.n_rows) {
-        const int64_t prow = (int64_t)it.part_base + r;
-        float* dst = a.part_o + prow * D + 4 * grp;
+      const int64_t prow = (int64_t)it.part_base + r;
+      float* dst = a.part_o + prow * D + 4 * h;
 #pragma unroll
-        for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[rb][b] * inv);
-        if (grp == 0) a.part_lse[prow] = lse2;
-      }
-    } else if (r < it.n_rows) {
-      TO* dst = static_cast<TO*>(a.o) + (int64_t)row[rb].q_row * D + 4 * grp;
+      for (int b = 0; b < NO; ++b)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[rb][b] * inv);
-      if (grp == 0 && a.lse) a.lse[row[rb].q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
+        for (int q = 0; q < 4; ++q)
+          store4(dst + 32 * b + 8 * q, f32x4_t{acc[b][4 * q], acc[b][4 * q + 1], acc[b][4 * q + 2], acc[b][4 * q + 3]} * inv);
+      if (h == 0) a.part_lse[prow] = lse2;
+    } else {
+      TO* dst = static_cast<TO*>(a.o) + (int64_t)row.q_row * D + 4 * h;
+#pragma unroll
+      for (int b = 0; b < NO; ++b)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          store4(dst + 32 * b + 8 * q, f32x4_t{acc[b][4 * q], acc[b][4 * q + 1], acc[b][4 * q + 2], acc[b][4 * q + 3]} * inv);
+      if (h == 0 && a.lse) a.lse[row.q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
     }
   }
 }
 
 // ---------------------------------------------------------------- launch
 // One launch runs both roles: the first wide_blocks blocks are wide items
-// (MFMA/LDS-bound grouped prefix or prefill work), the rest hold four narrow
-// items each (mostly HBM-bound suffix streaming), so the two kinds of work
+// (MFMA/LDS-bound grouped prefix or prefill work), the rest hold one narrow
+// item per wave (mostly HBM-bound suffix streaming), so the two kinds of work
 // overlap on the GPU. RB = 0: no wide role (fp32 inputs).
 // The grid is dealt in rounds of 8 blocks (one per XCD); rounds of the two
 // roles are spread evenly over the launch so every CU mixes MFMA-heavy wide
 // blocks with HBM-heavy narrow ones, and within a role the block index modulo
 // 8 still names the XCD (xcd_remap stays valid).
 template <typename T, int D, typename TO, int RB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 ? 2 : 1)))
+__global__ __launch_bounds__(64 * block_waves<T>())
+__attribute__((amdgpu_waves_per_eu(block_waves<T>() / 4)))
 void attn_kernel(AttnArgs a) {
+  static_assert(RB == 0 || block_waves<T>() == kWideWaves, "wide items need kWideWaves-wave blocks");
   const int b = blockIdx.x;
   const int x = b & 7, r = b >> 3;
   if constexpr (RB > 0) {
@@ -714,7 +912,7 @@ void attn_kernel(AttnArgs a) {
     const int w_upto = (int)((int64_t)(r + 1) * wr / tr);
     if (w_upto > w_before) {
       const int item = xcd_remap(w_before * 8 + x, a.wide_group);
-      if (item < a.n_wide) wide_item<D, RB, TO>(a, item);
+      if (item < a.n_wide) wide_item<D, TO>(a, item);
       return;
     }
     narrow_block<T, D, TO>(a, xcd_remap((r - w_upto) * 8 + x, a.narrow_group));
@@ -846,9 +1044,9 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
       if (!a.v_layout) {           // K: [D/E][16][E]
         c = (e / (16 * E)) * E + e % E;
         t = (e / E) % 16;
-      } else {                     // V: [D][16]
+      } else {                     // V: [D][16], slots hold tokens 0-3, 8-11, 4-7, 12-15
         c = e >> 4;
-        t = e & 15;
+        t = v_token_at_slot(e & 15);
       }
       tile[t * (D + 1) + c] = src[e];
     }
@@ -879,18 +1077,20 @@ template <typename T, int D, typename TO>
 void launch_attention(AttnArgs args, const MergeArgs& margs, int wide_rb, hipStream_t stream) {
   const int rb = sizeof(T) == 2 ? wide_rb : 0;
   args.wide_blocks = (rb > 0 && args.n_wide > 0) ? pad_to(args.n_wide, 8 * args.wide_group) : 0;
-  args.narrow_blocks = args.n_items > 0 ? pad_to((args.n_items + 3) / 4, 8 * args.narrow_group) : 0;
+  constexpr int W = block_waves<T>();
+  args.narrow_per_block = std::min(std::max(args.narrow_per_block, 1), W);
+  args.narrow_blocks = args.n_items > 0 ? pad_to((args.n_items + args.narrow_per_block - 1) / args.narrow_per_block,
+                                                 8 * args.narrow_group)
+                                        : 0;
   const int grid = args.wide_blocks + args.narrow_blocks;
   if (grid > 0) {
     if constexpr (sizeof(T) == 2) {
-      if (rb == 2)
-        hipLaunchKernelGGL((attn_kernel<T, D, TO, 2>), dim3(grid), dim3(256), 0, stream, args);
-      else if (rb == 1)
-        hipLaunchKernelGGL((attn_kernel<T, D, TO, 1>), dim3(grid), dim3(256), 0, stream, args);
+      if (rb > 0)
+        hipLaunchKernelGGL((attn_kernel<T, D, TO, 1>), dim3(grid), dim3(64 * W), 0, stream, args);
       else
-        hipLaunchKernelGGL((attn_kernel<T, D, TO, 0>), dim3(grid), dim3(256), 0, stream, args);
+        hipLaunchKernelGGL((attn_kernel<T, D, TO, 0>), dim3(grid), dim3(64 * W), 0, stream, args);
     } else {
-      hipLaunchKernelGGL((attn_kernel<T, D, TO, 0>), dim3(grid), dim3(256), 0, stream, args);
+      hipLaunchKernelGGL((attn_kernel<T, D, TO, 0>), dim3(grid), dim3(64 * W), 0, stream, args);
     }
   }
   if (margs.n_merge > 0) {
@@ -936,7 +1136,7 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                 reinterpret_cast<const Item*>(m + L.wide_items),
                 reinterpret_cast<const Span*>(m + L.spans),
                 reinterpret_cast<const Row*>(m + L.rows),
-                plan->n_items, plan->n_wide, 0, 0, plan->wide_group, plan->narrow_group,
+                plan->n_items, plan->n_wide, 0, 0, plan->narrow_per_block, plan->wide_group, plan->narrow_group,
                 p.num_kv_heads, p.sm_scale * kLog2e};
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),

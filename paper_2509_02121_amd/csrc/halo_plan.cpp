@@ -263,10 +263,11 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     int kc = kc_shared;
     if (wide) {
       const double avg_rows = wsum > 0 ? wrows / wsum : 0;
-      int rb = avg_rows >= 128 ? 2 : 1;
-      rb = env_int("HALO_WIDE_RB", rb, 1, 2);
-      plan->wide_rb = rb;
-      rows_per = 64 * rb;
+      plan->wide_rb = 1;
+      // rows per wide item: the row-weighted group size rounded up to whole
+      // 32-row waves, at most one workgroup
+      rows_per = (int)std::min<double>(kMaxWideRows, std::max(32.0, std::ceil(avg_rows / 32.0) * 32.0));
+      rows_per = env_int("HALO_WIDE_ROWS", rows_per, 32, kMaxWideRows) / 32 * 32;
       // row groups of one shared chunk read the same pages: keep up to 8 of
       // them on one XCD
       plan->wide_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / rows_per)));
@@ -286,10 +287,10 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       // 16-row items of one shared chunk are consecutive: keep the blocks
       // holding them on one XCD
       const double avg_rows = wsum > 0 ? wrows / wsum : 0;
-      plan->narrow_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / (4.0 * kRowsPerItem))));
+      const double block_rows = (double)narrow_items_per_block(p.kv_dtype) * kRowsPerItem;
+      plan->narrow_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / block_rows)));
     }
     plan->narrow_group = env_int("HALO_NARROW_GROUP", plan->narrow_group, 1, 64);
-    plan->wide_group = env_int("HALO_WIDE_GROUP", plan->wide_group, 1, 64);
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
       std::vector<Span> sp;
@@ -350,12 +351,11 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         }
     }
   } else {
-    // Prefill: bf16 rows go to wide items of 64 * rb (query, head) rows.
+    // Prefill: bf16 rows go to wide items of up to kMaxWideRows (query, head) rows.
     const bool wide = p.kv_dtype == HALO_BF16 && env_int("HALO_WIDE", 1, 0, 1) == 1;
-    int rb = env_int("HALO_WIDE_RB", 2, 1, 2);
-    plan->wide_rb = wide ? rb : 0;
+    plan->wide_rb = wide ? 1 : 0;
     plan->wide_group = 1;
-    const int rows_per = wide ? 64 * rb : kRowsPerItem;
+    const int rows_per = wide ? env_int("HALO_WIDE_ROWS", kMaxWideRows, 32, kMaxWideRows) / 32 * 32 : kRowsPerItem;
     for (int r = 0; r < R; ++r) {
       const int32_t n = f.q_len[r];
       if (n == 0) continue;
@@ -493,6 +493,15 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   }
 
   plan->n_items = (int32_t)items.size();
+  // Narrow items per workgroup (one per wave): each CU streams only ~30 GB/s,
+  // so a small batch spreads its items over every CU (about 256 workgroups)
+  // instead of filling workgroups; a large batch fills them.
+  {
+    const int cap = narrow_items_per_block(p.kv_dtype);
+    int per = (int)std::min<int64_t>(cap, std::max<int64_t>(1, (int64_t)items.size() / 256));
+    if (items.size() < 4096) per = std::min(per, 4);
+    plan->narrow_per_block = env_int("HALO_NARROW_PER_BLOCK", per, 1, cap);
+  }
   plan->n_wide = (int32_t)witems.size();
   if (plan->n_wide == 0) plan->wide_rb = 0;
   plan->n_spans = (int32_t)spans.size();

@@ -375,19 +375,23 @@ def test_pool_pages_hold_the_logical_tokens():
     w = make_config(0)
     kp = w.k_pool.numpy()
     vp = w.v_pool.numpy()
+
+    def vslot(t):   # V rows keep tokens 0-3, 8-11, 4-7, 12-15: bits 2 and 3 swapped
+        return (t & 3) | ((t & 4) << 1) | ((t & 8) >> 1)
     for s in range(len(w.seg_len)):
         n = int(w.seg_len[s])
         pages = np.asarray(w.seg_pages[s])
         k_np = np.stack([kp[pages[t // 16], :, :, t % 16, :].reshape(kp.shape[1], -1)
                          for t in range(n)])
-        v_np = np.stack([vp[pages[t // 16], :, :, t % 16] for t in range(n)])
+        v_np = np.stack([vp[pages[t // 16], :, :, vslot(t % 16)] for t in range(n)])
         k, v = w.segment_kv(s)
         assert np.array_equal(k.numpy(), k_np) and np.array_equal(v.numpy(), v_np)
         assert not np.isnan(k_np).any()
         tail = n % 16
         if tail:
             assert np.isnan(kp[pages[-1], :, :, tail:, :]).all()
-            assert np.isnan(vp[pages[-1], :, :, tail:]).all()
+            assert np.isnan(vp[pages[-1], :, :, [vslot(t) for t in range(tail, 16)]]).all()
+            assert not np.isnan(vp[pages[-1], :, :, [vslot(t) for t in range(tail)]]).any()
 
 
 def test_page_placement_does_not_change_oracle_output():
@@ -397,13 +401,16 @@ def test_page_placement_does_not_change_oracle_output():
     paths = [[0, 1], [0, 2]]
     a = build_workload("a", 5, 4, 2, 8, torch.float32, seg_len, paths, exact_pool=True)
     b = build_workload("b", 6, 4, 2, 8, torch.float32, seg_len, paths, capacity_factor=3.0)
+    def vslot(t):
+        return (t & 3) | ((t & 4) << 1) | ((t & 8) >> 1)
+
     # copy a's logical tokens into b's placement
     for s in range(3):
         k, v = a.segment_kv(s)
         for t in range(seg_len[s]):
             p = int(b.seg_pages[s][t // 16])
             b.k_pool[p, :, :, t % 16, :] = k[t].reshape(b.k_pool.shape[1], -1, b.k_pool.shape[-1])
-            b.v_pool[p, :, :, t % 16] = v[t]
+            b.v_pool[p, :, :, vslot(t % 16)] = v[t]
     for w in (a, b):
         w.q = a.q.clone()
     outs = []

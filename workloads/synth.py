@@ -10,7 +10,9 @@ Page pools (the layout the library reads):
   k_pool: [P, H_kv, d/E, page_size, E]  16-byte units of E elements (E = 8
                                         for bf16, 4 for fp32), token-major
                                         inside each unit column
-  v_pool: [P, H_kv, d, page_size]       dim-major inside a (page, head) tile
+  v_pool: [P, H_kv, d, page_size]       dim-major inside a (page, head) tile;
+                                        the 16 slots of a dim row hold tokens
+                                        0-3, 8-11, 4-7, 12-15 (V_SLOT_OF_TOKEN)
 Unused pages and the tail slots of a segment's last page are NaN when
 ``poison`` is set, so any read of them shows up in the results.
 
@@ -26,6 +28,10 @@ import numpy as np
 import torch
 
 PAGE_SIZE = 16
+
+# Slot of token t inside a V dim row (slots 4-7 and 8-11 swapped, i.e. bits 2
+# and 3 of the index exchanged; the map is its own inverse).
+V_SLOT_OF_TOKEN = np.array([0, 1, 2, 3, 8, 9, 10, 11, 4, 5, 6, 7, 12, 13, 14, 15], dtype=np.int64)
 
 # Workloads by name, in the order they are numbered (seed = 1000 + index).
 CONFIG_NAMES = (
@@ -90,6 +96,7 @@ class Workload:
         pages = torch.as_tensor(np.asarray(self.seg_pages[s], np.int64))
         kp = self.k_pool[pages.to(self.k_pool.device)].cpu()   # [n, H, d/E, ps, E]
         vp = self.v_pool[pages.to(self.v_pool.device)].cpu()   # [n, H, d, ps]
+        vp = vp[..., torch.as_tensor(V_SLOT_OF_TOKEN)]          # slot order -> token order
         k = kp.permute(0, 3, 1, 2, 4).reshape(-1, self.num_kv_heads, self.head_dim)
         v = vp.permute(0, 3, 1, 2).reshape(-1, self.num_kv_heads, self.head_dim)
         return k[:length].contiguous(), v[:length].contiguous()
@@ -183,7 +190,7 @@ def build_workload(name, seed, num_q_heads, num_kv_heads, head_dim, dtype,
             if tail and n_pages[s]:
                 p = int(seg_pages[s][-1])
                 k_pool[p, :, :, tail:, :] = float("nan")
-                v_pool[p, :, :, tail:] = float("nan")
+                v_pool[p, :, :, torch.as_tensor(V_SLOT_OF_TOKEN[tail:], device=device)] = float("nan")
 
     return Workload(name=name, seed=int(seed), num_q_heads=num_q_heads,
                     num_kv_heads=num_kv_heads, head_dim=head_dim, dtype=dtype,
