@@ -189,7 +189,9 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
  * for inspection and host-side testing of the work lists. Byte offsets of
  * each int32 array inside the image, and the element counts:
  *   items, wide_items: n_items / n_wide x {row_begin, n_rows, span_begin,
- *                       n_spans, kv_head, part_base (-1: final rows), keys, unused}
+ *                       n_spans, kv_head, part_base (-1: final rows), keys, flags}
+ *   block_items [n_narrow_blocks + 1]: narrow workgroup b runs items
+ *                       block_items[b] .. block_items[b + 1] - 1
  *   spans:  n_spans  x {segment, key_begin, key_end, causal, page-table offset,
  *                       unused x 3}; a span covers at most 1024 keys
  *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position,
@@ -199,8 +201,8 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
  * *image stays valid until halo_plan_destroy. */
 typedef struct {
   uint64_t seg_page_off, seg_len, page_ids, items, wide_items, spans, rows;
-  uint64_t merge_rows, merge_indptr, merge_parts, total_bytes;
-  int32_t n_items, n_wide, n_spans, n_rows, n_merge, n_merge_parts, n_pages;
+  uint64_t merge_rows, merge_indptr, merge_parts, total_bytes, block_items;
+  int32_t n_items, n_wide, n_spans, n_rows, n_merge, n_merge_parts, n_pages, n_narrow_blocks;
 } halo_plan_layout_t;
 
 halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void** image,

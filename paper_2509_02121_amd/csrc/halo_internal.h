@@ -17,6 +17,12 @@ constexpr int kWideWaves = 8;
 constexpr int kMaxWideRows = kWideWaves * 32;
 // Narrow items per workgroup (one per wave): 8 for bf16, 4 for fp32.
 inline int narrow_items_per_block(halo_dtype_t dt) { return dt == HALO_BF16 ? 8 : 4; }
+// Compute units of an MI355X: a decode plan with no wide items launches one
+// narrow workgroup per CU.
+constexpr int kNumCUs = 256;
+// Fixed cost of one narrow item (metadata, Q load, output write), counted in
+// keys when items are dealt to workgroups.
+constexpr int kItemOverheadKeys = 64;
 // Keys consumed per inner step: two pages of 16 (one K=32 MFMA for P*V).
 constexpr int kKeysPerStep = 32;
 
@@ -64,7 +70,8 @@ struct MetaLayout {
   size_t seg_page_off = 0;   // int32 [S]  first page slot of each segment
   size_t seg_len = 0;        // int32 [S]
   size_t page_ids = 0;       // int32 [total pages]
-  size_t items = 0;          // Item  [n_items]     narrow (one wavefront)
+  size_t items = 0;          // Item  [n_items]     narrow (one wavefront), grouped by workgroup
+  size_t block_items = 0;    // int32 [n_narrow_blocks + 1] first item of each narrow workgroup
   size_t wide_items = 0;     // Item  [n_wide]      wide (one 4-wave workgroup)
   size_t spans = 0;          // Span  [n_spans]
   size_t rows = 0;           // Row   [n_rows]
@@ -86,8 +93,8 @@ struct halo_plan {
   int32_t n_wide = 0;
   int32_t wide_rb = 0;       // 1 when the plan has wide items (32 rows per wave), else 0
   int32_t wide_group = 1;    // wide items that share pages, kept on one XCD
-  int32_t narrow_group = 1;  // narrow blocks that share pages, kept on one XCD
-  int32_t narrow_per_block = 1;  // narrow items per workgroup (one per wave)
+  int32_t n_narrow_blocks = 0;  // workgroups the narrow items are dealt to (a multiple of 8),
+                                // at most one item per wave
   int32_t n_shared_items = 0;
   int32_t n_merge = 0;
   int32_t n_spans = 0;

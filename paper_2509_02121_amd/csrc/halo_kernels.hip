@@ -194,17 +194,16 @@ struct AttnArgs {
   const int32_t* seg_page_off;
   const int32_t* seg_len;
   const int32_t* page_ids;
-  const Item* items;        // narrow items (one wavefront each)
-  const Item* wide_items;   // wide items (one 4-wave workgroup each)
+  const Item* items;        // narrow items (one wavefront each), grouped by workgroup
+  const int32_t* block_items;  // [narrow_blocks + 1]: first item of each narrow workgroup
+  const Item* wide_items;   // wide items (one workgroup each)
   const Span* spans;
   const Row* rows;
   int32_t n_items;
   int32_t n_wide;
   int32_t wide_blocks;     // grid blocks of the wide role (n_wide padded, see xcd_remap)
-  int32_t narrow_blocks;   // grid blocks of the narrow role (narrow_per_block items each, padded)
-  int32_t narrow_per_block;  // narrow items per block, one per wave (the other waves exit)
+  int32_t narrow_blocks;   // grid blocks of the narrow role (a multiple of 8)
   int32_t wide_group;      // consecutive wide items kept on one XCD
-  int32_t narrow_group;    // consecutive narrow blocks kept on one XCD
   int32_t num_kv_heads;
   float scale_log2;   // sm_scale * log2(e)
 };
@@ -469,12 +468,14 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
 // one wave per SIMD.
 template <typename T> constexpr int block_waves() { return sizeof(T) == 2 ? 8 : 4; }
 
-// One narrow item per wave of the block.
+// Narrow workgroup `block` runs items block_items[block] ..
+// block_items[block + 1] - 1 (dealt by the planner), one per wave; waves past
+// the count exit.
 template <typename T, int D, typename TO>
 __device__ __forceinline__ void narrow_block(const AttnArgs& a, int block) {
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const int item_id = block * a.narrow_per_block + wave;
-  if (wave >= a.narrow_per_block || item_id >= a.n_items) return;
+  const int item_id = a.block_items[block] + wave;
+  if (item_id >= a.block_items[block + 1]) return;
   const Item it = a.items[item_id];
   if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, threadIdx.x & 63);
   else run_item<T, D, TO, false, 2>(a, it, threadIdx.x & 63);
@@ -890,14 +891,15 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
 }
 
 // ---------------------------------------------------------------- launch
-// One launch runs both roles: the first wide_blocks blocks are wide items
-// (MFMA/LDS-bound grouped prefix or prefill work), the rest hold one narrow
-// item per wave (mostly HBM-bound suffix streaming), so the two kinds of work
-// overlap on the GPU. RB = 0: no wide role (fp32 inputs).
+// One launch runs both roles: wide workgroups (MFMA/LDS-bound grouped
+// prefix or prefill work) and narrow ones (lists of one-wave items, mostly
+// HBM-bound suffix streaming), so the two kinds of work overlap on the GPU.
+// RB = 0: no wide role.
 // The grid is dealt in rounds of 8 blocks (one per XCD); rounds of the two
 // roles are spread evenly over the launch so every CU mixes MFMA-heavy wide
 // blocks with HBM-heavy narrow ones, and within a role the block index modulo
-// 8 still names the XCD (xcd_remap stays valid).
+// 8 still names the XCD (xcd_remap, and the planner's dealing of narrow
+// items to XCDs, rely on it).
 template <typename T, int D, typename TO, int RB>
 __global__ __launch_bounds__(64 * block_waves<T>())
 __attribute__((amdgpu_waves_per_eu(block_waves<T>() / 4)))
@@ -915,9 +917,9 @@ void attn_kernel(AttnArgs a) {
       if (item < a.n_wide) wide_item<D, TO>(a, item);
       return;
     }
-    narrow_block<T, D, TO>(a, xcd_remap((r - w_upto) * 8 + x, a.narrow_group));
+    narrow_block<T, D, TO>(a, (r - w_upto) * 8 + x);
   } else {
-    narrow_block<T, D, TO>(a, xcd_remap(b, a.narrow_group));
+    narrow_block<T, D, TO>(a, b);
   }
 }
 
@@ -1078,10 +1080,6 @@ void launch_attention(AttnArgs args, const MergeArgs& margs, int wide_rb, hipStr
   const int rb = sizeof(T) == 2 ? wide_rb : 0;
   args.wide_blocks = (rb > 0 && args.n_wide > 0) ? pad_to(args.n_wide, 8 * args.wide_group) : 0;
   constexpr int W = block_waves<T>();
-  args.narrow_per_block = std::min(std::max(args.narrow_per_block, 1), W);
-  args.narrow_blocks = args.n_items > 0 ? pad_to((args.n_items + args.narrow_per_block - 1) / args.narrow_per_block,
-                                                 8 * args.narrow_group)
-                                        : 0;
   const int grid = args.wide_blocks + args.narrow_blocks;
   if (grid > 0) {
     if constexpr (sizeof(T) == 2) {
@@ -1133,10 +1131,11 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                 reinterpret_cast<const int32_t*>(m + L.seg_len),
                 reinterpret_cast<const int32_t*>(m + L.page_ids),
                 reinterpret_cast<const Item*>(m + L.items),
+                reinterpret_cast<const int32_t*>(m + L.block_items),
                 reinterpret_cast<const Item*>(m + L.wide_items),
                 reinterpret_cast<const Span*>(m + L.spans),
                 reinterpret_cast<const Row*>(m + L.rows),
-                plan->n_items, plan->n_wide, 0, 0, plan->narrow_per_block, plan->wide_group, plan->narrow_group,
+                plan->n_items, plan->n_wide, 0, plan->n_narrow_blocks, plan->wide_group,
                 p.num_kv_heads, p.sm_scale * kLog2e};
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),

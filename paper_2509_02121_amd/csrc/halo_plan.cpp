@@ -23,6 +23,7 @@
 #include <cstring>
 #include <limits>
 #include <new>
+#include <queue>
 #include <string>
 #include <vector>
 
@@ -214,8 +215,10 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     int64_t keys;
     bool shared;
     bool wide;
+    int32_t chunk = -1;   // shared items: id of the (piece, kv head) whose pages they read
   };
   std::vector<Proto> protos;
+  int32_t n_chunks = 0;
 
   if (!prefill) {
     const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, kMaxSpanKeys) / 32 * 32;
@@ -283,14 +286,6 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       }
       kc = env_int("HALO_KC_WIDE", kc, 32, kMaxSpanKeys) / 32 * 32;
     }
-    if (!wide) {
-      // 16-row items of one shared chunk are consecutive: keep the blocks
-      // holding them on one XCD
-      const double avg_rows = wsum > 0 ? wrows / wsum : 0;
-      const double block_rows = (double)narrow_items_per_block(p.kv_dtype) * kRowsPerItem;
-      plan->narrow_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / block_rows)));
-    }
-    plan->narrow_group = env_int("HALO_NARROW_GROUP", plan->narrow_group, 1, 64);
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
       std::vector<Span> sp;
@@ -301,7 +296,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
           for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, 0});
         // chunk-major, row group innermost: items reading the same pages
         // are neighbours in the launch order.
-        for (const Span& piece : sp)
+        for (const Span& piece : sp) {
           for (size_t rb = 0; rb < rows.size(); rb += rows_per) {
             Proto pr;
             pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
@@ -310,8 +305,11 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
             pr.keys = piece.key_end - piece.key_begin;
             pr.shared = true;
             pr.wide = wide;
+            pr.chunk = n_chunks;
             protos.push_back(std::move(pr));
           }
+          n_chunks++;
+        }
       }
     }
     // Suffix pass: each request's private keys, in chunks.
@@ -421,13 +419,17 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     is_final[i] = prefill || all_one;
   }
 
-  // Longest items first (stable: sharing neighbours stay together).
+  // Shared items first, then private ones; longest first within each class
+  // (stable: items reading the same pages stay neighbours).
   std::vector<size_t> order(protos.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = i;
-  std::stable_sort(order.begin(), order.end(),
-                   [&](size_t a, size_t b) { return protos[a].keys > protos[b].keys; });
+  std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) {
+    if (protos[a].shared != protos[b].shared) return protos[a].shared;
+    return protos[a].keys > protos[b].keys;
+  });
 
   std::vector<Item> items, witems;
+  std::vector<int32_t> item_chunk;   // per narrow item: its proto's chunk id
   std::vector<Span> spans;
   std::vector<Row> rows;
   std::vector<std::vector<int32_t>> row_parts(prefill ? 0 : n_q_rows * Hq);
@@ -467,6 +469,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       }
     it.n_spans = (int32_t)spans.size() - it.span_begin;
     (pr.wide ? witems : items).push_back(it);
+    if (!pr.wide) item_chunk.push_back(pr.chunk);
   }
 
   // Merge list: every decode row no final item writes, i.e. every row with
@@ -493,15 +496,92 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   }
 
   plan->n_items = (int32_t)items.size();
-  // Narrow items per workgroup (one per wave): each CU streams only ~30 GB/s,
-  // so a small batch spreads its items over every CU (about 256 workgroups)
-  // instead of filling workgroups; a large batch fills them.
-  {
-    const int cap = narrow_items_per_block(p.kv_dtype);
-    int per = (int)std::min<int64_t>(cap, std::max<int64_t>(1, (int64_t)items.size() / 256));
-    if (items.size() < 4096) per = std::min(per, 4);
-    plan->narrow_per_block = env_int("HALO_NARROW_PER_BLOCK", per, 1, cap);
+  // Narrow items are dealt to workgroups ahead of time, at most `cap` to a
+  // workgroup (one per wave; the waves past its count exit). A CU ingests
+  // only ~30 GB/s from HBM (~70 GB/s from L2), so a small batch is spread
+  // over every CU (at least 256 workgroups of 8 waves, one per CU) and
+  // items go longest first to the least loaded workgroup. Beside wide
+  // workgroups, narrow ones take half their waves' worth of items.
+  // Workgroup b runs on XCD b % 8 (dispatch is round-robin), and the row
+  // groups of one shared chunk go to workgroups of one XCD, in units of up
+  // to shared_unit items on one workgroup, so re-reads of the chunk hit that
+  // XCD's L2 or the CU's L1.
+  std::vector<int32_t> block_items{0};
+  if (!items.empty()) {
+    const int waves = narrow_items_per_block(p.kv_dtype);
+    const int64_t n = (int64_t)items.size();
+    const int cap = env_int("HALO_ITEMS_PER_BLOCK", witems.empty() ? waves : std::max(1, waves / 2), 1, waves);
+    int64_t nb = std::max<int64_t>((n + cap - 1) / cap, std::min<int64_t>(n, kNumCUs));
+    nb = (nb + 7) / 8 * 8;
+    const int shared_unit = std::min(cap, env_int("HALO_SHARED_UNIT", 4, 1, 64));
+    // work units: runs of up to shared_unit items of one chunk, or one item
+    struct Unit { int32_t first, count, chunk; int64_t cost; };
+    std::vector<Unit> units;
+    auto cost_of = [&](const Item& it) { return (int64_t)it.keys + kItemOverheadKeys; };
+    for (int32_t i = 0; i < (int32_t)n; ++i) {
+      const int32_t c = item_chunk[i];
+      if (c >= 0 && !units.empty() && units.back().chunk == c && units.back().count < shared_unit &&
+          units.back().first + units.back().count == i) {
+        units.back().count++;
+        units.back().cost += cost_of(items[i]);
+      } else {
+        units.push_back(Unit{i, 1, c, cost_of(items[i])});
+      }
+    }
+    std::stable_sort(units.begin(), units.end(), [](const Unit& a, const Unit& b) { return a.cost > b.cost; });
+    // one min-heap of (load, block) per XCD over the blocks with room left
+    using Slot = std::pair<int64_t, int32_t>;
+    std::vector<std::priority_queue<Slot, std::vector<Slot>, std::greater<Slot>>> heap(8);
+    for (int32_t b = 0; b < (int32_t)nb; ++b) heap[b % 8].push(Slot{0, b});
+    std::vector<std::vector<int32_t>> blk(nb);
+    // place `count` items from `first` on the least loaded block of XCD x
+    // with room for them; false if there is none
+    auto place_on = [&](int x, int32_t first, int32_t count, int64_t cost) {
+      std::vector<Slot> aside;
+      bool ok = false;
+      while (!heap[x].empty()) {
+        Slot s0 = heap[x].top();
+        heap[x].pop();
+        if ((int)blk[s0.second].size() + count <= cap) {
+          for (int32_t k = 0; k < count; ++k) blk[s0.second].push_back(first + k);
+          s0.first += cost;
+          if ((int)blk[s0.second].size() < cap) heap[x].push(s0);
+          ok = true;
+          break;
+        }
+        aside.push_back(s0);
+      }
+      for (const Slot& s0 : aside) heap[x].push(s0);
+      return ok;
+    };
+    auto least_loaded_xcd = [&]() {
+      int x = -1;
+      for (int y = 0; y < 8; ++y)
+        if (!heap[y].empty() && (x < 0 || heap[y].top() < heap[x].top())) x = y;
+      return x;
+    };
+    for (const Unit& u : units) {
+      if (u.chunk >= 0 && place_on(u.chunk % 8, u.first, u.count, u.cost)) continue;
+      const int x = least_loaded_xcd();
+      if (x >= 0 && place_on(x, u.first, u.count, u.cost)) continue;
+      // no block has room for the whole unit: deal its items one by one
+      for (int32_t k = 0; k < u.count; ++k) {
+        const int y = least_loaded_xcd();
+        if (y < 0 || !place_on(y, u.first + k, 1, cost_of(items[u.first + k]))) {
+          delete plan;
+          return fail(HALO_ERR_INVALID_ARGUMENT, "internal: narrow items do not fit their workgroups");
+        }
+      }
+    }
+    std::vector<Item> dealt;
+    dealt.reserve(n);
+    for (auto& list : blk) {
+      for (int32_t i : list) dealt.push_back(items[i]);
+      block_items.push_back((int32_t)dealt.size());
+    }
+    items.swap(dealt);
   }
+  plan->n_narrow_blocks = (int32_t)block_items.size() - 1;
   plan->n_wide = (int32_t)witems.size();
   if (plan->n_wide == 0) plan->wide_rb = 0;
   plan->n_spans = (int32_t)spans.size();
@@ -527,6 +607,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   L.seg_len = place(sizeof(int32_t) * std::max(S, 1));
   L.page_ids = place(sizeof(int32_t) * std::max<int64_t>(total_pages, 1));
   L.items = place(sizeof(Item) * std::max<size_t>(items.size(), 1));
+  L.block_items = place(sizeof(int32_t) * block_items.size());
   L.wide_items = place(sizeof(Item) * std::max<size_t>(witems.size(), 1));
   L.spans = place(sizeof(Span) * std::max<size_t>(spans.size(), 1));
   L.rows = place(sizeof(Row) * std::max<size_t>(rows.size(), 1));
@@ -543,6 +624,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   }
   if (total_pages) memcpy(m + L.page_ids, f.seg_page_ids, sizeof(int32_t) * total_pages);
   if (!items.empty()) memcpy(m + L.items, items.data(), sizeof(Item) * items.size());
+  memcpy(m + L.block_items, block_items.data(), sizeof(int32_t) * block_items.size());
   if (!witems.empty()) memcpy(m + L.wide_items, witems.data(), sizeof(Item) * witems.size());
   if (!spans.empty()) memcpy(m + L.spans, spans.data(), sizeof(Span) * spans.size());
   if (!rows.empty()) memcpy(m + L.rows, rows.data(), sizeof(Row) * rows.size());
@@ -585,6 +667,7 @@ extern "C" halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void**
   out->seg_len = L.seg_len;
   out->page_ids = L.page_ids;
   out->items = L.items;
+  out->block_items = L.block_items;
   out->wide_items = L.wide_items;
   out->spans = L.spans;
   out->rows = L.rows;
@@ -593,6 +676,7 @@ extern "C" halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void**
   out->merge_parts = L.merge_parts;
   out->total_bytes = L.total;
   out->n_items = plan->n_items;
+  out->n_narrow_blocks = plan->n_narrow_blocks;
   out->n_wide = plan->n_wide;
   out->n_spans = plan->n_spans;
   out->n_rows = plan->n_rows;

@@ -164,6 +164,15 @@ def _check_plan(w, plan):
     st = plan.stats()
     assert st["visible_pairs"] == int(eh.sum())
     assert st["num_items"] == n_narrow and st["num_wide_items"] == len(items) - n_narrow
+    # narrow workgroups: a partition of the narrow items in order, at most
+    # one item per wave (8 bf16 / 4 fp32), a whole number of XCD rounds
+    bi = m["block_items"]
+    waves = 8 if w.dtype.itemsize == 2 else 4
+    if n_narrow:
+        assert bi[0] == 0 and bi[-1] == n_narrow and len(bi) > 1 and (len(bi) - 1) % 8 == 0
+        assert (np.diff(bi) >= 0).all() and (np.diff(bi) <= waves).all()
+    else:
+        assert len(bi) == 1 and bi[0] == 0
     return m
 
 
