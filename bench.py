@@ -177,10 +177,8 @@ def main():
         traffic = None
 
     kernels = []
-    if stats["num_wide_items"]:
-        kernels.append("attn_wide_kernel")
-    if stats["num_items"]:
-        kernels.append("attn_items_kernel")
+    if stats["num_wide_items"] or stats["num_items"]:
+        kernels.append("attn_kernel")
     if stats["num_merge_rows"]:
         kernels.append("merge_kernel")
     kernel_desc = " + ".join(kernels) + (" (one library call; time = all of its kernels)" if len(kernels) > 1 else "")

@@ -189,11 +189,16 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
  * for inspection and host-side testing of the work lists. Byte offsets of
  * each int32 array inside the image, and the element counts:
  *   items, wide_items: n_items / n_wide x {row_begin, n_rows, span_begin,
- *                       n_spans, kv_head, part_base (-1: final rows), keys, flags}
- *   block_items [n_narrow_blocks + 1]: narrow workgroup b runs items
- *                       block_items[b] .. block_items[b + 1] - 1
+ *                       n_spans, kv_head, part_base (-1: final rows), keys,
+ *                       flags, first span's key_begin, key_end, causal,
+ *                       unused x 5}
+ *                       narrow item b * narrow_slots + k runs in slot k of
+ *                       narrow workgroup b; n_rows = 0 marks an empty slot
+ *   item_recs: n_items x {q_row x 16 (-1 past n_rows), chunk position x 16,
+ *                       page ids of the first 32 pages of the first span}
  *   spans:  n_spans  x {segment, key_begin, key_end, causal, page-table offset,
- *                       unused x 3}; a span covers at most 1024 keys
+ *                       unused x 3}; a span covers at most 1024 keys (512 in
+ *                       a narrow item)
  *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position,
  *                       merge entry or -1, unused}
  *   merge_rows [n_merge], merge_indptr [n_merge + 1], merge_parts: partial
@@ -201,8 +206,9 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
  * *image stays valid until halo_plan_destroy. */
 typedef struct {
   uint64_t seg_page_off, seg_len, page_ids, items, wide_items, spans, rows;
-  uint64_t merge_rows, merge_indptr, merge_parts, total_bytes, block_items;
+  uint64_t merge_rows, merge_indptr, merge_parts, total_bytes, item_recs;
   int32_t n_items, n_wide, n_spans, n_rows, n_merge, n_merge_parts, n_pages, n_narrow_blocks;
+  int32_t narrow_slots;
 } halo_plan_layout_t;
 
 halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void** image,

@@ -26,20 +26,38 @@ constexpr int kItemOverheadKeys = 64;
 // Keys consumed per inner step: two pages of 16 (one K=32 MFMA for P*V).
 constexpr int kKeysPerStep = 32;
 
-// One wavefront's work: up to 16 query rows against a list of key spans.
-// 32 bytes, read by all 64 lanes.
+// One work item: up to 16 query rows (narrow, one wavefront) or up to 256
+// (wide, one workgroup) against a list of key spans. 64 bytes, read by the
+// scalar unit; the first span is repeated inline so that a narrow item can
+// start loading keys without first reading the span table.
 struct Item {
   int32_t row_begin;   // first entry in the row table
-  int32_t n_rows;      // 1..16
+  int32_t n_rows;      // 1..16 narrow, 1..256 wide; 0: an empty slot (narrow)
   int32_t span_begin;  // first entry in the span table
-  int32_t n_spans;     // >= 1
+  int32_t n_spans;     // >= 0
   int32_t kv_head;
   int32_t part_base;   // >= 0: partial rows part_base + i in the workspace;
                        // -1: final rows written straight to o / lse
   int32_t keys;        // visible-key estimate (cost, for ordering only)
   int32_t flags;       // kItemStream: keys read by this item only (stream them)
+  int32_t s0_key_begin;   // the first span (when n_spans > 0)
+  int32_t s0_key_end;
+  int32_t s0_causal;
+  int32_t pad[5];
 };
 constexpr int32_t kItemStream = 1;
+
+// What the 64 lanes of a narrow item's wavefront read at its start, one
+// 32-bit word each (256 bytes): the q_row and chunk position of each of its
+// (up to 16) rows, and the page ids of the first 32 pages of its first span.
+struct ItemRec {
+  int32_t q_row[16];   // -1 past n_rows
+  int32_t qpos[16];
+  int32_t page[32];
+};
+// Narrow items' spans are cut at this many keys, so that the first span's
+// page ids fit the record.
+constexpr int kNarrowSpanKeys = 512;
 
 // A contiguous range of keys of one segment, [key_begin, key_end).
 // key_begin is a multiple of kKeysPerStep and a span covers at most
@@ -70,8 +88,8 @@ struct MetaLayout {
   size_t seg_page_off = 0;   // int32 [S]  first page slot of each segment
   size_t seg_len = 0;        // int32 [S]
   size_t page_ids = 0;       // int32 [total pages]
-  size_t items = 0;          // Item  [n_items]     narrow (one wavefront), grouped by workgroup
-  size_t block_items = 0;    // int32 [n_narrow_blocks + 1] first item of each narrow workgroup
+  size_t items = 0;          // Item  [n_narrow_blocks * narrow_slots]  narrow, by workgroup slot
+  size_t item_recs = 0;      // ItemRec, one per narrow slot
   size_t wide_items = 0;     // Item  [n_wide]      wide (one 4-wave workgroup)
   size_t spans = 0;          // Span  [n_spans]
   size_t rows = 0;           // Row   [n_rows]
@@ -93,8 +111,10 @@ struct halo_plan {
   int32_t n_wide = 0;
   int32_t wide_rb = 0;       // 1 when the plan has wide items (32 rows per wave), else 0
   int32_t wide_group = 1;    // wide items that share pages, kept on one XCD
-  int32_t n_narrow_blocks = 0;  // workgroups the narrow items are dealt to (a multiple of 8),
-                                // at most one item per wave
+  int32_t n_narrow_blocks = 0;  // workgroups the narrow items are dealt to (a multiple of 8)
+  int32_t narrow_slots = 0;     // item slots per narrow workgroup (slot k: waves
+                                // k*narrow_split .. k*narrow_split + narrow_split - 1)
+  int32_t narrow_split = 1;     // waves sharing one narrow item
   int32_t n_shared_items = 0;
   int32_t n_merge = 0;
   int32_t n_spans = 0;

@@ -37,6 +37,8 @@ typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLn2 = 0.69314718055994530942f;
+// Most waves that may share one narrow item.
+constexpr int kMaxSplit = 8;
 constexpr float kLog2e = 1.44269504088896340736f;
 
 // ---------------------------------------------------------------- fragments
@@ -194,8 +196,8 @@ struct AttnArgs {
   const int32_t* seg_page_off;
   const int32_t* seg_len;
   const int32_t* page_ids;
-  const Item* items;        // narrow items (one wavefront each), grouped by workgroup
-  const int32_t* block_items;  // [narrow_blocks + 1]: first item of each narrow workgroup
+  const Item* items;        // narrow item slots: slot k of narrow workgroup b is item b * narrow_slots + k
+  const ItemRec* item_recs; // their lane records
   const Item* wide_items;   // wide items (one workgroup each)
   const Span* spans;
   const Row* rows;
@@ -203,6 +205,8 @@ struct AttnArgs {
   int32_t n_wide;
   int32_t wide_blocks;     // grid blocks of the wide role (n_wide padded, see xcd_remap)
   int32_t narrow_blocks;   // grid blocks of the narrow role (a multiple of 8)
+  int32_t narrow_slots;    // item slots per narrow workgroup
+  int32_t narrow_split;    // waves sharing one narrow item (block waves / narrow_slots)
   int32_t wide_group;      // consecutive wide items kept on one XCD
   int32_t num_kv_heads;
   float scale_log2;   // sm_scale * log2(e)
@@ -219,6 +223,16 @@ __device__ __forceinline__ int xcd_remap(int p, int S) {
   const int x = p & 7, j = p >> 3;
   return ((j / S) * 8 + x) * S + j % S;
 }
+
+// s_waitcnt with only the vector-memory counter limited (gfx9 encoding:
+// vmcnt low bits [3:0] and high bits [15:14]; expcnt and lgkmcnt at their
+// "no wait" maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // A span's keys and its page ids, one page per lane (a span has at most 64
 // pages), so a step finds its page ids with two lane reads instead of
@@ -273,8 +287,13 @@ struct StepRegs {
 //  * Loads are software-pipelined: the operands of step i+1 are in flight
 //    while step i is computed, and the next span's page ids are loaded when
 //    its predecessor starts.
+//  * split > 1: `split` waves share the item, wave `part` walking the item's
+//    steps part, part + split, ...; instead of writing the output it leaves
+//    its unnormalized accumulator, running max and sum in `red` (LDS) for
+//    merge_split.
 template <typename T, int D, typename TO, bool NT, int P>
-__device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int lane) {
+__device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, const ItemRec* rec, int lane,
+                                         int split, int part, float* red) {
   using F = typename FragOf<T>::type;
   constexpr int NS = D / 32;   // QK steps over d
   constexpr int NB = D / 16;   // PV output blocks over d
@@ -283,8 +302,10 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
   const int col = lane & 15;
   const int grp = lane >> 4;
 
-  Row row{-1, 0, -1, 0};
-  if (col < it.n_rows) row = a.rows[it.row_begin + col];
+  // The item's lane record (one load per field, all in flight together):
+  // this lane's row, and page j of the first span in lane j.
+  Row row{rec->q_row[col], rec->qpos[col], -1, 0};
+  const int32_t vpid0 = rec->page[lane & 31];
 
   F qf[NS];
   {
@@ -340,21 +361,30 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
     for (int b = 0; b < NB; ++b) r.v[b] = load_v8<NT>(vq, v_off + b * 256);
   };
 
-  // Span cursor: cur is being walked, nxt is loaded one span ahead.
+  // Span cursor. The first span comes with the item and its record; a later
+  // span's page ids are loaded when the walk reaches it, and waited for at
+  // once: the wait then never has to be repeated on the loop's back edge,
+  // where the compiler would otherwise drain every load in flight (the K/V
+  // of the next step included) on each iteration.
   int si = 0;
-  SpanState cur = load_span(0);
-  SpanState nxt = load_span(1);
-  int t_next = cur.kb;   // first key of the next step to issue
+  SpanState cur;
+  cur.valid = it.n_spans > 0;
+  cur.kb = it.s0_key_begin;
+  cur.ke = it.s0_key_end;
+  cur.causal = it.s0_causal;
+  cur.vpid = vpid0;
+  int gs = part;   // index of this wave's next step among the item's steps
+  int sb = 0;      // index of cur's first step
   auto advance = [&]() {
-    // position of the next step to issue, moving to the next span if needed
-    if (t_next >= cur.ke) {
-      cur = nxt;
+    // position of the next step to issue, moving on to the span holding it
+    while (cur.valid && gs >= sb + ((cur.ke - cur.kb + kKeysPerStep - 1) >> 5)) {
+      sb += (cur.ke - cur.kb + kKeysPerStep - 1) >> 5;
       ++si;
-      nxt = load_span(si + 1);
-      t_next = cur.kb;
+      cur = load_span(si);
+      wait_vmcnt<0>();
     }
-    StepPos p = step_at(cur, t_next);
-    t_next += kKeysPerStep;
+    StepPos p = step_at(cur, cur.kb + (gs - sb) * kKeysPerStep);
+    gs += split;
     return p;
   };
 
@@ -384,13 +414,6 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
         const bool vis = key < p.key_end && (!p.causal || key <= row.qpos);
         sv[j] = vis ? sacc[j >> 2][j & 3] * a.scale_log2 : kNegInf;
       }
-      // Keys past the span end may be NaN page tails (or a repeated page):
-      // zero V there, since P = 0 times NaN would still poison the sum.
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (p.t0 + slot_key(grp, j) >= p.key_end)
-#pragma unroll
-          for (int b = 0; b < NB; ++b) r.v[b][j] = (T)0.f;
     }
     float mt = sv[0];
 #pragma unroll
@@ -410,20 +433,36 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
     m = m_new;
     const F pf = to_frag(pr, (F*)nullptr);
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      acc[b] *= alpha;
-      acc[b] = mma(r.v[b], pf, acc[b]);
+    for (int b = 0; b < NB; ++b) acc[b] *= alpha;
+    if (p.t0 + kKeysPerStep <= p.key_end) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[b] = mma(r.v[b], pf, acc[b]);
+    } else {
+      // Keys past the span end may be NaN page tails (or a repeated page):
+      // zero V there, since P = 0 times NaN would still poison the sum.
+      // The operand registers stay untouched (copies are masked), so the
+      // register stages keep fixed registers across the loop.
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        F vb = r.v[b];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (p.t0 + slot_key(grp, j) >= p.key_end) vb[j] = (T)0.f;
+        acc[b] = mma(vb, pf, acc[b]);
+      }
     }
   };
 
   // P register stages rotate: while step s is computed, the next P - 1
   // steps are in flight. A position past the end re-fetches the current
   // step's pages (in bounds, never used).
-  if (cur.valid) {
-    Regs r[P];
-    StepPos ps[P];
+  Regs r[P];
+  StepPos ps[P];
+  ps[0] = advance();
+  if (ps[0].valid) {
+    fetch(ps[0], r[0]);
 #pragma unroll
-    for (int i = 0; i < P - 1; ++i) {
+    for (int i = 1; i < P - 1; ++i) {
       ps[i] = advance();
       fetch(pick(ps[i].valid, ps[i], ps[0]), r[i]);
     }
@@ -444,6 +483,16 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
   }
 
   lsum = rows_sum(lsum);
+  if (split > 1) {
+    // red: [NB][64 lanes][4] accumulator, then per row its max and sum
+#pragma unroll
+    for (int b = 0; b < NB; ++b) *reinterpret_cast<f32x4_t*>(red + (b * 64 + lane) * 4) = acc[b];
+    if (grp == 0) {
+      red[NB * 256 + col] = m;
+      red[NB * 256 + 16 + col] = lsum;
+    }
+    return;
+  }
   const bool has_row = col < it.n_rows;
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   const float lse2 = lsum > 0.f ? m + __log2f(lsum) : kNegInf;
@@ -468,17 +517,79 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, int 
 // one wave per SIMD.
 template <typename T> constexpr int block_waves() { return sizeof(T) == 2 ? 8 : 4; }
 
-// Narrow workgroup `block` runs items block_items[block] ..
-// block_items[block + 1] - 1 (dealt by the planner), one per wave; waves past
-// the count exit.
+// Floats of one wave's hand-off area for a shared item: the [D/16][64][4]
+// accumulator, then 16 row maxima and 16 row sums.
+template <int D> constexpr int red_floats() { return (D / 16) * 256 + 32; }
+
+// Combines the `split` partial results that the waves of one item left in
+// LDS (red0: the first of them), with the exact rule
+//   M = max_q m_q, s_q = 2^(m_q - M), O = sum_q s_q acc_q / sum_q s_q l_q,
+// and writes the item's rows. Wave `part` of the item writes the output
+// blocks part, part + split, ... (the LSE with part 0).
 template <typename T, int D, typename TO>
-__device__ __forceinline__ void narrow_block(const AttnArgs& a, int block) {
+__device__ __forceinline__ void merge_split(const AttnArgs& a, const Item& it, const ItemRec* rec, int lane,
+                                            int split, int part, const float* red0) {
+  constexpr int NB = D / 16;
+  constexpr int kRed = red_floats<D>();
+  const int col = lane & 15, grp = lane >> 4;
+  float sq[kMaxSplit];
+  float M = kNegInf;
+#pragma unroll
+  for (int q = 0; q < kMaxSplit; ++q) {
+    sq[q] = q < split ? red0[q * kRed + NB * 256 + col] : kNegInf;
+    M = fmaxf(M, sq[q]);
+  }
+  float L = 0.f;
+#pragma unroll
+  for (int q = 0; q < kMaxSplit; ++q) {
+    sq[q] = (q < split && sq[q] != kNegInf) ? __builtin_amdgcn_exp2f(sq[q] - M) : 0.f;
+    if (q < split) L += sq[q] * red0[q * kRed + NB * 256 + 16 + col];
+  }
+  const bool has_row = col < it.n_rows;
+  if (!has_row) return;
+  const int q_row = rec->q_row[col];
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  const float lse2 = L > 0.f ? M + __log2f(L) : kNegInf;
+  for (int b = part; b < NB; b += split) {
+    f32x4_t o = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < kMaxSplit; ++q)
+      if (q < split) o += sq[q] * *reinterpret_cast<const f32x4_t*>(red0 + q * kRed + (b * 64 + lane) * 4);
+    o *= inv;
+    if (it.part_base >= 0) store4(a.part_o + ((int64_t)it.part_base + col) * D + 16 * b + 4 * grp, o);
+    else store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 16 * b + 4 * grp, o);
+  }
+  if (part == 0 && grp == 0) {
+    if (it.part_base >= 0) a.part_lse[it.part_base + col] = lse2;
+    else if (a.lse) a.lse[q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
+  }
+}
+
+// Narrow workgroup `block` runs the items in its narrow_slots slots (dealt
+// by the planner; n_rows = 0 marks an empty slot). With narrow_split = 1
+// each wave runs one item and waves of empty slots exit. With
+// narrow_split = s > 1, waves s*k .. s*k + s - 1 share item k: they walk its
+// steps interleaved, hand their partial results over in LDS and merge them,
+// so an item's chain of dependent steps is s times shorter.
+template <typename T, int D, typename TO>
+__device__ __forceinline__ void narrow_block(const AttnArgs& a, int block, float* red_all) {
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const int item_id = a.block_items[block] + wave;
-  if (item_id >= a.block_items[block + 1]) return;
+  const int lane = threadIdx.x & 63;
+  const int split = a.narrow_split;
+  const int slot = wave / split, part = wave - slot * split;
+  const int64_t item_id = (int64_t)block * a.narrow_slots + slot;
   const Item it = a.items[item_id];
-  if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, threadIdx.x & 63);
-  else run_item<T, D, TO, false, 2>(a, it, threadIdx.x & 63);
+  const ItemRec* rec = a.item_recs + item_id;
+  const bool has = it.n_rows > 0;
+  if (split == 1 && !has) return;
+  if (has) {
+    float* red = red_all + wave * red_floats<D>();
+    if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, rec, lane, split, part, red);
+    else run_item<T, D, TO, false, 2>(a, it, rec, lane, split, part, red);
+  }
+  if (split == 1) return;
+  __syncthreads();
+  if (has) merge_split<T, D, TO>(a, it, rec, lane, split, part, red_all + slot * split * red_floats<D>());
 }
 
 // ---------------------------------------------------------------- wide items
@@ -518,18 +629,12 @@ __device__ __forceinline__ void narrow_block(const AttnArgs& a, int block) {
 constexpr float kRescaleLog2 = 8.f;
 constexpr int kWideStages = 6;
 
-// s_waitcnt with only the vector-memory counter limited (gfx9 encoding:
-// vmcnt low bits [3:0] and high bits [15:14]; expcnt and lgkmcnt at their
-// "no wait" maxima).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
-}
-__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+// Bytes of the wide items' LDS ring: kWideStages step images of
+// 2 * D/32 + D/16 blocks of 1 KB.
+template <int D> constexpr int wide_ring_bytes() { return kWideStages * (D / 16 + 2 * (D / 32)) * 1024; }
 
 template <int D, typename TO>
-__device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
+__device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_t* smem) {
   using T = __bf16;
   using F = bf16x8_t;
   constexpr int NK = D / 16;                      // 16-dim slices of Q K^T
@@ -541,7 +646,8 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id) {
   constexpr int S = kWideStages;
   static_assert(S >= 5 && S % 2 == 0, "the ring needs >= 5 stages, an even count keeps tile parity static");
   constexpr int64_t kTile = 16 * D;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[S][kStepBytes];
+  static_assert(S * kStepBytes == wide_ring_bytes<D>(), "ring size");
+  uint8_t (*lds)[kStepBytes] = reinterpret_cast<uint8_t (*)[kStepBytes]>(smem);
 
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -905,6 +1011,11 @@ __global__ __launch_bounds__(64 * block_waves<T>())
 __attribute__((amdgpu_waves_per_eu(block_waves<T>() / 4)))
 void attn_kernel(AttnArgs a) {
   static_assert(RB == 0 || block_waves<T>() == kWideWaves, "wide items need kWideWaves-wave blocks");
+  // one LDS area for whichever role the block takes: the wide ring, or the
+  // hand-off of shared narrow items
+  constexpr int kRedBytes = block_waves<T>() * red_floats<D>() * 4;
+  constexpr int kSmem = RB > 0 && wide_ring_bytes<D>() > kRedBytes ? wide_ring_bytes<D>() : kRedBytes;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmem];
   const int b = blockIdx.x;
   const int x = b & 7, r = b >> 3;
   if constexpr (RB > 0) {
@@ -914,12 +1025,12 @@ void attn_kernel(AttnArgs a) {
     const int w_upto = (int)((int64_t)(r + 1) * wr / tr);
     if (w_upto > w_before) {
       const int item = xcd_remap(w_before * 8 + x, a.wide_group);
-      if (item < a.n_wide) wide_item<D, TO>(a, item);
+      if (item < a.n_wide) wide_item<D, TO>(a, item, smem);
       return;
     }
-    narrow_block<T, D, TO>(a, (r - w_upto) * 8 + x);
+    narrow_block<T, D, TO>(a, (r - w_upto) * 8 + x, reinterpret_cast<float*>(smem));
   } else {
-    narrow_block<T, D, TO>(a, b);
+    narrow_block<T, D, TO>(a, b, reinterpret_cast<float*>(smem));
   }
 }
 
@@ -1131,11 +1242,12 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                 reinterpret_cast<const int32_t*>(m + L.seg_len),
                 reinterpret_cast<const int32_t*>(m + L.page_ids),
                 reinterpret_cast<const Item*>(m + L.items),
-                reinterpret_cast<const int32_t*>(m + L.block_items),
+                reinterpret_cast<const ItemRec*>(m + L.item_recs),
                 reinterpret_cast<const Item*>(m + L.wide_items),
                 reinterpret_cast<const Span*>(m + L.spans),
                 reinterpret_cast<const Row*>(m + L.rows),
-                plan->n_items, plan->n_wide, 0, plan->n_narrow_blocks, plan->wide_group,
+                plan->n_items, plan->n_wide, 0, plan->n_narrow_blocks, plan->narrow_slots, plan->narrow_split,
+                plan->wide_group,
                 p.num_kv_heads, p.sm_scale * kLog2e};
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),

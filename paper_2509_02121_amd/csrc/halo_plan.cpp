@@ -286,6 +286,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       }
       kc = env_int("HALO_KC_WIDE", kc, 32, kMaxSpanKeys) / 32 * 32;
     }
+    const bool rotate = env_int("HALO_ROTATE", 1, 0, 1) == 1;
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
       std::vector<Span> sp;
@@ -295,12 +296,26 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         for (int32_t r : seg_reqs[s])
           for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, 0});
         // chunk-major, row group innermost: items reading the same pages
-        // are neighbours in the launch order.
+        // are neighbours in the launch order. The row groups of a chunk
+        // start at evenly spread steps of it and wrap around, so that at
+        // any moment they read different pages: each page is fetched from
+        // HBM by one of them and found in L2 by the others, instead of all
+        // of them waiting on the same misses.
+        const size_t n_groups = (rows.size() + rows_per - 1) / rows_per;
         for (const Span& piece : sp) {
+          const int32_t n_steps = (piece.key_end - piece.key_begin + kKeysPerStep - 1) / kKeysPerStep;
           for (size_t rb = 0; rb < rows.size(); rb += rows_per) {
             Proto pr;
             pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
-            pr.spans = {piece};
+            const int32_t off = rotate ? (int32_t)((rb / rows_per) * n_steps / n_groups) * kKeysPerStep : 0;
+            if (off > 0) {
+              Span head = piece, tail = piece;
+              head.key_begin = piece.key_begin + off;
+              tail.key_end = piece.key_begin + off;
+              pr.spans = {head, tail};
+            } else {
+              pr.spans = {piece};
+            }
             pr.kv_head = g;
             pr.keys = piece.key_end - piece.key_begin;
             pr.shared = true;
@@ -458,16 +473,24 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     }
     if (pr.shared) plan->n_shared_items++;
     rows.insert(rows.end(), pr.rows.begin(), pr.rows.end());
-    // Split spans at kMaxSpanKeys and resolve their page-table offsets.
+    // Split spans at kMaxSpanKeys (kNarrowSpanKeys for narrow items) and
+    // resolve their page-table offsets.
+    const int32_t max_keys = pr.wide ? kMaxSpanKeys : kNarrowSpanKeys;
     for (const Span& sp : pr.spans)
-      for (int32_t kb = sp.key_begin; kb < sp.key_end; kb += kMaxSpanKeys) {
+      for (int32_t kb = sp.key_begin; kb < sp.key_end; kb += max_keys) {
         Span piece = sp;
         piece.key_begin = kb;
-        piece.key_end = std::min(sp.key_end, kb + kMaxSpanKeys);
+        piece.key_end = std::min(sp.key_end, kb + max_keys);
         piece.page_off = f.seg_page_indptr[sp.seg] + kb / p.page_size;
         spans.push_back(piece);
       }
     it.n_spans = (int32_t)spans.size() - it.span_begin;
+    if (it.n_spans > 0) {
+      const Span& s0 = spans[it.span_begin];
+      it.s0_key_begin = s0.key_begin;
+      it.s0_key_end = s0.key_end;
+      it.s0_causal = s0.causal;
+    }
     (pr.wide ? witems : items).push_back(it);
     if (!pr.wide) item_chunk.push_back(pr.chunk);
   }
@@ -495,24 +518,32 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
           }
   }
 
-  plan->n_items = (int32_t)items.size();
-  // Narrow items are dealt to workgroups ahead of time, at most `cap` to a
-  // workgroup (one per wave; the waves past its count exit). A CU ingests
-  // only ~30 GB/s from HBM (~70 GB/s from L2), so a small batch is spread
-  // over every CU (at least 256 workgroups of 8 waves, one per CU) and
-  // items go longest first to the least loaded workgroup. Beside wide
-  // workgroups, narrow ones take half their waves' worth of items.
-  // Workgroup b runs on XCD b % 8 (dispatch is round-robin), and the row
-  // groups of one shared chunk go to workgroups of one XCD, in units of up
-  // to shared_unit items on one workgroup, so re-reads of the chunk hit that
-  // XCD's L2 or the CU's L1.
-  std::vector<int32_t> block_items{0};
+  // Narrow items are dealt to workgroups ahead of time: workgroup b has
+  // `slots` item slots (one per wave, or one per narrow_split waves), and
+  // item b * slots + k, if not empty, runs in slot k. A CU ingests only
+  // ~30 GB/s from HBM (~70 GB/s from L2), so a small batch is spread over
+  // every CU (at least 256 workgroups of 8 waves, one per CU) and items go
+  // longest first to the least loaded workgroup. Beside wide workgroups,
+  // narrow ones fill half their slots. Workgroup b runs on XCD b % 8
+  // (dispatch is round-robin), and the row groups of one shared chunk go to
+  // workgroups of one XCD, in units of up to shared_unit items on one
+  // workgroup, so re-reads of the chunk hit that XCD's L2 or the CU's L1.
+  std::vector<ItemRec> recs;
+  const int64_t n_real_items = (int64_t)items.size();
   if (!items.empty()) {
     const int waves = narrow_items_per_block(p.kv_dtype);
     const int64_t n = (int64_t)items.size();
-    const int cap = env_int("HALO_ITEMS_PER_BLOCK", witems.empty() ? waves : std::max(1, waves / 2), 1, waves);
+    int split = env_int("HALO_SPLIT", 1, 1, waves);
+    while (waves % split) --split;
+    plan->narrow_split = split;
+    const int slots = waves / split;
+    const int cap = env_int("HALO_ITEMS_PER_BLOCK", witems.empty() ? slots : std::max(1, slots / 2), 1, slots);
     int64_t nb = std::max<int64_t>((n + cap - 1) / cap, std::min<int64_t>(n, kNumCUs));
     nb = (nb + 7) / 8 * 8;
+    if (nb * slots > (int64_t)std::numeric_limits<int32_t>::max()) {
+      delete plan;
+      return fail(HALO_ERR_INVALID_ARGUMENT, "too many narrow work items");
+    }
     const int shared_unit = std::min(cap, env_int("HALO_SHARED_UNIT", 4, 1, 64));
     // work units: runs of up to shared_unit items of one chunk, or one item
     struct Unit { int32_t first, count, chunk; int64_t cost; };
@@ -573,15 +604,30 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         }
       }
     }
-    std::vector<Item> dealt;
-    dealt.reserve(n);
-    for (auto& list : blk) {
-      for (int32_t i : list) dealt.push_back(items[i]);
-      block_items.push_back((int32_t)dealt.size());
-    }
+    // slot layout, empty slots n_rows = 0; and each slot's lane record
+    std::vector<Item> dealt((size_t)(nb * slots), Item{});
+    recs.assign((size_t)(nb * slots), ItemRec{});
+    for (int64_t b = 0; b < nb; ++b)
+      for (size_t k = 0; k < blk[b].size(); ++k) {
+        const size_t at = (size_t)(b * slots) + k;
+        const Item& it = items[blk[b][k]];
+        dealt[at] = it;
+        ItemRec& rc = recs[at];
+        for (int r = 0; r < 16; ++r) {
+          rc.q_row[r] = r < it.n_rows ? rows[it.row_begin + r].q_row : -1;
+          rc.qpos[r] = r < it.n_rows ? rows[it.row_begin + r].qpos : 0;
+        }
+        if (it.n_spans > 0) {
+          const Span& s0 = spans[it.span_begin];
+          const int32_t np = (s0.key_end - s0.key_begin + p.page_size - 1) / p.page_size;
+          for (int32_t j = 0; j < np && j < 32; ++j) rc.page[j] = f.seg_page_ids[s0.page_off + j];
+        }
+      }
     items.swap(dealt);
+    plan->n_narrow_blocks = (int32_t)nb;
+    plan->narrow_slots = slots;
   }
-  plan->n_narrow_blocks = (int32_t)block_items.size() - 1;
+  plan->n_items = (int32_t)n_real_items;
   plan->n_wide = (int32_t)witems.size();
   if (plan->n_wide == 0) plan->wide_rb = 0;
   plan->n_spans = (int32_t)spans.size();
@@ -607,7 +653,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   L.seg_len = place(sizeof(int32_t) * std::max(S, 1));
   L.page_ids = place(sizeof(int32_t) * std::max<int64_t>(total_pages, 1));
   L.items = place(sizeof(Item) * std::max<size_t>(items.size(), 1));
-  L.block_items = place(sizeof(int32_t) * block_items.size());
+  L.item_recs = place(sizeof(ItemRec) * std::max<size_t>(recs.size(), 1));
   L.wide_items = place(sizeof(Item) * std::max<size_t>(witems.size(), 1));
   L.spans = place(sizeof(Span) * std::max<size_t>(spans.size(), 1));
   L.rows = place(sizeof(Row) * std::max<size_t>(rows.size(), 1));
@@ -624,7 +670,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   }
   if (total_pages) memcpy(m + L.page_ids, f.seg_page_ids, sizeof(int32_t) * total_pages);
   if (!items.empty()) memcpy(m + L.items, items.data(), sizeof(Item) * items.size());
-  memcpy(m + L.block_items, block_items.data(), sizeof(int32_t) * block_items.size());
+  if (!recs.empty()) memcpy(m + L.item_recs, recs.data(), sizeof(ItemRec) * recs.size());
   if (!witems.empty()) memcpy(m + L.wide_items, witems.data(), sizeof(Item) * witems.size());
   if (!spans.empty()) memcpy(m + L.spans, spans.data(), sizeof(Span) * spans.size());
   if (!rows.empty()) memcpy(m + L.rows, rows.data(), sizeof(Row) * rows.size());
@@ -667,7 +713,7 @@ extern "C" halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void**
   out->seg_len = L.seg_len;
   out->page_ids = L.page_ids;
   out->items = L.items;
-  out->block_items = L.block_items;
+  out->item_recs = L.item_recs;
   out->wide_items = L.wide_items;
   out->spans = L.spans;
   out->rows = L.rows;
@@ -675,8 +721,9 @@ extern "C" halo_status_t halo_plan_inspect(const halo_plan_t* plan, const void**
   out->merge_indptr = L.merge_indptr;
   out->merge_parts = L.merge_parts;
   out->total_bytes = L.total;
-  out->n_items = plan->n_items;
+  out->n_items = plan->n_narrow_blocks * plan->narrow_slots;
   out->n_narrow_blocks = plan->n_narrow_blocks;
+  out->narrow_slots = plan->narrow_slots;
   out->n_wide = plan->n_wide;
   out->n_spans = plan->n_spans;
   out->n_rows = plan->n_rows;

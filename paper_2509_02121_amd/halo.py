@@ -52,9 +52,9 @@ class PlanStats(ctypes.Structure):
 class PlanLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "seg_page_off", "seg_len", "page_ids", "items", "wide_items", "spans", "rows", "merge_rows",
-        "merge_indptr", "merge_parts", "total_bytes", "block_items")] + [(n, ctypes.c_int32) for n in (
+        "merge_indptr", "merge_parts", "total_bytes", "item_recs")] + [(n, ctypes.c_int32) for n in (
             "n_items", "n_wide", "n_spans", "n_rows", "n_merge", "n_merge_parts", "n_pages",
-            "n_narrow_blocks")]
+            "n_narrow_blocks", "narrow_slots")]
 
 
 EXPORTED_SYMBOLS = (
@@ -215,9 +215,10 @@ class Plan:
         return dict(
             seg_page_off=arr(lay.seg_page_off, S), seg_len=arr(lay.seg_len, S),
             page_ids=arr(lay.page_ids, lay.n_pages),
-            items=arr(lay.items, lay.n_items, 8).copy(),
-            block_items=arr(lay.block_items, lay.n_narrow_blocks + 1),
-            wide_items=arr(lay.wide_items, lay.n_wide, 8).copy(), spans=arr(lay.spans, lay.n_spans, 8).copy(),
+            items=arr(lay.items, lay.n_items, 16).copy(),
+            item_recs=arr(lay.item_recs, lay.n_items, 64).copy(),
+            n_narrow_blocks=lay.n_narrow_blocks, narrow_slots=lay.narrow_slots,
+            wide_items=arr(lay.wide_items, lay.n_wide, 16).copy(), spans=arr(lay.spans, lay.n_spans, 8).copy(),
             rows=arr(lay.rows, lay.n_rows, 4).copy(), merge_rows=arr(lay.merge_rows, lay.n_merge),
             merge_indptr=arr(lay.merge_indptr, lay.n_merge + 1),
             merge_parts=arr(lay.merge_parts, lay.n_merge_parts), total_bytes=lay.total_bytes)

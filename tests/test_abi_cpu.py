@@ -96,9 +96,26 @@ def _check_plan(w, plan):
     m = plan.inspect()
     hq, hkv = w.num_q_heads, w.num_kv_heads
     group = hq // hkv
-    items = np.concatenate([m["items"].reshape(-1, 8), m["wide_items"].reshape(-1, 8)])
-    n_narrow = len(m["items"])
     spans, rows = m["spans"], m["rows"]
+    # narrow slots: workgroup b, slot k = item b * slots + k; n_rows 0 = empty
+    slot_items = m["items"].reshape(-1, 16)
+    assert len(slot_items) == m["n_narrow_blocks"] * m["narrow_slots"] and m["n_narrow_blocks"] % 8 == 0
+    waves = 8 if w.dtype.itemsize == 2 else 4
+    assert m["narrow_slots"] in (0, 1, 2, 4, 8) and m["narrow_slots"] <= waves
+    used = slot_items[:, 1] > 0
+    recs = m["item_recs"].reshape(-1, 64)
+    for it, rc in zip(slot_items[used], recs[used]):
+        nr = it[1]
+        assert np.array_equal(rc[:nr], rows[it[0]:it[0] + nr, 0]) and (rc[nr:16] == -1).all()
+        assert np.array_equal(rc[16:16 + nr], rows[it[0]:it[0] + nr, 1])
+        if it[3] > 0:
+            sp = spans[it[2]]
+            assert tuple(it[8:11]) == (sp[1], sp[2], sp[3]), "inline first span"
+            assert sp[2] - sp[1] <= 512, "narrow spans are cut at 512 keys"
+            npg = (sp[2] - sp[1] + 15) // 16
+            assert np.array_equal(rc[32:32 + npg], m["page_ids"][sp[4]:sp[4] + npg])
+    items = np.concatenate([slot_items[used], m["wide_items"].reshape(-1, 16)])[:, :8]
+    n_narrow = int(used.sum())
     for sp in spans:
         seg, kb, ke, causal, page_off = sp[:5]
         assert kb % 32 == 0 and 0 <= kb < ke <= w.seg_len[seg] and ke - kb <= 1024
@@ -164,15 +181,6 @@ def _check_plan(w, plan):
     st = plan.stats()
     assert st["visible_pairs"] == int(eh.sum())
     assert st["num_items"] == n_narrow and st["num_wide_items"] == len(items) - n_narrow
-    # narrow workgroups: a partition of the narrow items in order, at most
-    # one item per wave (8 bf16 / 4 fp32), a whole number of XCD rounds
-    bi = m["block_items"]
-    waves = 8 if w.dtype.itemsize == 2 else 4
-    if n_narrow:
-        assert bi[0] == 0 and bi[-1] == n_narrow and len(bi) > 1 and (len(bi) - 1) % 8 == 0
-        assert (np.diff(bi) >= 0).all() and (np.diff(bi) <= waves).all()
-    else:
-        assert len(bi) == 1 and bi[0] == 0
     return m
 
 
@@ -211,8 +219,8 @@ def test_plan_empty_batch_and_empty_segments(lib):
     # spans (which write O = 0, LSE = -inf), never in the merge list
     empty_rows = {r * 4 + h for r in (0, 1, 3) for h in range(4)}
     found = set()
-    for it in m["items"]:
-        if it[3] == 0:
+    for it in m["items"].reshape(-1, 16):
+        if it[1] > 0 and it[3] == 0:
             assert it[5] == -1
             found |= set(m["rows"][it[0]:it[0] + it[1], 0].tolist())
     assert found == empty_rows
