@@ -26,6 +26,17 @@ DEFAULT_WORKLOAD = "llama8b_decode"
 MALL_BYTES = 256 << 20
 
 
+def source_sha256():
+    """sha256 over the kernel, planner and shared-header sources: measured
+    traffic stays valid only for the code it was measured on."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("halo_kernels.hip", "halo_plan.cpp", "halo_internal.h"):
+        with open(os.path.join(ROOT, "paper_2509_02121_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
 def algorithmic_bytes(w, stats):
     """Bytes the method must move once: each segment's K and V, the page-id
     table, Q, O and the LSE."""
@@ -162,15 +173,13 @@ def main():
     eff_gbps = alg_bytes / (wall_ms / 1e3) / 1e9
 
     # Measured HBM bytes per call (calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE),
-    # valid only while the kernel source is the one the counters were taken on.
+    # valid only while the kernel and planner sources are the ones the
+    # counters were taken on.
     traffic = None
     try:
-        import hashlib
         with open(args.traffic_json) as f:
             tr = json.load(f)
-        src = os.path.join(ROOT, "paper_2509_02121_amd", "csrc", "halo_kernels.hip")
-        with open(src, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
+        sha = source_sha256()
         if tr.get("_kernel_source_sha256") == sha and w.name in tr:
             traffic = tr[w.name]["bytes_per_call"]
     except (OSError, ValueError, KeyError):

@@ -1,15 +1,22 @@
 // gfx950 kernels and the run-time entry points of the C ABI.
 //
-// attn_items_kernel: one wavefront per work item (<= 16 query rows against a
-//   list of key spans). Per step of 32 keys (two 16-token pages):
-//     S^T = K Q^T  on v_mfma_f32_16x16x32_bf16 (one 16-key tile per page,
-//                  4 MFMAs per tile at d=128)
-//     online softmax in the log2 domain (row max / sum over the 4 lane groups)
-//     O^T += V^T P^T on the same MFMA (8 MFMAs at d=128)
-//   K pages are stored in 16-byte units ([d/E][16][E]) and V pages dim-major
-//   ([d][16]), so every MFMA A operand is a direct load from one page: 1 KB
-//   contiguous per wave for K, 512 B for V. The QK output layout is already
-//   the PV B operand (no lane exchange).
+// attn_kernel: one launch for the grouped prefix pass, the suffix pass and
+//   chunked prefill, with two kinds of workgroups:
+//   * narrow: item slots of one wavefront each (<= 16 query rows against a
+//     list of key spans). Per step of 32 keys (two 16-token pages):
+//       S^T = K Q^T  on v_mfma_f32_16x16x32_bf16 (one 16-key tile per page,
+//                    4 MFMAs per tile at d=128)
+//       online softmax in the log2 domain (row max / sum over the 4 lane
+//       groups)
+//       O^T += V^T P^T on the same MFMA (8 MFMAs at d=128)
+//     K pages are stored in 16-byte units ([d/E][16][E]) and V pages
+//     dim-major ([d][16], slots permuted so 8 keys of a lane are 16
+//     contiguous bytes), so every MFMA operand is a direct 1 KB-per-wave load
+//     from one or two pages. The QK output layout is already the PV B
+//     operand (no lane exchange).
+//   * wide: up to 256 query rows (8 waves x 32) sharing one key stream,
+//     staged once per workgroup through an LDS ring by direct global-to-LDS
+//     loads, on v_mfma_f32_32x32x16_bf16.
 // merge_kernel: exact log-sum-exp combination of partial results over
 //   disjoint key ranges (the merge that makes shared == unshared), in its own
 //   launch so the kernel boundary makes every partial visible (an in-kernel

@@ -286,7 +286,6 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       }
       kc = env_int("HALO_KC_WIDE", kc, 32, kMaxSpanKeys) / 32 * 32;
     }
-    const bool rotate = env_int("HALO_ROTATE", 1, 0, 1) == 1;
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
       std::vector<Span> sp;
@@ -296,26 +295,12 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         for (int32_t r : seg_reqs[s])
           for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, 0});
         // chunk-major, row group innermost: items reading the same pages
-        // are neighbours in the launch order. The row groups of a chunk
-        // start at evenly spread steps of it and wrap around, so that at
-        // any moment they read different pages: each page is fetched from
-        // HBM by one of them and found in L2 by the others, instead of all
-        // of them waiting on the same misses.
-        const size_t n_groups = (rows.size() + rows_per - 1) / rows_per;
+        // are neighbours in the launch order.
         for (const Span& piece : sp) {
-          const int32_t n_steps = (piece.key_end - piece.key_begin + kKeysPerStep - 1) / kKeysPerStep;
           for (size_t rb = 0; rb < rows.size(); rb += rows_per) {
             Proto pr;
             pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
-            const int32_t off = rotate ? (int32_t)((rb / rows_per) * n_steps / n_groups) * kKeysPerStep : 0;
-            if (off > 0) {
-              Span head = piece, tail = piece;
-              head.key_begin = piece.key_begin + off;
-              tail.key_end = piece.key_begin + off;
-              pr.spans = {head, tail};
-            } else {
-              pr.spans = {piece};
-            }
+            pr.spans = {piece};
             pr.kv_head = g;
             pr.keys = piece.key_end - piece.key_begin;
             pr.shared = true;
