@@ -189,20 +189,23 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
  * for inspection and host-side testing of the work lists. Byte offsets of
  * each int32 array inside the image, and the element counts:
  *   items, wide_items: n_items / n_wide x {row_begin, n_rows, span_begin,
- *                       n_spans, kv_head, part_base (-1: final rows), keys,
- *                       flags, first span's key_begin, key_end, causal,
- *                       unused x 5}
+ *                       n_spans, kv_head, partial flag (>= 0: the rows write
+ *                       partials at their slots; -1: final rows), keys, flags,
+ *                       first span's key_begin, key_end, causal, unused x 5}
  *                       narrow item b * narrow_slots + k runs in slot k of
  *                       narrow workgroup b; n_rows = 0 marks an empty slot
- *   item_recs: n_items x {q_row x 16 (-1 past n_rows), chunk position x 16,
- *                       page ids of the first 32 pages of the first span}
+ *   item_recs: n_items x {q_row x 16 (-1 past n_rows), per row its chunk
+ *                       position (prefill) or partial slot (decode item with
+ *                       partials), page ids of the first 32 pages of the
+ *                       first span}
  *   spans:  n_spans  x {segment, key_begin, key_end, causal, page-table offset,
  *                       unused x 3}; a span covers at most 1024 keys (512 in
  *                       a narrow item)
  *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position,
- *                       merge entry or -1, unused}
- *   merge_rows [n_merge], merge_indptr [n_merge + 1], merge_parts: partial
- *   row ids combined into each listed output row.
+ *                       merge entry or -1, partial slot or -1}
+ *   merge_rows [n_merge], merge_indptr [n_merge + 1], merge_parts: the
+ *   partial slots combined into each listed output row; the slots of entry
+ *   m are merge_indptr[m] .. merge_indptr[m + 1] - 1.
  * *image stays valid until halo_plan_destroy. */
 typedef struct {
   uint64_t seg_page_off, seg_len, page_ids, items, wide_items, spans, rows;

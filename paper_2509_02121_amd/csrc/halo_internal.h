@@ -36,8 +36,9 @@ struct Item {
   int32_t span_begin;  // first entry in the span table
   int32_t n_spans;     // >= 0
   int32_t kv_head;
-  int32_t part_base;   // >= 0: partial rows part_base + i in the workspace;
-                       // -1: final rows written straight to o / lse
+  int32_t part_base;   // >= 0: the rows write partial results, each to its
+                       // row's slot (Row::slot, ItemRec::aux); -1: final rows
+                       // written straight to o / lse
   int32_t keys;        // visible-key estimate (cost, for ordering only)
   int32_t flags;       // kItemStream: keys read by this item only (stream them)
   int32_t s0_key_begin;   // the first span (when n_spans > 0)
@@ -48,11 +49,14 @@ struct Item {
 constexpr int32_t kItemStream = 1;
 
 // What the 64 lanes of a narrow item's wavefront read at its start, one
-// 32-bit word each (256 bytes): the q_row and chunk position of each of its
-// (up to 16) rows, and the page ids of the first 32 pages of its first span.
+// 32-bit word each (256 bytes): the q_row of each of its (up to 16) rows, a
+// second word per row, and the page ids of the first 32 pages of its first
+// span. The second word is the row's chunk position for a prefill item (the
+// causal mask needs it; prefill rows are always final) and its partial slot
+// for a decode item that writes partials (decode has no mask).
 struct ItemRec {
   int32_t q_row[16];   // -1 past n_rows
-  int32_t qpos[16];
+  int32_t aux[16];
   int32_t page[32];
 };
 // Narrow items' spans are cut at this many keys, so that the first span's
@@ -74,13 +78,14 @@ constexpr int kMaxSpanKeys = 1024;
 
 // One query row: its row index into q / o (token * H_q + head), its
 // position inside the prefill chunk (for the causal span) and, for a row
-// whose keys are split over several items, its merge-list entry.
+// whose keys are split over several items, its merge-list entry and the
+// workspace slot of this item's partial result. The partials of merge entry
+// m fill slots merge_indptr[m] .. merge_indptr[m + 1] - 1.
 struct Row {
   int32_t q_row;
   int32_t qpos;
   int32_t merge_idx;   // entry in the merge list, or -1 when the row is final here
-                       // (inspection only; the merge kernel walks the list)
-  int32_t pad;
+  int32_t slot;        // partial slot, or -1 when the row is final here
 };
 
 // Offsets (bytes) of the arrays packed in the device metadata buffer.
@@ -95,7 +100,7 @@ struct MetaLayout {
   size_t rows = 0;           // Row   [n_rows]
   size_t merge_rows = 0;     // int32 [n_merge] output row (q_row) per merge entry
   size_t merge_indptr = 0;   // int32 [n_merge + 1]
-  size_t merge_parts = 0;    // int32 [n_parts] partial row ids
+  size_t merge_parts = 0;    // int32 [n_parts] partial slot ids (merge_indptr[m] + k)
   size_t total = 0;
 };
 

@@ -311,7 +311,8 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
 
   // The item's lane record (one load per field, all in flight together):
   // this lane's row, and page j of the first span in lane j.
-  Row row{rec->q_row[col], rec->qpos[col], -1, 0};
+  // (aux: chunk position for a prefill item, partial slot for a decode one)
+  Row row{rec->q_row[col], rec->aux[col], -1, rec->aux[col]};
   const int32_t vpid0 = rec->page[lane & 31];
 
   F qf[NS];
@@ -505,7 +506,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
   const float lse2 = lsum > 0.f ? m + __log2f(lsum) : kNegInf;
   if (it.part_base >= 0) {
     if (has_row) {
-      const int64_t prow = (int64_t)it.part_base + col;
+      const int64_t prow = row.slot;
       float* dst = a.part_o + prow * D + 4 * grp;
 #pragma unroll
       for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[b] * inv);
@@ -555,6 +556,7 @@ __device__ __forceinline__ void merge_split(const AttnArgs& a, const Item& it, c
   const bool has_row = col < it.n_rows;
   if (!has_row) return;
   const int q_row = rec->q_row[col];
+  const int64_t slot = rec->aux[col];
   const float inv = L > 0.f ? 1.f / L : 0.f;
   const float lse2 = L > 0.f ? M + __log2f(L) : kNegInf;
   for (int b = part; b < NB; b += split) {
@@ -563,11 +565,11 @@ __device__ __forceinline__ void merge_split(const AttnArgs& a, const Item& it, c
     for (int q = 0; q < kMaxSplit; ++q)
       if (q < split) o += sq[q] * *reinterpret_cast<const f32x4_t*>(red0 + q * kRed + (b * 64 + lane) * 4);
     o *= inv;
-    if (it.part_base >= 0) store4(a.part_o + ((int64_t)it.part_base + col) * D + 16 * b + 4 * grp, o);
+    if (it.part_base >= 0) store4(a.part_o + slot * D + 16 * b + 4 * grp, o);
     else store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 16 * b + 4 * grp, o);
   }
   if (part == 0 && grp == 0) {
-    if (it.part_base >= 0) a.part_lse[it.part_base + col] = lse2;
+    if (it.part_base >= 0) a.part_lse[slot] = lse2;
     else if (a.lse) a.lse[q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
   }
 }
@@ -666,7 +668,7 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
 
   // This lane's row: row c of this wave's block.
   const int r = wave * 32 + c;
-  const Row row = r < it.n_rows ? a.rows[it.row_begin + r] : Row{-1, 0, -1, 0};
+  const Row row = r < it.n_rows ? a.rows[it.row_begin + r] : Row{-1, 0, -1, -1};
   F qf[NK];
   {
     const T* qp = static_cast<const T*>(a.q) + (int64_t)(row.q_row < 0 ? 0 : row.q_row) * D + 8 * h;
@@ -983,7 +985,7 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
     const float inv = l > 0.f ? 1.f / l : 0.f;
     const float lse2 = l > 0.f ? m + __log2f(l) : kNegInf;
     if (it.part_base >= 0) {
-      const int64_t prow = (int64_t)it.part_base + r;
+      const int64_t prow = row.slot;
       float* dst = a.part_o + prow * D + 4 * h;
 #pragma unroll
       for (int b = 0; b < NO; ++b)
@@ -1048,7 +1050,6 @@ struct MergeArgs {
   const float* part_lse;
   const int32_t* merge_rows;
   const int32_t* merge_indptr;
-  const int32_t* merge_parts;
   void* o;
   float* lse;
   int32_t n_merge;
@@ -1058,9 +1059,11 @@ struct MergeArgs {
 // normalized o_i and lse_i (log2) of disjoint key sets:
 //   M = max_i lse_i,  w_i = 2^(lse_i - M),  O = sum w_i o_i / sum w_i,
 //   LSE = (M + log2 sum w_i) * ln 2
-// which is exact in real arithmetic (shared == unshared, §3 "Scope"). One
-// group of D/4 threads per row, 4 dims per thread; the partial ids and
-// LSEs of up to 8 parts are fetched together so the loads overlap.
+// which is exact in real arithmetic (shared == unshared, §3 "Scope"). The
+// partials of merge entry r sit in slots merge_indptr[r] ..
+// merge_indptr[r + 1] - 1, so a row needs one metadata load before its
+// partials. One group of D/4 threads per row, 4 dims per thread; the LSEs
+// and partials of up to 8 slots are fetched together so the loads overlap.
 template <int D, typename TO>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
   constexpr int TPR = D / 4;
@@ -1079,7 +1082,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     int pid[kBatch];
     float l[kBatch];
 #pragma unroll
-    for (int k = 0; k < kBatch; ++k) pid[k] = pb + k < p1 ? a.merge_parts[pb + k] : -1;
+    for (int k = 0; k < kBatch; ++k) pid[k] = pb + k < p1 ? pb + k : -1;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) l[k] = pid[k] >= 0 ? a.part_lse[pid[k]] : kNegInf;
     f32x4_t v[kBatch];
@@ -1259,7 +1262,6 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),
                   reinterpret_cast<const int32_t*>(m + L.merge_indptr),
-                  reinterpret_cast<const int32_t*>(m + L.merge_parts),
                   o, lse, plan->n_merge};
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();   // clear any stale error of the caller

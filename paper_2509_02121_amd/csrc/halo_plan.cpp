@@ -293,7 +293,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       for (int g = 0; g < Hkv; ++g) {
         std::vector<Row> rows;
         for (int32_t r : seg_reqs[s])
-          for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, 0});
+          for (int j = 0; j < G; ++j) rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, -1});
         // chunk-major, row group innermost: items reading the same pages
         // are neighbours in the launch order.
         for (const Span& piece : sp) {
@@ -338,7 +338,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
           for (int j0 = 0; j0 < G; j0 += kRowsPerItem) {
             Proto pr;
             for (int j = j0; j < std::min(G, j0 + kRowsPerItem); ++j)
-              pr.rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, 0});
+              pr.rows.push_back(Row{(int32_t)(r * Hq + g * G + j), 0, -1, -1});
             pr.spans = ch;
             pr.kv_head = g;
             pr.keys = keys;
@@ -371,7 +371,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         std::vector<Row> rows;
         for (int32_t i = 0; i < n; ++i)
           for (int j = 0; j < G; ++j)
-            rows.push_back(Row{(int32_t)((tok0[r] + i) * Hq + g * G + j), i, -1, 0});
+            rows.push_back(Row{(int32_t)((tok0[r] + i) * Hq + g * G + j), i, -1, -1});
         for (size_t rb = 0; rb < rows.size(); rb += rows_per) {
           Proto pr;
           pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
@@ -399,7 +399,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   if (!prefill) {
     std::vector<std::vector<Row>> empty(Hkv);
     for (int64_t qr = 0; qr < n_q_rows * Hq; ++qr)
-      if (n_parts[qr] == 0) empty[(qr % Hq) / G].push_back(Row{(int32_t)qr, 0, -1, 0});
+      if (n_parts[qr] == 0) empty[(qr % Hq) / G].push_back(Row{(int32_t)qr, 0, -1, -1});
     for (int g = 0; g < Hkv; ++g)
     for (size_t i = 0; i < empty[g].size(); i += kRowsPerItem) {
       Proto pr;
@@ -484,14 +484,20 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   // partial results (several, or one from an item that also holds
   // multi-part rows); the merge kernel combines them after the attention
   // kernels.
+  // The partials of one merge entry get consecutive workspace slots, so the
+  // merge reads a row's partials as one range.
   std::vector<int32_t> merge_rows, merge_indptr{0}, merge_parts;
   if (!prefill) {
     std::vector<int32_t> merge_of(n_q_rows * Hq, -1);
+    std::vector<int32_t> slot_of_part(part_rows, -1);
     for (int64_t qr = 0; qr < n_q_rows * Hq; ++qr) {
       if (row_parts[qr].empty()) continue;   // written by a final item
       merge_of[qr] = (int32_t)merge_rows.size();
       merge_rows.push_back((int32_t)qr);
-      merge_parts.insert(merge_parts.end(), row_parts[qr].begin(), row_parts[qr].end());
+      for (int32_t pid : row_parts[qr]) {
+        slot_of_part[pid] = (int32_t)merge_parts.size();
+        merge_parts.push_back((int32_t)merge_parts.size());
+      }
       merge_indptr.push_back((int32_t)merge_parts.size());
     }
     for (const std::vector<Item>* list : {&items, &witems})
@@ -500,6 +506,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
           for (int32_t k = 0; k < it.n_rows; ++k) {
             Row& row = rows[it.row_begin + k];
             row.merge_idx = merge_of[row.q_row];
+            row.slot = slot_of_part[it.part_base + k];
           }
   }
 
@@ -600,7 +607,8 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         ItemRec& rc = recs[at];
         for (int r = 0; r < 16; ++r) {
           rc.q_row[r] = r < it.n_rows ? rows[it.row_begin + r].q_row : -1;
-          rc.qpos[r] = r < it.n_rows ? rows[it.row_begin + r].qpos : 0;
+          rc.aux[r] = r >= it.n_rows ? 0 : it.part_base >= 0 ? rows[it.row_begin + r].slot
+                                                             : rows[it.row_begin + r].qpos;
         }
         if (it.n_spans > 0) {
           const Span& s0 = spans[it.span_begin];

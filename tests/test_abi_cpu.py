@@ -107,7 +107,8 @@ def _check_plan(w, plan):
     for it, rc in zip(slot_items[used], recs[used]):
         nr = it[1]
         assert np.array_equal(rc[:nr], rows[it[0]:it[0] + nr, 0]) and (rc[nr:16] == -1).all()
-        assert np.array_equal(rc[16:16 + nr], rows[it[0]:it[0] + nr, 1])
+        second = rows[it[0]:it[0] + nr, 3] if it[5] >= 0 else rows[it[0]:it[0] + nr, 1]
+        assert np.array_equal(rc[16:16 + nr], second), "aux word: partial slot or chunk position"
         if it[3] > 0:
             sp = spans[it[2]]
             assert tuple(it[8:11]) == (sp[1], sp[2], sp[3]), "inline first span"
@@ -133,7 +134,8 @@ def _check_plan(w, plan):
     q_row = rows[row_idx, 0].astype(np.int64)
     qpos = rows[row_idx, 1].astype(np.int64)
     assert ((q_row % hq) // group == items[it_rep, 4]).all(), "row outside the item's kv head"
-    part = np.where(items[it_rep, 5] >= 0, items[it_rep, 5] + (row_idx - items[it_rep, 0]), -1)
+    part = np.where(items[it_rep, 5] >= 0, rows[row_idx, 3], -1)
+    assert (rows[row_idx, 3][items[it_rep, 5] < 0] == -1).all(), "final rows have no slot"
     # every (item, row, span) interval
     ns = items[it_rep, 3]
     ir = np.repeat(np.arange(len(it_rep)), ns)
@@ -178,6 +180,8 @@ def _check_plan(w, plan):
     for i, r_ in enumerate(mrows.tolist()):
         got_parts = set(m["merge_parts"][m["merge_indptr"][i]:m["merge_indptr"][i + 1]].tolist())
         assert got_parts == by_row.get(r_, set())
+        # an entry's partials fill its slot range
+        assert got_parts == set(range(m["merge_indptr"][i], m["merge_indptr"][i + 1]))
     st = plan.stats()
     assert st["visible_pairs"] == int(eh.sum())
     assert st["num_items"] == n_narrow and st["num_wide_items"] == len(items) - n_narrow
