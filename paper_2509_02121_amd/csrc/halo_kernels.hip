@@ -831,6 +831,7 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
     mt = halves_max(mt) * a.scale_log2;
     const bool move = mt > m + kRescaleLog2;
     if (__any(move)) {
+      asm volatile("");   // a real branch (see the fast iteration)
       const float m_new = move ? mt : m;
       const float alpha = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - m_new);
       lsum *= alpha;
@@ -959,6 +960,9 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
           float alpha;
           fast_iter(lds[pv_st], lds[nx], pf[nxt_p], sacc[cur_p], sacc[nxt_p], pf[cur_p], alpha);
           if (__any(alpha != 1.f)) {
+            // the empty volatile asm keeps this a real branch: if-converted,
+            // the rescale would cost 64 multiplies on every step
+            asm volatile("");
 #pragma unroll
             for (int b = 0; b < NO; ++b) acc[b] *= alpha;
           }

@@ -222,18 +222,16 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
 
   if (!prefill) {
     const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, kMaxSpanKeys) / 32 * 32;
-    // Private chunks: 512 keys, or 1024 when that still leaves >= 16K items
-    // (fewer partials to write and merge; the sweep over the three decode
-    // workloads favours these).
-    int64_t private_keys = 0;
-    {
-      std::vector<int32_t> rc(S, 0);
-      for (int r = 0; r < R; ++r)
-        for (int32_t i = path_begin(r); i < path_end(r); ++i) rc[f.req_seg_ids[i]]++;
-      for (int s = 0; s < S; ++s)
-        if (rc[s] == 1) private_keys += f.seg_len[s];
+    // Private chunks: 1024 keys when that still leaves >= 512 items (two per
+    // CU; fewer partials to write and merge), else 512.
+    int64_t items_at_1024 = 0;
+    for (int r = 0; r < R; ++r) {
+      int64_t priv = 0;
+      for (int32_t i = path_begin(r); i < path_end(r); ++i)
+        if (refs[f.req_seg_ids[i]] == 1) priv += f.seg_len[f.req_seg_ids[i]];
+      items_at_1024 += ceil_div(priv, 1024) * Hkv;
     }
-    const int kc_private_default = private_keys * Hkv / 1024 >= 16384 ? 1024 : 512;
+    const int kc_private_default = items_at_1024 >= 2 * kNumCUs ? 1024 : 512;
     const int kc_private = env_int("HALO_KC_PRIVATE", kc_private_default, 32, kMaxSpanKeys) / 32 * 32;
     for (int r = 0; r < R; ++r) {
       int64_t keys = 0;
@@ -241,10 +239,12 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       plan->visible_pairs += keys * Hq;
     }
     // Grouped prefix pass: shared segments, all their rows stacked. With
-    // bf16 inputs the rows go to wide items (a 4-wave workgroup reading each
-    // page once for up to 256 rows); the row-block count per wave follows the
-    // row-weighted size of the shared groups, and the key chunk shrinks until
-    // there are enough workgroups to cover the GPU.
+    // bf16 inputs and enough shared work the rows go to wide items (an 8-wave
+    // workgroup reading each page once for up to 256 rows); the rows per item
+    // follow the row-weighted size of the shared groups, and the key chunk
+    // (at most 2048 keys) shrinks until there are >= 128 wide items. Longer
+    // chunks mean fewer partials to write and merge, and a wide item's ring
+    // start-up and 256-row epilogue are paid fewer times.
     std::vector<std::vector<int32_t>> seg_reqs(S);
     for (int r = 0; r < R; ++r)
       for (int32_t i = path_begin(r); i < path_end(r); ++i) seg_reqs[f.req_seg_ids[i]].push_back(r);
@@ -274,8 +274,8 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       // row groups of one shared chunk read the same pages: keep up to 8 of
       // them on one XCD
       plan->wide_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / rows_per)));
-      const int min_items = env_int("HALO_WIDE_MIN_ITEMS", 512, 1, 1 << 30);
-      kc = kMaxSpanKeys;
+      const int min_items = env_int("HALO_WIDE_MIN_ITEMS", 128, 1, 1 << 30);
+      kc = 2 * kMaxSpanKeys;
       while (kc > 128) {
         int64_t n = 0;
         for (int s = 0; s < S; ++s)
@@ -284,7 +284,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         if (n >= min_items) break;
         kc /= 2;
       }
-      kc = env_int("HALO_KC_WIDE", kc, 32, kMaxSpanKeys) / 32 * 32;
+      kc = env_int("HALO_KC_WIDE", kc, 32, 1 << 16) / 32 * 32;
     }
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
@@ -529,7 +529,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     while (waves % split) --split;
     plan->narrow_split = split;
     const int slots = waves / split;
-    const int cap = env_int("HALO_ITEMS_PER_BLOCK", witems.empty() ? slots : std::max(1, slots / 2), 1, slots);
+    const int cap = env_int("HALO_ITEMS_PER_BLOCK", slots, 1, slots);
     int64_t nb = std::max<int64_t>((n + cap - 1) / cap, std::min<int64_t>(n, kNumCUs));
     nb = (nb + 7) / 8 * 8;
     if (nb * slots > (int64_t)std::numeric_limits<int32_t>::max()) {
