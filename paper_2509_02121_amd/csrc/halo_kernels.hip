@@ -831,7 +831,6 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
     mt = halves_max(mt) * a.scale_log2;
     const bool move = mt > m + kRescaleLog2;
     if (__any(move)) {
-      asm volatile("");   // a real branch (see the fast iteration)
       const float m_new = move ? mt : m;
       const float alpha = m == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m - m_new);
       lsum *= alpha;
@@ -875,11 +874,15 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
     f32x16_t sn = f32x16_t{};
 #pragma unroll
     for (int s = 0; s < NK; ++s) sn = mma32(kf[s], qf[s], sn);
-    // softmax of step t (no masks: full step)
-    float mt = fmaxf(fmaxf(fmaxf(sacc_cur[0], sacc_cur[1]), fmaxf(sacc_cur[2], sacc_cur[3])),
-                     fmaxf(fmaxf(sacc_cur[4], sacc_cur[5]), fmaxf(sacc_cur[6], sacc_cur[7])));
-    mt = fmaxf(mt, fmaxf(fmaxf(fmaxf(sacc_cur[8], sacc_cur[9]), fmaxf(sacc_cur[10], sacc_cur[11])),
-                         fmaxf(fmaxf(sacc_cur[12], sacc_cur[13]), fmaxf(sacc_cur[14], sacc_cur[15]))));
+    // softmax of step t (no masks: full step); the max as a tree of
+    // three-input maxima (v_max3_f32, 8 instructions for 16 scores)
+    auto max3 = [](float x, float y, float z) { return fmaxf(fmaxf(x, y), z); };
+    const float m0 = max3(sacc_cur[0], sacc_cur[1], sacc_cur[2]);
+    const float m1 = max3(sacc_cur[3], sacc_cur[4], sacc_cur[5]);
+    const float m2 = max3(sacc_cur[6], sacc_cur[7], sacc_cur[8]);
+    const float m3 = max3(sacc_cur[9], sacc_cur[10], sacc_cur[11]);
+    const float m4 = max3(sacc_cur[12], sacc_cur[13], sacc_cur[14]);
+    float mt = fmaxf(max3(m0, m1, m2), max3(m3, m4, sacc_cur[15]));
     mt = halves_max(mt) * a.scale_log2;
     const bool move = mt > m + kRescaleLog2;
     const float m_new = move ? mt : m;
@@ -889,10 +892,6 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
     float pr[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) pr[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc_cur[i], a.scale_log2, -m_use));
-    float ps = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; i += 4) ps += (pr[i] + pr[i + 1]) + (pr[i + 2] + pr[i + 3]);
-    lsum = __builtin_fmaf(lsum, alpha, ps);
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
       float half[8];
@@ -900,6 +899,10 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
       for (int j = 0; j < 8; ++j) half[j] = pr[8 * g + j];
       pf_cur[g] = to_frag(half, (F*)nullptr);
     }
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; i += 4) ps += (pr[i] + pr[i + 1]) + (pr[i + 2] + pr[i + 3]);
+    lsum = __builtin_fmaf(lsum, alpha, ps);
     sacc_nxt = sn;
     // keep the softmax results in this block (they are consumed only after
     // the next barrier, and would otherwise sink below the rescale branch)
@@ -960,9 +963,6 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
           float alpha;
           fast_iter(lds[pv_st], lds[nx], pf[nxt_p], sacc[cur_p], sacc[nxt_p], pf[cur_p], alpha);
           if (__any(alpha != 1.f)) {
-            // the empty volatile asm keeps this a real branch: if-converted,
-            // the rescale would cost 64 multiplies on every step
-            asm volatile("");
 #pragma unroll
             for (int b = 0; b < NO; ++b) acc[b] *= alpha;
           }
