@@ -90,9 +90,16 @@ def cpu_baseline(w, min_seconds=10.0):
                 break
         sample = f"{passes} request(s) of {int(w.q_len[0])} new tokens each"
     dt = time.perf_counter() - t0
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:  # pragma: no cover
+        pass
     return {"value": tokens / dt, "unit": "query-tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": sample, "seconds": round(dt, 3),
-            "host_cpus": len(os.sched_getaffinity(0))}
+            "host_cpus": len(os.sched_getaffinity(0)), "os_cpu_count": os.cpu_count(),
+            "cpu_model": model, "blas_threads": int(threads)}
 
 
 def main():
@@ -107,7 +114,11 @@ def main():
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (from rocprofv3 counters), if present")
     ap.add_argument("--copy-bytes", type=int, default=0,
-                    help="only run one plain device copy of this many bytes (counter calibration)")
+                    help="only run a plain device copy of this many bytes (counter calibration; "
+                         "also reports its rate as the streaming context)")
+    ap.add_argument("--pool-fill", type=float, default=0.0,
+                    help="stress variant: grow the page pool to this fraction of the GPU's free "
+                         "memory, the needed pages scattered over it (TLB and page-spread effects)")
     args = ap.parse_args()
     if args.copy_bytes:
         import torch
@@ -115,9 +126,18 @@ def main():
         src = torch.ones(n, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        dst.copy_(src)   # the calibration dispatch
         torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes": n * 4}), flush=True)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 5
+        print(json.dumps({"copy_bytes": n * 4, "copy_us": round(ms * 1e3, 2),
+                          "copy_gbps_read_plus_write": round(2 * n * 4 / (ms / 1e3) / 1e9, 1)}), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
@@ -132,6 +152,16 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = make_config(args.workload, device=dev)
+    if args.pool_fill > 0:
+        # same forest and values, in a pool of pool_fill x (free memory): the
+        # needed pages land at random over the whole pool
+        page_bytes = (w.k_pool[0].numel() + w.v_pool[0].numel()) * w.k_pool.element_size()
+        have = w.num_pool_pages
+        del w
+        torch.cuda.empty_cache()
+        free = torch.cuda.mem_get_info(dev)[0]
+        target = int(args.pool_fill * free) // page_bytes
+        w = make_config(args.workload, device=dev, extra_pages=max(0, target - have))
     params = halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages,
                               w.scale, w.dtype)
     runner = halo.PrefixAttention(params, w.forest_csr(), dev)
@@ -167,6 +197,18 @@ def main():
     wall_ms = (t1 - t0) * 1e3 / args.steps
     gpu_ms = ev0.elapsed_time(ev1) / args.steps
 
+    # Spread of single calls (a separate pass, one event pair per call).
+    per_call = []
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(min(args.steps, 200))]
+    for i, (a, b) in enumerate(pairs):
+        a.record(stream)
+        step(i)
+        b.record(stream)
+    torch.cuda.synchronize()
+    per_call = sorted(a.elapsed_time(b) * 1e3 for a, b in pairs)
+    pct = lambda f: round(per_call[min(len(per_call) - 1, int(f * len(per_call)))], 2)
+
     q_tokens = w.q.shape[0]
     alg_bytes = algorithmic_bytes(w, stats)
     value = q_tokens / (wall_ms / 1e3)
@@ -180,7 +222,7 @@ def main():
         with open(args.traffic_json) as f:
             tr = json.load(f)
         sha = source_sha256()
-        if tr.get("_kernel_source_sha256") == sha and w.name in tr:
+        if tr.get("_kernel_source_sha256") == sha and w.name in tr and not args.pool_fill:
             traffic = tr[w.name]["bytes_per_call"]
     except (OSError, ValueError, KeyError):
         traffic = None
@@ -222,13 +264,15 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
         "data": "synthetic",
+        "per_call_us": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9), "calls": len(per_call)},
         "effective_hbm_gbps": round(eff_gbps, 1),
         "hbm_roofline_frac": round(eff_gbps / HBM_PEAK_GBPS, 4),
         "config": {"workload": w.name, "requests": w.num_requests, "query_tokens": q_tokens,
                    "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
                    "head_dim": w.head_dim, "page_size": w.page_size,
                    "distinct_kv_tokens": stats["distinct_kv_tokens"], "replicas": n_rep,
-                   "work_items": stats["num_items"], "merge_rows": stats["num_merge_rows"]},
+                   "work_items": stats["num_items"], "merge_rows": stats["num_merge_rows"],
+                   "pool_gb": round(pool_bytes / 1e9, 2), "pool_pages": int(w.num_pool_pages)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }
