@@ -102,6 +102,103 @@ def cpu_baseline(w, min_seconds=10.0):
             "cpu_model": model, "blas_threads": int(threads)}
 
 
+def _time_launches(call, steps, warmup, stream):
+    """Average GPU time of one launch: HIP events on the launch stream around
+    `steps` back-to-back launches."""
+    import torch
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / steps
+
+
+def write_path_bench(args):
+    """Paged-KV write path on the workload's own page lists (one JSON line).
+
+    Scatter: every request's last segment (its private suffix, or its prefill
+    chunk) is the target; decode appends the segment's last token (start =
+    length - 1, count 1), prefill writes the whole chunk. Copy: one page per
+    request, the first page of its last segment, to a distinct free page of
+    the pool (the copy of copy-on-write; distinct sources, so that no copy
+    reads another's source out of cache). Algorithmic bytes: the
+    token bytes read from the input plus the same bytes written to the pool
+    (scatter); a page read plus a page written (copy)."""
+    import numpy as np
+    import torch
+    from paper_2509_02121_amd import halo
+    from workloads import make_config
+
+    halo.load_library(require_gpu=True)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = make_config(args.workload, device=dev, poison=False)
+    params = halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages,
+                              w.scale, w.dtype)
+    R = w.num_requests
+    elt = w.k_pool.element_size()
+    tok_bytes = w.num_kv_heads * w.head_dim * elt          # one token, one pool
+    last = [w.req_paths[r][-1] for r in range(R)]
+    lens = np.array([int(w.seg_len[s]) for s in last], np.int64)
+    if w.is_prefill:
+        start, count = np.zeros(R, np.int32), lens.astype(np.int32)
+    else:
+        start, count = (lens - 1).astype(np.int32), np.ones(R, np.int32)
+    pages = [np.asarray(w.seg_pages[s], np.int32) for s in last]
+    indptr = np.zeros(R + 1, np.int32)
+    indptr[1:] = np.cumsum([len(p) for p in pages])
+    offs = np.zeros(R, np.int64)
+    offs[1:] = np.cumsum(count)[:-1]
+    n_tok = int(count.sum())
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    src = torch.randn((n_tok, w.num_kv_heads, w.head_dim), generator=gen, device=dev).to(w.dtype)
+    t = lambda a: torch.as_tensor(a, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    sc_args = (t(np.concatenate(pages)), t(indptr), t(start), t(count), t(offs), src, flag, stream)
+    used = np.zeros(w.num_pool_pages, bool)
+    for p in w.seg_pages:
+        used[np.asarray(p, np.int64)] = True
+    free = np.nonzero(~used)[0].astype(np.int32)
+    if len(free) < R:
+        raise SystemExit(f"pool has {len(free)} free pages, {R} needed for the copies")
+    cp_src = t(np.array([int(w.seg_pages[s][0]) for s in last], np.int32))
+    cp_dst = t(free[:R])
+    res = {}
+    for name, pool, kind in (("k", w.k_pool, halo.HALO_POOL_K), ("v", w.v_pool, halo.HALO_POOL_V)):
+        call = halo.bind_kv_page_scatter(pool, params, kind, *sc_args[:5], src, flag, stream)
+        res["scatter_" + name + "_us"] = _time_launches(call, args.steps, args.warmup, stream)
+    call = halo.bind_kv_page_copy(w.k_pool, params, cp_src, cp_dst, flag, stream)
+    res["copy_us"] = _time_launches(call, args.steps, args.warmup, stream)
+    torch.cuda.synchronize()
+    if int(flag.item()):
+        raise SystemExit("write path flagged bad input")
+    sc_bytes = 2 * n_tok * tok_bytes
+    page_bytes = w.num_kv_heads * w.page_size * w.head_dim * elt
+    cp_bytes = 2 * R * page_bytes
+    gbps = lambda b, us: round(b / (us * 1e-6) / 1e9, 1)
+    line = {
+        "metric": "paged-KV write path: HBM GB/s per launch",
+        "config": {"workload": w.name, "mode": "prefill chunk write" if w.is_prefill else "decode append",
+                   "sequences": R, "tokens": n_tok, "copy_pages": R, "steps": args.steps},
+        "scatter_bytes": sc_bytes, "copy_bytes": cp_bytes,
+    }
+    for name in ("k", "v"):
+        us = res["scatter_" + name + "_us"]
+        line["scatter_" + name] = {"us": round(us, 2), "gbps": gbps(sc_bytes, us),
+                                   "frac": round(gbps(sc_bytes, us) / HBM_PEAK_GBPS, 4)}
+    line["copy"] = {"us": round(res["copy_us"], 2), "gbps": gbps(cp_bytes, res["copy_us"]),
+                    "frac": round(gbps(cp_bytes, res["copy_us"]) / HBM_PEAK_GBPS, 4)}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -119,7 +216,17 @@ def main():
     ap.add_argument("--pool-fill", type=float, default=0.0,
                     help="stress variant: grow the page pool to this fraction of the GPU's free "
                          "memory, the needed pages scattered over it (TLB and page-spread effects)")
+    ap.add_argument("--write-path", action="store_true",
+                    help="only time the paged-KV write path on the workload's page lists: each "
+                         "request's newest token appended (decode) or its chunk written (prefill), "
+                         "K and V pools, and a copy-on-write page copy per request")
     args = ap.parse_args()
+    if args.write_path:
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        write_path_bench(args)
+        return
     if args.copy_bytes:
         import torch
         n = args.copy_bytes // 4

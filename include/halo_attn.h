@@ -169,6 +169,46 @@ halo_status_t halo_kv_page_gather(const void* pool, const halo_attn_params_t* pa
                                   int32_t num_seqs, void* out, int32_t* error_flag,
                                   void* stream);
 
+/* Page scatter, the write path of the paged KV cache (§7 PagedAttention;
+ * §2 KV reuse: new tokens are written once, then read by every request
+ * that shares them): the inverse of halo_kv_page_gather.
+ *   token start + t of sequence i, head h  <-  in[in_token_offset[i] + t][h][:]
+ * for 0 <= t < seq_count[i], start = seq_start[i]; the token at position p
+ * of sequence i lives in page page_ids[seq_page_indptr[i] + p / page_size],
+ * slot p % page_size, stored in the pool_kind layout. A decode step appends
+ * one token (count 1, start = the sequence's length so far); a prefill
+ * chunk writes its q_len tokens. Slots of tokens outside the written range
+ * are left untouched. page_ids, seq_page_indptr, seq_start, seq_count,
+ * in_token_offset and in are DEVICE pointers; in is [*][num_kv_heads]
+ * [head_dim] of kv_dtype, bits copied unchanged; pool and in must be 16-byte
+ * aligned. Only params' num_kv_heads,
+ * head_dim, page_size, num_pool_pages and kv_dtype are used. A sequence whose
+ * range does not fit its page list (start < 0 or start + count > pages *
+ * page_size) is skipped whole, and a touched page whose id is outside
+ * [0, num_pool_pages) is skipped (the sequence's other pages are written);
+ * either way, if error_flag (device int32, may be NULL) is given, 1 is
+ * written there (0 never is). Two sequences must not write the same slot.
+ * in_token_offset[i] + seq_count[i] must not exceed the rows of in. */
+halo_status_t halo_kv_page_scatter(void* pool, const halo_attn_params_t* params,
+                                   halo_pool_kind_t pool_kind,
+                                   const int32_t* page_ids, const int32_t* seq_page_indptr,
+                                   const int32_t* seq_start, const int32_t* seq_count,
+                                   const int64_t* in_token_offset, int32_t num_seqs,
+                                   const void* in, int32_t* error_flag, void* stream);
+
+/* Whole-page copy inside one pool, every head, bit for bit: page dst_pages[k]
+ * becomes a copy of page src_pages[k], k < num_pages. This is the copy of
+ * copy-on-write: before a request writes into a page it shares with others
+ * (a shared prefix that ends inside a page), the caller copies that page to
+ * a private one, points the request's page list at the copy and writes there.
+ * Call once per pool. src_pages and dst_pages are DEVICE int32 arrays; pool
+ * must be 16-byte aligned. dst pages must be distinct and none may also be a
+ * src page of the same call. Ids outside [0, num_pool_pages) are skipped and
+ * flagged as for the scatter. */
+halo_status_t halo_kv_page_copy(void* pool, const halo_attn_params_t* params,
+                                const int32_t* src_pages, const int32_t* dst_pages,
+                                int32_t num_pages, int32_t* error_flag, void* stream);
+
 /* Plan statistics for callers and benchmarks (host memory, no device work). */
 typedef struct {
   int32_t is_prefill;

@@ -61,6 +61,7 @@ EXPORTED_SYMBOLS = (
     "halo_plan_create", "halo_plan_upload", "halo_plan_destroy", "halo_plan_get_stats",
     "halo_plan_inspect",
     "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_kv_page_gather",
+    "halo_kv_page_scatter", "halo_kv_page_copy",
     "halo_status_string", "halo_last_error_message",
 )
 
@@ -123,6 +124,11 @@ def load_library(require_gpu=False):
     lib.halo_kv_page_gather.argtypes = [vp, ctypes.POINTER(AttnParams), ctypes.c_int, vp, vp, vp, vp,
                                         ctypes.c_int32, vp, vp, vp]
     lib.halo_kv_page_gather.restype = ctypes.c_int
+    lib.halo_kv_page_scatter.argtypes = [vp, ctypes.POINTER(AttnParams), ctypes.c_int, vp, vp, vp, vp, vp,
+                                         ctypes.c_int32, vp, vp, vp]
+    lib.halo_kv_page_scatter.restype = ctypes.c_int
+    lib.halo_kv_page_copy.argtypes = [vp, ctypes.POINTER(AttnParams), vp, vp, ctypes.c_int32, vp, vp]
+    lib.halo_kv_page_copy.restype = ctypes.c_int
     lib.halo_status_string.argtypes = [ctypes.c_int]
     lib.halo_status_string.restype = ctypes.c_char_p
     lib.halo_last_error_message.argtypes = []
@@ -271,6 +277,61 @@ def kv_page_gather(pool, params, pool_kind, page_ids, seq_page_indptr, seq_len, 
                                     out.data_ptr(),
                                     error_flag.data_ptr() if error_flag is not None else None,
                                     _stream_handle(stream)))
+
+
+def kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq_start, seq_count,
+                    in_token_offset, src, error_flag=None, stream=None):
+    """halo_kv_page_scatter on torch tensors (int arrays on the GPU)."""
+    load_library()
+    _check(_LIB.halo_kv_page_scatter(pool.data_ptr(), ctypes.byref(params), int(pool_kind),
+                                     page_ids.data_ptr(), seq_page_indptr.data_ptr(), seq_start.data_ptr(),
+                                     seq_count.data_ptr(), in_token_offset.data_ptr(),
+                                     int(seq_page_indptr.numel() - 1), src.data_ptr(),
+                                     error_flag.data_ptr() if error_flag is not None else None,
+                                     _stream_handle(stream)))
+
+
+def kv_page_copy(pool, params, src_pages, dst_pages, error_flag=None, stream=None):
+    """halo_kv_page_copy on torch tensors (int arrays on the GPU)."""
+    load_library()
+    _check(_LIB.halo_kv_page_copy(pool.data_ptr(), ctypes.byref(params), src_pages.data_ptr(),
+                                  dst_pages.data_ptr(), int(src_pages.numel()),
+                                  error_flag.data_ptr() if error_flag is not None else None,
+                                  _stream_handle(stream)))
+
+
+def bind_kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq_start, seq_count,
+                         in_token_offset, src, error_flag=None, stream=None):
+    """A zero-argument callable that enqueues kv_page_scatter with every
+    pointer converted once (for tight timing loops); the tensors and params
+    must stay alive while it is used."""
+    load_library()
+    args = (pool.data_ptr(), ctypes.byref(params), int(pool_kind), page_ids.data_ptr(),
+            seq_page_indptr.data_ptr(), seq_start.data_ptr(), seq_count.data_ptr(),
+            in_token_offset.data_ptr(), int(seq_page_indptr.numel() - 1), src.data_ptr(),
+            error_flag.data_ptr() if error_flag is not None else None, _stream_handle(stream))
+    fn = _LIB.halo_kv_page_scatter
+
+    def call():
+        st = fn(*args)
+        if st != HALO_OK:
+            _check(st)
+    return call
+
+
+def bind_kv_page_copy(pool, params, src_pages, dst_pages, error_flag=None, stream=None):
+    """kv_page_copy as a zero-argument callable (see bind_kv_page_scatter)."""
+    load_library()
+    args = (pool.data_ptr(), ctypes.byref(params), src_pages.data_ptr(), dst_pages.data_ptr(),
+            int(src_pages.numel()), error_flag.data_ptr() if error_flag is not None else None,
+            _stream_handle(stream))
+    fn = _LIB.halo_kv_page_copy
+
+    def call():
+        st = fn(*args)
+        if st != HALO_OK:
+            _check(st)
+    return call
 
 
 class PrefixAttention:

@@ -319,3 +319,25 @@ def test_run_calls_reject_bad_arguments_without_touching_the_gpu(lib):
     assert rc == halo.HALO_ERR_UNSUPPORTED
     rc = lib.halo_kv_page_gather(fake, ctypes.byref(params), 0, fake, fake, fake, fake, 0, fake, None, None)
     assert rc == halo.HALO_OK      # nothing to do
+    rc = lib.halo_kv_page_scatter(fake, ctypes.byref(p2), 1, fake, fake, fake, fake, fake, 1, fake, None, None)
+    assert rc == halo.HALO_ERR_UNSUPPORTED
+    rc = lib.halo_kv_page_scatter(fake, ctypes.byref(params), 1, fake, fake, None, fake, fake, 1, fake, None,
+                                  None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # seq_start NULL
+    rc = lib.halo_kv_page_scatter(fake, ctypes.byref(params), 2, fake, fake, fake, fake, fake, 1, fake, None,
+                                  None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # no such pool kind
+    rc = lib.halo_kv_page_scatter(fake, ctypes.byref(params), 0, fake, fake, fake, fake, fake, 0, fake, None,
+                                  None)
+    assert rc == halo.HALO_OK      # nothing to do
+    rc = lib.halo_kv_page_scatter(fake, ctypes.byref(params), 0, fake, fake, fake, fake, fake, 1, fake + 2, None,
+                                  None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # input not 16-byte aligned
+    rc = lib.halo_kv_page_copy(fake + 4, ctypes.byref(params), fake, fake, 1, None, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # pool not 16-byte aligned
+    rc = lib.halo_kv_page_copy(fake, ctypes.byref(p2), fake, fake, 1, None, None)
+    assert rc == halo.HALO_ERR_UNSUPPORTED
+    rc = lib.halo_kv_page_copy(fake, ctypes.byref(params), fake, fake, -1, None, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT
+    rc = lib.halo_kv_page_copy(fake, ctypes.byref(params), fake, fake, 0, None, None)
+    assert rc == halo.HALO_OK
