@@ -45,17 +45,20 @@ def build(verbose=True):
     try:
         plan_o = os.path.join(tmp, "halo_plan.o")
         kern_o = os.path.join(tmp, "halo_kernels.o")
+        pages_o = os.path.join(tmp, "halo_pages.o")
         procs = [
             subprocess.Popen(["g++", "-std=c++17", "-O2", "-fPIC", "-Wall", "-Wextra",
                               "-I", INCLUDE, "-c", os.path.join(CSRC, "halo_plan.cpp"), "-o", plan_o]),
             subprocess.Popen([HIPCC] + HIP_FLAGS + ["-I", INCLUDE, "-c",
                                                    os.path.join(CSRC, "halo_kernels.hip"), "-o", kern_o]),
+            subprocess.Popen([HIPCC] + HIP_FLAGS + ["-I", INCLUDE, "-c",
+                                                   os.path.join(CSRC, "halo_pages.hip"), "-o", pages_o]),
         ]
         rcs = [p.wait() for p in procs]
         if any(rcs):
             raise RuntimeError(f"compilation failed (exit codes {rcs})")
         out_tmp = LIB_PATH + ".tmp"
-        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, kern_o, "-o", out_tmp])
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, kern_o, pages_o, "-o", out_tmp])
         os.replace(out_tmp, LIB_PATH)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)

@@ -22,9 +22,7 @@
 //   launch so the kernel boundary makes every partial visible (an in-kernel
 //   last-arriver merge needs agent-scope release/acquire, i.e. L2
 //   write-back and invalidate, which measured 4x slower on this path).
-// gather_kernel: bit copy of paged tokens into a dense token-major buffer;
-// scatter_kernel and page_copy_kernel: the write path (new tokens into pages,
-// whole-page copies for copy-on-write).
+// The page gather and the write path live in halo_pages.hip.
 
 #include <hip/hip_runtime.h>
 
@@ -159,10 +157,6 @@ __device__ __forceinline__ void store4(__bf16* dst, f32x4_t v) {
   r[3] = (__bf16)v[3];
   *reinterpret_cast<uint2*>(dst) = __builtin_bit_cast(uint2, r);
 }
-
-// V pages keep the tokens of a dim row in the slot order 0-3, 8-11, 4-7,
-// 12-15 (bits 2 and 3 of the index swapped; the map is its own inverse).
-__device__ __forceinline__ int v_token_at_slot(int s) { return (s & 3) | ((s & 4) << 1) | ((s & 8) >> 1); }
 
 // Reductions over the four 16-lane rows of a wave (lanes l, l^16, l^32,
 // l^48) with the gfx950 row-swap instructions, which stay on the VALU
@@ -1119,245 +1113,6 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
   if (t == 0 && a.lse) a.lse[q_row] = wsum > 0.f ? (mx + __log2f(wsum)) * kLn2 : kNegInf;
 }
 
-// ---------------------------------------------------------------- gather
-
-struct GatherArgs {
-  const void* pool;
-  const int32_t* page_ids;
-  const int32_t* seq_page_indptr;
-  const int32_t* seq_len;
-  const int64_t* out_token_offset;
-  void* out;
-  int32_t* error_flag;
-  int64_t num_pool_pages;
-  int32_t num_seqs;
-  int32_t num_kv_heads;
-  int32_t head_dim;
-  int32_t v_layout;
-};
-
-// One block per (page slot, head) tile, grid-stride. W is an unsigned word of
-// the element's width, so every bit pattern (NaN payloads included) moves
-// unchanged.
-template <typename W>
-__global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
-  __shared__ W tile[16 * (128 + 1)];
-  const int D = a.head_dim;
-  const int64_t total_tiles = (int64_t)a.seq_page_indptr[a.num_seqs] * a.num_kv_heads;
-  const W* pool = static_cast<const W*>(a.pool);
-  W* out = static_cast<W*>(a.out);
-  for (int64_t tl = blockIdx.x; tl < total_tiles; tl += gridDim.x) {
-    const int64_t slot = tl / a.num_kv_heads;
-    const int h = (int)(tl % a.num_kv_heads);
-    int lo = 0, hi = a.num_seqs - 1;   // last sequence whose first slot <= slot
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.seq_page_indptr[mid] <= slot) lo = mid; else hi = mid - 1;
-    }
-    const int len = a.seq_len[lo];
-    const int npages = a.seq_page_indptr[lo + 1] - a.seq_page_indptr[lo];
-    const int pid = a.page_ids[slot];
-    if (len < 0 || npages != (len + 15) / 16 || pid < 0 || pid >= a.num_pool_pages) {
-      if (threadIdx.x == 0 && a.error_flag) a.error_flag[0] = 1;
-      continue;
-    }
-    const int t0 = (int)(slot - a.seq_page_indptr[lo]) * 16;
-    const int n = min(16, len - t0);
-    const int64_t out_tok = a.out_token_offset[lo] + t0;
-    const W* src = pool + ((int64_t)pid * a.num_kv_heads + h) * 16 * D;
-    // Read the whole (page, head) tile coalesced, in its stored order, and
-    // place element (token t, dim c) at tile[t][c] (row stride D + 1).
-    constexpr int E = 16 / (int)sizeof(W);
-    for (int e = threadIdx.x; e < 16 * D; e += blockDim.x) {
-      int t, c;
-      if (!a.v_layout) {           // K: [D/E][16][E]
-        c = (e / (16 * E)) * E + e % E;
-        t = (e / E) % 16;
-      } else {                     // V: [D][16], slots hold tokens 0-3, 8-11, 4-7, 12-15
-        c = e >> 4;
-        t = v_token_at_slot(e & 15);
-      }
-      tile[t * (D + 1) + c] = src[e];
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < n * D; e += blockDim.x) {
-      const int tok = e / D, c = e - tok * D;
-      out[((out_tok + tok) * a.num_kv_heads + h) * D + c] = tile[tok * (D + 1) + c];
-    }
-    __syncthreads();
-  }
-}
-
-// ---------------------------------------------------------------- write path
-
-struct ScatterArgs {
-  void* pool;
-  const int32_t* page_ids;
-  const int32_t* seq_page_indptr;
-  const int32_t* seq_start;
-  const int32_t* seq_count;
-  const int64_t* in_token_offset;
-  const void* in;
-  int32_t* error_flag;
-  int64_t num_pool_pages;
-  int32_t num_seqs;
-  int32_t num_kv_heads;
-  int32_t head_dim;
-  int32_t v_layout;
-};
-
-// The inverse of the gather: tokens start .. start + count - 1 of each
-// sequence are written from the dense input into their (page, head) tiles.
-// Blocks (x, y) take sequence x (grid-stride) and its touched tiles; each of
-// the block's four waves owns one tile at a time (tiles y*4 + wave, stepping
-// by gridDim.y*4), so only the pages the range touches are visited and a
-// decode append costs one tile per head whatever the sequence's length.
-// A full tile (16 touched tokens) is read with 16-byte loads, transposed in
-// the wave's own LDS buffer and written back as the tile's 4 KB (bf16,
-// d 128) in stored order, 16 bytes per lane. A partly touched tile (a
-// decode append, the ends of a chunk) is written straight from the input:
-// 16-byte vectors for K, whose vector (dim group, token) holds one token;
-// single elements for V, whose slots interleave tokens. Untouched slots are
-// never written. Words of the element's width keep every bit pattern.
-template <typename W, int D>
-__global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
-  constexpr int E = 16 / (int)sizeof(W);   // elements per 16-byte vector
-  constexpr int VPT = D / E;               // vectors per token and head
-  constexpr int TV = 16 * VPT;             // vectors per tile
-  constexpr int NV = TV / 64;              // vectors per lane for a full tile
-  constexpr int KROW = 17;                 // K staging: vector (j, t) at j * KROW + t
-  constexpr int KBUF = VPT * KROW;         // 16-byte vectors
-  // V staging: the tile in stored order, [D][16] elements, row c held at row
-  // c ^ ((c / E) & RMASK): the rows written by one instruction (dims
-  // j*E + q of four dim groups j) then fall in different 32-byte bank groups.
-  constexpr int RMASK = 128 / (16 * (int)sizeof(W)) - 1;
-  constexpr int VBUF = D * 16 / E;
-  constexpr int BUF = KBUF > VBUF ? KBUF : VBUF;
-  __shared__ u32x4_t stage[4][BUF];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int H = a.num_kv_heads;
-  const int64_t row = (int64_t)H * D;      // input elements per token
-  W* pool = static_cast<W*>(a.pool);
-  const W* in = static_cast<const W*>(a.in);
-  u32x4_t* kst = stage[wave];
-  W* vst = reinterpret_cast<W*>(stage[wave]);
-  for (int seq = blockIdx.x; seq < a.num_seqs; seq += gridDim.x) {
-    const int start = a.seq_start[seq], count = a.seq_count[seq];
-    if (count <= 0) continue;
-    const int base = a.seq_page_indptr[seq];
-    const int npages = a.seq_page_indptr[seq + 1] - base;
-    if (start < 0 || (int64_t)start + count > (int64_t)npages * 16) {
-      if (blockIdx.y == 0 && threadIdx.x == 0 && a.error_flag) a.error_flag[0] = 1;
-      continue;
-    }
-    const int first = start / 16, last = (start + count - 1) / 16;
-    const int ntiles = (last - first + 1) * H;
-    for (int k = blockIdx.y * 4 + wave; k < ntiles; k += gridDim.y * 4) {
-      const int pslot = first + k / H, h = k % H;
-      const int pid = a.page_ids[base + pslot];
-      if (pid < 0 || pid >= a.num_pool_pages) {
-        if (lane == 0 && a.error_flag) a.error_flag[0] = 1;
-        continue;
-      }
-      const int t0 = pslot * 16;
-      const int lo_t = max(start, t0), hi_t = min(start + count, t0 + 16);   // touched tokens
-      const int n = hi_t - lo_t;
-      const W* src = in + (a.in_token_offset[seq] + (lo_t - start)) * row + (int64_t)h * D;
-      W* dst = pool + ((int64_t)pid * H + h) * 16 * D;
-      if (n == 16 && !a.v_layout) {
-        u32x4_t v[NV];
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {
-          const int idx = lane + 64 * i, tok = idx / VPT, j = idx % VPT;
-          v[i] = *reinterpret_cast<const u32x4_t*>(src + tok * row + j * E);
-        }
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {
-          const int idx = lane + 64 * i, tok = idx / VPT, j = idx % VPT;
-          kst[j * KROW + tok] = v[i];
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {    // K: [D/E][16][E], vector idx = (j, t)
-          const int idx = lane + 64 * i;
-          *reinterpret_cast<u32x4_t*>(dst + idx * E) = kst[(idx / 16) * KROW + idx % 16];
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      } else if (n == 16) {
-        // Token fastest across lanes: one instruction's 16 lanes of a dim
-        // group fill the 16 slots of one staged row.
-        u32x4_t v[NV];
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {
-          const int idx = lane + 64 * i, tok = idx % 16, j = idx / 16;
-          v[i] = *reinterpret_cast<const u32x4_t*>(src + tok * row + j * E);
-        }
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {
-          const int idx = lane + 64 * i, tok = idx % 16, j = idx / 16;
-          const int slot = v_token_at_slot(tok);   // the permutation is its own inverse
-          const W* e = reinterpret_cast<const W*>(&v[i]);
-#pragma unroll
-          for (int q = 0; q < E; ++q) vst[((j * E + q) ^ (j & RMASK)) * 16 + slot] = e[q];
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-        for (int i = 0; i < NV; ++i) {    // V: [D][16], vector idx = (dim c, slot group)
-          const int idx = lane + 64 * i, c = idx / (16 / E), part = idx % (16 / E);
-          *reinterpret_cast<u32x4_t*>(dst + idx * E) =
-              *reinterpret_cast<const u32x4_t*>(vst + (c ^ ((c / E) & RMASK)) * 16 + part * E);
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      } else if (!a.v_layout) {
-        for (int idx = lane; idx < n * VPT; idx += 64) {
-          const int tok = idx / VPT, j = idx % VPT, t = lo_t - t0 + tok;
-          *reinterpret_cast<u32x4_t*>(dst + (j * 16 + t) * E) =
-              *reinterpret_cast<const u32x4_t*>(src + tok * row + j * E);
-        }
-      } else {
-        for (int idx = lane; idx < n * D; idx += 64) {
-          const int tok = idx / D, c = idx % D, t = lo_t - t0 + tok;
-          dst[c * 16 + v_token_at_slot(t)] = src[tok * row + c];
-        }
-      }
-    }
-  }
-}
-
-struct PageCopyArgs {
-  void* pool;
-  const int32_t* src_pages;
-  const int32_t* dst_pages;
-  int32_t* error_flag;
-  int64_t num_pool_pages;
-  int64_t page_vecs;   // 16-byte units of one page (all heads)
-  int32_t num_pages;
-};
-
-// Copy whole pages (every head) of one pool, 16 bytes per lane, grid-stride
-// over (page, unit). Pages with an id out of range are skipped and flagged.
-__global__ __launch_bounds__(256) void page_copy_kernel(PageCopyArgs a) {
-  const int64_t total = (int64_t)a.num_pages * a.page_vecs;
-  u32x4_t* pool = static_cast<u32x4_t*>(a.pool);
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t k = i / a.page_vecs, u = i - k * a.page_vecs;
-    const int src = a.src_pages[k], dst = a.dst_pages[k];
-    if (src < 0 || src >= a.num_pool_pages || dst < 0 || dst >= a.num_pool_pages) {
-      if (u == 0 && a.error_flag) a.error_flag[0] = 1;
-      continue;
-    }
-    pool[dst * a.page_vecs + u] = pool[src * a.page_vecs + u];
-  }
-}
-
 // ---------------------------------------------------------------- host side
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
@@ -1487,108 +1242,4 @@ extern "C" halo_status_t halo_prefix_attn_prefill(const halo_plan_t* plan, const
                                                   size_t workspace_bytes, void* stream) {
   return run_attention(plan, true, device_meta, q, k_pool, v_pool, o, lse, workspace, workspace_bytes,
                        stream);
-}
-
-extern "C" halo_status_t halo_kv_page_gather(const void* pool, const halo_attn_params_t* params,
-                                             halo_pool_kind_t pool_kind, const int32_t* page_ids,
-                                             const int32_t* seq_page_indptr, const int32_t* seq_len,
-                                             const int64_t* out_token_offset, int32_t num_seqs, void* out,
-                                             int32_t* error_flag, void* stream) {
-  clear_error();
-  if (!params) return fail(HALO_ERR_INVALID_ARGUMENT, "params must not be NULL");
-  if (num_seqs < 0) return fail(HALO_ERR_INVALID_ARGUMENT, "num_seqs must be >= 0");
-  if (num_seqs == 0) return HALO_OK;
-  if (!pool || !page_ids || !seq_page_indptr || !seq_len || !out_token_offset || !out)
-    return fail(HALO_ERR_INVALID_ARGUMENT, "pool, page_ids, seq_page_indptr, seq_len, out_token_offset, out "
-                                           "must not be NULL");
-  if (params->head_dim != 64 && params->head_dim != 128)
-    return fail(HALO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
-  if (params->page_size != 16) return fail(HALO_ERR_UNSUPPORTED, "page_size must be 16");
-  if (params->num_kv_heads < 1) return fail(HALO_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
-  if (pool_kind != HALO_POOL_K && pool_kind != HALO_POOL_V)
-    return fail(HALO_ERR_INVALID_ARGUMENT, "pool_kind must be HALO_POOL_K or HALO_POOL_V");
-  GatherArgs g{pool, page_ids, seq_page_indptr, seq_len, out_token_offset, out, error_flag,
-               params->num_pool_pages, num_seqs, params->num_kv_heads, params->head_dim,
-               pool_kind == HALO_POOL_V ? 1 : 0};
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();
-  const int blocks = 2048;
-  if (params->kv_dtype == HALO_BF16)
-    hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st, g);
-  else if (params->kv_dtype == HALO_F32)
-    hipLaunchKernelGGL(gather_kernel<uint32_t>, dim3(blocks), dim3(256), 0, st, g);
-  else
-    return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
-  return hip_check("gather launch");
-}
-
-extern "C" halo_status_t halo_kv_page_scatter(void* pool, const halo_attn_params_t* params,
-                                              halo_pool_kind_t pool_kind, const int32_t* page_ids,
-                                              const int32_t* seq_page_indptr, const int32_t* seq_start,
-                                              const int32_t* seq_count, const int64_t* in_token_offset,
-                                              int32_t num_seqs, const void* in, int32_t* error_flag,
-                                              void* stream) {
-  clear_error();
-  if (!params) return fail(HALO_ERR_INVALID_ARGUMENT, "params must not be NULL");
-  if (num_seqs < 0) return fail(HALO_ERR_INVALID_ARGUMENT, "num_seqs must be >= 0");
-  if (num_seqs == 0) return HALO_OK;
-  if (!pool || !page_ids || !seq_page_indptr || !seq_start || !seq_count || !in_token_offset || !in)
-    return fail(HALO_ERR_INVALID_ARGUMENT, "pool, page_ids, seq_page_indptr, seq_start, seq_count, "
-                                           "in_token_offset, in must not be NULL");
-  if (params->head_dim != 64 && params->head_dim != 128)
-    return fail(HALO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
-  if (params->page_size != 16) return fail(HALO_ERR_UNSUPPORTED, "page_size must be 16");
-  if (params->num_kv_heads < 1) return fail(HALO_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
-  if (pool_kind != HALO_POOL_K && pool_kind != HALO_POOL_V)
-    return fail(HALO_ERR_INVALID_ARGUMENT, "pool_kind must be HALO_POOL_K or HALO_POOL_V");
-  if (!aligned16(pool) || !aligned16(in))
-    return fail(HALO_ERR_INVALID_ARGUMENT, "pool and in must be 16-byte aligned");
-  ScatterArgs g{pool, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset, in, error_flag,
-                params->num_pool_pages, num_seqs, params->num_kv_heads, params->head_dim,
-                pool_kind == HALO_POOL_V ? 1 : 0};
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();
-  // One x-block per sequence (grid-stride past 65536), enough y-blocks per
-  // sequence that a call fills the chip with about 2048 workgroups.
-  const int bx = std::min(num_seqs, 65536);
-  const dim3 grid(bx, std::min(std::max(2048 / bx, 1), 2048));
-  const bool d128 = params->head_dim == 128;
-  if (params->kv_dtype == HALO_BF16) {
-    if (d128) hipLaunchKernelGGL((scatter_kernel<uint16_t, 128>), grid, dim3(256), 0, st, g);
-    else hipLaunchKernelGGL((scatter_kernel<uint16_t, 64>), grid, dim3(256), 0, st, g);
-  } else if (params->kv_dtype == HALO_F32) {
-    if (d128) hipLaunchKernelGGL((scatter_kernel<uint32_t, 128>), grid, dim3(256), 0, st, g);
-    else hipLaunchKernelGGL((scatter_kernel<uint32_t, 64>), grid, dim3(256), 0, st, g);
-  } else {
-    return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
-  }
-  return hip_check("scatter launch");
-}
-
-extern "C" halo_status_t halo_kv_page_copy(void* pool, const halo_attn_params_t* params,
-                                           const int32_t* src_pages, const int32_t* dst_pages,
-                                           int32_t num_pages, int32_t* error_flag, void* stream) {
-  clear_error();
-  if (!params) return fail(HALO_ERR_INVALID_ARGUMENT, "params must not be NULL");
-  if (num_pages < 0) return fail(HALO_ERR_INVALID_ARGUMENT, "num_pages must be >= 0");
-  if (num_pages == 0) return HALO_OK;
-  if (!pool || !src_pages || !dst_pages)
-    return fail(HALO_ERR_INVALID_ARGUMENT, "pool, src_pages, dst_pages must not be NULL");
-  if (params->head_dim != 64 && params->head_dim != 128)
-    return fail(HALO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
-  if (params->page_size != 16) return fail(HALO_ERR_UNSUPPORTED, "page_size must be 16");
-  if (params->num_kv_heads < 1) return fail(HALO_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
-  int elt;
-  if (params->kv_dtype == HALO_BF16) elt = 2;
-  else if (params->kv_dtype == HALO_F32) elt = 4;
-  else return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
-  if (!aligned16(pool)) return fail(HALO_ERR_INVALID_ARGUMENT, "pool must be 16-byte aligned");
-  const int64_t page_bytes = (int64_t)params->num_kv_heads * 16 * params->head_dim * elt;
-  PageCopyArgs g{pool, src_pages, dst_pages, error_flag, params->num_pool_pages, page_bytes / 16, num_pages};
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();
-  const int64_t want = ((int64_t)num_pages * g.page_vecs + 255) / 256;
-  const int blocks = (int)std::min<int64_t>(std::max<int64_t>(want, 1), 4096);
-  hipLaunchKernelGGL(page_copy_kernel, dim3(blocks), dim3(256), 0, st, g);
-  return hip_check("page copy launch");
 }
