@@ -124,7 +124,8 @@ def write_path_bench(args):
 
     Scatter: every request's last segment (its private suffix, or its prefill
     chunk) is the target; decode appends the segment's last token (start =
-    length - 1, count 1), prefill writes the whole chunk. Copy: one page per
+    length - 1, count 1), prefill writes the whole chunk; timed per pool and
+    for both pools in one call. Copy: one page per
     request, the first page of its last segment, to a distinct free page of
     the pool (the copy of copy-on-write; distinct sources, so that no copy
     reads another's source out of cache). Algorithmic bytes: the
@@ -175,6 +176,8 @@ def write_path_bench(args):
     for name, pool, kind in (("k", w.k_pool, halo.HALO_POOL_K), ("v", w.v_pool, halo.HALO_POOL_V)):
         call = halo.bind_kv_page_scatter(pool, params, kind, *sc_args[:5], src, flag, stream)
         res["scatter_" + name + "_us"] = _time_launches(call, args.steps, args.warmup, stream)
+    call = halo.bind_kv_page_scatter_kv(w.k_pool, w.v_pool, params, *sc_args[:5], src, src, flag, stream)
+    res["scatter_kv_us"] = _time_launches(call, args.steps, args.warmup, stream)
     call = halo.bind_kv_page_copy(w.k_pool, params, cp_src, cp_dst, flag, stream)
     res["copy_us"] = _time_launches(call, args.steps, args.warmup, stream)
     torch.cuda.synchronize()
@@ -194,6 +197,9 @@ def write_path_bench(args):
         us = res["scatter_" + name + "_us"]
         line["scatter_" + name] = {"us": round(us, 2), "gbps": gbps(sc_bytes, us),
                                    "frac": round(gbps(sc_bytes, us) / HBM_PEAK_GBPS, 4)}
+    us = res["scatter_kv_us"]
+    line["scatter_kv_one_call"] = {"us": round(us, 2), "gbps": gbps(2 * sc_bytes, us),
+                                   "frac": round(gbps(2 * sc_bytes, us) / HBM_PEAK_GBPS, 4)}
     line["copy"] = {"us": round(res["copy_us"], 2), "gbps": gbps(cp_bytes, res["copy_us"]),
                     "frac": round(gbps(cp_bytes, res["copy_us"]) / HBM_PEAK_GBPS, 4)}
     print(json.dumps(line), flush=True)

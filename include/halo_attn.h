@@ -196,6 +196,20 @@ halo_status_t halo_kv_page_scatter(void* pool, const halo_attn_params_t* params,
                                    const int64_t* in_token_offset, int32_t num_seqs,
                                    const void* in, int32_t* error_flag, void* stream);
 
+/* halo_kv_page_scatter for the K and the V pool of the same tokens in one
+ * launch: k_in goes to k_pool (HALO_POOL_K layout), v_in to v_pool
+ * (HALO_POOL_V layout), with one set of page lists, ranges and input offsets.
+ * The result equals the two single-pool calls; the error rules are theirs
+ * (a flagged sequence or page is skipped in both pools). For a decode step,
+ * whose per-pool work is a few KB, one launch instead of two halves the fixed
+ * cost of the append. */
+halo_status_t halo_kv_page_scatter_kv(void* k_pool, void* v_pool, const halo_attn_params_t* params,
+                                      const int32_t* page_ids, const int32_t* seq_page_indptr,
+                                      const int32_t* seq_start, const int32_t* seq_count,
+                                      const int64_t* in_token_offset, int32_t num_seqs,
+                                      const void* k_in, const void* v_in, int32_t* error_flag,
+                                      void* stream);
+
 /* Whole-page copy inside one pool, every head, bit for bit: page dst_pages[k]
  * becomes a copy of page src_pages[k], k < num_pages. This is the copy of
  * copy-on-write: before a request writes into a page it shares with others

@@ -96,20 +96,22 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
 
 // ---------------------------------------------------------------- write path
 
+// Up to two (pool, input) pairs written by one launch, pair blockIdx.z: the
+// K and V pools of one append share the page lists and the launch.
 struct ScatterArgs {
-  void* pool;
+  void* pool[2];
+  const void* in[2];
+  int32_t v_layout[2];
   const int32_t* page_ids;
   const int32_t* seq_page_indptr;
   const int32_t* seq_start;
   const int32_t* seq_count;
   const int64_t* in_token_offset;
-  const void* in;
   int32_t* error_flag;
   int64_t num_pool_pages;
   int32_t num_seqs;
   int32_t num_kv_heads;
   int32_t head_dim;
-  int32_t v_layout;
 };
 
 // The inverse of the gather: tokens start .. start + count - 1 of each
@@ -143,8 +145,9 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int H = a.num_kv_heads;
   const int64_t row = (int64_t)H * D;      // input elements per token
-  W* pool = static_cast<W*>(a.pool);
-  const W* in = static_cast<const W*>(a.in);
+  W* pool = static_cast<W*>(a.pool[blockIdx.z]);
+  const W* in = static_cast<const W*>(a.in[blockIdx.z]);
+  const bool v_layout = a.v_layout[blockIdx.z] != 0;
   u32x4_t* kst = stage[wave];
   W* vst = reinterpret_cast<W*>(stage[wave]);
   for (int seq = blockIdx.x; seq < a.num_seqs; seq += gridDim.x) {
@@ -153,7 +156,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
     const int base = a.seq_page_indptr[seq];
     const int npages = a.seq_page_indptr[seq + 1] - base;
     if (start < 0 || (int64_t)start + count > (int64_t)npages * 16) {
-      if (blockIdx.y == 0 && threadIdx.x == 0 && a.error_flag) a.error_flag[0] = 1;
+      if (blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0 && a.error_flag) a.error_flag[0] = 1;
       continue;
     }
     const int first = start / 16, last = (start + count - 1) / 16;
@@ -170,7 +173,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
       const int n = hi_t - lo_t;
       const W* src = in + (a.in_token_offset[seq] + (lo_t - start)) * row + (int64_t)h * D;
       W* dst = pool + ((int64_t)pid * H + h) * 16 * D;
-      if (n == 16 && !a.v_layout) {
+      if (n == 16 && !v_layout) {
         u32x4_t v[NV];
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
@@ -222,7 +225,7 @@ __global__ __launch_bounds__(256) void scatter_kernel(ScatterArgs a) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      } else if (!a.v_layout) {
+      } else if (!v_layout) {
         for (int idx = lane; idx < n * VPT; idx += 64) {
           const int tok = idx / VPT, j = idx % VPT, t = lo_t - t0 + tok;
           *reinterpret_cast<u32x4_t*>(dst + (j * 16 + t) * E) =
@@ -309,6 +312,41 @@ extern "C" halo_status_t halo_kv_page_gather(const void* pool, const halo_attn_p
   return hip_check("gather launch");
 }
 
+namespace {
+
+// Shared checks and launch of the scatter entry points (n_pairs = 1 or 2).
+halo_status_t launch_scatter(const halo_attn_params_t* params, ScatterArgs g, int n_pairs, void* stream) {
+  if (params->head_dim != 64 && params->head_dim != 128)
+    return fail(HALO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (params->page_size != 16) return fail(HALO_ERR_UNSUPPORTED, "page_size must be 16");
+  if (params->num_kv_heads < 1) return fail(HALO_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
+  if (params->kv_dtype != HALO_BF16 && params->kv_dtype != HALO_F32)
+    return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
+  for (int z = 0; z < n_pairs; ++z)
+    if (!aligned16(g.pool[z]) || !aligned16(g.in[z]))
+      return fail(HALO_ERR_INVALID_ARGUMENT, "pools and inputs must be 16-byte aligned");
+  g.num_pool_pages = params->num_pool_pages;
+  g.num_kv_heads = params->num_kv_heads;
+  g.head_dim = params->head_dim;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  // One x-block per sequence (grid-stride past 65536), enough y-blocks per
+  // sequence that a call fills the chip with about 2048 workgroups.
+  const int bx = std::min(g.num_seqs, 65536);
+  const dim3 grid(bx, std::min(std::max(2048 / (bx * n_pairs), 1), 2048), n_pairs);
+  const bool d128 = params->head_dim == 128;
+  if (params->kv_dtype == HALO_BF16) {
+    if (d128) hipLaunchKernelGGL((scatter_kernel<uint16_t, 128>), grid, dim3(256), 0, st, g);
+    else hipLaunchKernelGGL((scatter_kernel<uint16_t, 64>), grid, dim3(256), 0, st, g);
+  } else {
+    if (d128) hipLaunchKernelGGL((scatter_kernel<uint32_t, 128>), grid, dim3(256), 0, st, g);
+    else hipLaunchKernelGGL((scatter_kernel<uint32_t, 64>), grid, dim3(256), 0, st, g);
+  }
+  return hip_check("scatter launch");
+}
+
+}  // namespace
+
 extern "C" halo_status_t halo_kv_page_scatter(void* pool, const halo_attn_params_t* params,
                                               halo_pool_kind_t pool_kind, const int32_t* page_ids,
                                               const int32_t* seq_page_indptr, const int32_t* seq_start,
@@ -322,34 +360,51 @@ extern "C" halo_status_t halo_kv_page_scatter(void* pool, const halo_attn_params
   if (!pool || !page_ids || !seq_page_indptr || !seq_start || !seq_count || !in_token_offset || !in)
     return fail(HALO_ERR_INVALID_ARGUMENT, "pool, page_ids, seq_page_indptr, seq_start, seq_count, "
                                            "in_token_offset, in must not be NULL");
-  if (params->head_dim != 64 && params->head_dim != 128)
-    return fail(HALO_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
-  if (params->page_size != 16) return fail(HALO_ERR_UNSUPPORTED, "page_size must be 16");
-  if (params->num_kv_heads < 1) return fail(HALO_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
   if (pool_kind != HALO_POOL_K && pool_kind != HALO_POOL_V)
     return fail(HALO_ERR_INVALID_ARGUMENT, "pool_kind must be HALO_POOL_K or HALO_POOL_V");
-  if (!aligned16(pool) || !aligned16(in))
-    return fail(HALO_ERR_INVALID_ARGUMENT, "pool and in must be 16-byte aligned");
-  ScatterArgs g{pool, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset, in, error_flag,
-                params->num_pool_pages, num_seqs, params->num_kv_heads, params->head_dim,
-                pool_kind == HALO_POOL_V ? 1 : 0};
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();
-  // One x-block per sequence (grid-stride past 65536), enough y-blocks per
-  // sequence that a call fills the chip with about 2048 workgroups.
-  const int bx = std::min(num_seqs, 65536);
-  const dim3 grid(bx, std::min(std::max(2048 / bx, 1), 2048));
-  const bool d128 = params->head_dim == 128;
-  if (params->kv_dtype == HALO_BF16) {
-    if (d128) hipLaunchKernelGGL((scatter_kernel<uint16_t, 128>), grid, dim3(256), 0, st, g);
-    else hipLaunchKernelGGL((scatter_kernel<uint16_t, 64>), grid, dim3(256), 0, st, g);
-  } else if (params->kv_dtype == HALO_F32) {
-    if (d128) hipLaunchKernelGGL((scatter_kernel<uint32_t, 128>), grid, dim3(256), 0, st, g);
-    else hipLaunchKernelGGL((scatter_kernel<uint32_t, 64>), grid, dim3(256), 0, st, g);
-  } else {
-    return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
-  }
-  return hip_check("scatter launch");
+  ScatterArgs g{};
+  g.pool[0] = pool;
+  g.in[0] = in;
+  g.v_layout[0] = pool_kind == HALO_POOL_V ? 1 : 0;
+  g.page_ids = page_ids;
+  g.seq_page_indptr = seq_page_indptr;
+  g.seq_start = seq_start;
+  g.seq_count = seq_count;
+  g.in_token_offset = in_token_offset;
+  g.error_flag = error_flag;
+  g.num_seqs = num_seqs;
+  return launch_scatter(params, g, 1, stream);
+}
+
+extern "C" halo_status_t halo_kv_page_scatter_kv(void* k_pool, void* v_pool, const halo_attn_params_t* params,
+                                                 const int32_t* page_ids, const int32_t* seq_page_indptr,
+                                                 const int32_t* seq_start, const int32_t* seq_count,
+                                                 const int64_t* in_token_offset, int32_t num_seqs,
+                                                 const void* k_in, const void* v_in, int32_t* error_flag,
+                                                 void* stream) {
+  clear_error();
+  if (!params) return fail(HALO_ERR_INVALID_ARGUMENT, "params must not be NULL");
+  if (num_seqs < 0) return fail(HALO_ERR_INVALID_ARGUMENT, "num_seqs must be >= 0");
+  if (num_seqs == 0) return HALO_OK;
+  if (!k_pool || !v_pool || !page_ids || !seq_page_indptr || !seq_start || !seq_count || !in_token_offset ||
+      !k_in || !v_in)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "k_pool, v_pool, page_ids, seq_page_indptr, seq_start, seq_count, "
+                                           "in_token_offset, k_in, v_in must not be NULL");
+  ScatterArgs g{};
+  g.pool[0] = k_pool;
+  g.pool[1] = v_pool;
+  g.in[0] = k_in;
+  g.in[1] = v_in;
+  g.v_layout[0] = 0;
+  g.v_layout[1] = 1;
+  g.page_ids = page_ids;
+  g.seq_page_indptr = seq_page_indptr;
+  g.seq_start = seq_start;
+  g.seq_count = seq_count;
+  g.in_token_offset = in_token_offset;
+  g.error_flag = error_flag;
+  g.num_seqs = num_seqs;
+  return launch_scatter(params, g, 2, stream);
 }
 
 extern "C" halo_status_t halo_kv_page_copy(void* pool, const halo_attn_params_t* params,

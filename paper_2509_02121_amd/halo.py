@@ -61,7 +61,7 @@ EXPORTED_SYMBOLS = (
     "halo_plan_create", "halo_plan_upload", "halo_plan_destroy", "halo_plan_get_stats",
     "halo_plan_inspect",
     "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_kv_page_gather",
-    "halo_kv_page_scatter", "halo_kv_page_copy",
+    "halo_kv_page_scatter", "halo_kv_page_scatter_kv", "halo_kv_page_copy",
     "halo_status_string", "halo_last_error_message",
 )
 
@@ -127,6 +127,9 @@ def load_library(require_gpu=False):
     lib.halo_kv_page_scatter.argtypes = [vp, ctypes.POINTER(AttnParams), ctypes.c_int, vp, vp, vp, vp, vp,
                                          ctypes.c_int32, vp, vp, vp]
     lib.halo_kv_page_scatter.restype = ctypes.c_int
+    lib.halo_kv_page_scatter_kv.argtypes = [vp, vp, ctypes.POINTER(AttnParams), vp, vp, vp, vp, vp,
+                                            ctypes.c_int32, vp, vp, vp, vp]
+    lib.halo_kv_page_scatter_kv.restype = ctypes.c_int
     lib.halo_kv_page_copy.argtypes = [vp, ctypes.POINTER(AttnParams), vp, vp, ctypes.c_int32, vp, vp]
     lib.halo_kv_page_copy.restype = ctypes.c_int
     lib.halo_status_string.argtypes = [ctypes.c_int]
@@ -291,6 +294,23 @@ def kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq_star
                                      _stream_handle(stream)))
 
 
+def _scatter_kv_args(k_pool, v_pool, params, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset,
+                     k_src, v_src, error_flag, stream):
+    return (k_pool.data_ptr(), v_pool.data_ptr(), ctypes.byref(params), page_ids.data_ptr(),
+            seq_page_indptr.data_ptr(), seq_start.data_ptr(), seq_count.data_ptr(), in_token_offset.data_ptr(),
+            int(seq_page_indptr.numel() - 1), k_src.data_ptr(), v_src.data_ptr(),
+            error_flag.data_ptr() if error_flag is not None else None, _stream_handle(stream))
+
+
+def kv_page_scatter_kv(k_pool, v_pool, params, page_ids, seq_page_indptr, seq_start, seq_count,
+                       in_token_offset, k_src, v_src, error_flag=None, stream=None):
+    """halo_kv_page_scatter_kv (both pools, one launch) on torch tensors."""
+    load_library()
+    _check(_LIB.halo_kv_page_scatter_kv(*_scatter_kv_args(k_pool, v_pool, params, page_ids, seq_page_indptr,
+                                                          seq_start, seq_count, in_token_offset, k_src, v_src,
+                                                          error_flag, stream)))
+
+
 def kv_page_copy(pool, params, src_pages, dst_pages, error_flag=None, stream=None):
     """halo_kv_page_copy on torch tensors (int arrays on the GPU)."""
     load_library()
@@ -311,6 +331,21 @@ def bind_kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq
             in_token_offset.data_ptr(), int(seq_page_indptr.numel() - 1), src.data_ptr(),
             error_flag.data_ptr() if error_flag is not None else None, _stream_handle(stream))
     fn = _LIB.halo_kv_page_scatter
+
+    def call():
+        st = fn(*args)
+        if st != HALO_OK:
+            _check(st)
+    return call
+
+
+def bind_kv_page_scatter_kv(k_pool, v_pool, params, page_ids, seq_page_indptr, seq_start, seq_count,
+                            in_token_offset, k_src, v_src, error_flag=None, stream=None):
+    """kv_page_scatter_kv as a zero-argument callable (see bind_kv_page_scatter)."""
+    load_library()
+    args = _scatter_kv_args(k_pool, v_pool, params, page_ids, seq_page_indptr, seq_start, seq_count,
+                            in_token_offset, k_src, v_src, error_flag, stream)
+    fn = _LIB.halo_kv_page_scatter_kv
 
     def call():
         st = fn(*args)

@@ -333,6 +333,18 @@ def test_run_calls_reject_bad_arguments_without_touching_the_gpu(lib):
     rc = lib.halo_kv_page_scatter(fake, ctypes.byref(params), 0, fake, fake, fake, fake, fake, 1, fake + 2, None,
                                   None)
     assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # input not 16-byte aligned
+    rc = lib.halo_kv_page_scatter_kv(fake, fake, ctypes.byref(params), fake, fake, fake, fake, fake, 1, fake,
+                                     None, None, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # v_in NULL
+    rc = lib.halo_kv_page_scatter_kv(fake, fake + 8, ctypes.byref(params), fake, fake, fake, fake, fake, 1, fake,
+                                     fake, None, None)
+    assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # v_pool not 16-byte aligned
+    rc = lib.halo_kv_page_scatter_kv(fake, fake, ctypes.byref(p2), fake, fake, fake, fake, fake, 1, fake, fake,
+                                     None, None)
+    assert rc == halo.HALO_ERR_UNSUPPORTED
+    rc = lib.halo_kv_page_scatter_kv(None, None, ctypes.byref(params), None, None, None, None, None, 0, None,
+                                     None, None, None)
+    assert rc == halo.HALO_OK      # nothing to do
     rc = lib.halo_kv_page_copy(fake + 4, ctypes.byref(params), fake, fake, 1, None, None)
     assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # pool not 16-byte aligned
     rc = lib.halo_kv_page_copy(fake, ctypes.byref(p2), fake, fake, 1, None, None)

@@ -109,6 +109,39 @@ def test_scatter_bit_exact(gpu_lib, dtype, D, kind):
     assert np.array_equal(got, exp)
 
 
+@pytest.mark.parametrize("dtype,D", [(torch.bfloat16, 128), (torch.float32, 64)])
+def test_scatter_kv_equals_two_single_pool_calls(gpu_lib, dtype, D):
+    """The two-pool call writes exactly what the two single-pool calls write,
+    also with a flagged sequence among the good ones."""
+    print(f"case: scatter_kv {dtype} d{D}", flush=True)
+    rng = np.random.default_rng(21 + D)
+    H, n_pool = 3, 64
+    ity = _int_type(dtype)
+    seqs, spare = _random_seqs(rng, n_pool, 12, 4)
+    seqs.append((spare[:1], 9, 8))                       # 9 + 8 > 16: flagged, skipped
+    total = sum(c for _, _, c in seqs)
+    dev = "cuda"
+    pools = [_random_bits((n_pool * H * PAGE * D,), ity, rng).to(dev).view(dtype) for _ in range(2)]
+    ins = [_random_bits((total, H, D), ity, rng).to(dev).view(dtype) for _ in range(2)]
+    indptr = np.zeros(len(seqs) + 1, np.int32)
+    indptr[1:] = np.cumsum([len(p) for p, _, _ in seqs])
+    offs = np.concatenate([[0], np.cumsum([c for _, _, c in seqs])[:-1]]).astype(np.int64)
+    lists = (torch.as_tensor(np.concatenate([p for p, _, _ in seqs]), device=dev), torch.as_tensor(indptr, device=dev),
+             torch.as_tensor(np.array([st for _, st, _ in seqs], np.int32), device=dev),
+             torch.as_tensor(np.array([c for _, _, c in seqs], np.int32), device=dev),
+             torch.as_tensor(offs, device=dev))
+    params = halo.make_params(H, H, D, dtype, n_pool, 0.125, dtype)
+    single = [p.clone() for p in pools]
+    flags = torch.zeros(2, dtype=torch.int32, device=dev)
+    halo.kv_page_scatter(single[0], params, halo.HALO_POOL_K, *lists, ins[0], flags[0:1])
+    halo.kv_page_scatter(single[1], params, halo.HALO_POOL_V, *lists, ins[1], flags[0:1])
+    halo.kv_page_scatter_kv(pools[0], pools[1], params, *lists, ins[0], ins[1], flags[1:2])
+    torch.cuda.synchronize()
+    assert flags.tolist() == [1, 1]
+    for a, b in zip(pools, single):
+        assert torch.equal(a.view(ity), b.view(ity))
+
+
 def test_scatter_then_gather_round_trip(gpu_lib):
     """Decode-style appends (one token per sequence at its current length),
     read back with the gather: the appended token is the input, earlier
@@ -217,8 +250,7 @@ def test_decode_append_then_attention_matches_oracle(gpu_lib):
         halo.kv_page_scatter(pool, params, kind, *args, nan)      # the token is not there yet
     torch.cuda.synchronize()
     assert not torch.isfinite(w.segment_kv(last[0])[0][-1]).all()
-    for kind, pool, new in ((halo.HALO_POOL_K, w.k_pool, k_new), (halo.HALO_POOL_V, w.v_pool, v_new)):
-        halo.kv_page_scatter(pool, params, kind, *args, new)      # the decode step writes it
+    halo.kv_page_scatter_kv(w.k_pool, w.v_pool, params, *args, k_new, v_new)   # the decode step writes it
     o, lse, _ = run_library(w)
     o_ref, lse_ref, rows = oracle_for(w)
     assert torch.equal(w.segment_kv(last[0])[0][-1].view(torch.int16).cpu(), k_new[0].view(torch.int16).cpu())
