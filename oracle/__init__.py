@@ -22,6 +22,9 @@ What it follows (arXiv 2509.02121, "Halo"):
 The paper never writes out the attention formula; it is the textbook scaled
 dot-product attention, softmax(scale * q k^T) v, with grouped heads (q head h
 reads kv head h // (H_q / H_kv)).
+
+``paged_kv`` holds the reference of the paged-KV write path (token scatter
+into the pool layouts, page copy for copy-on-write).
 """
 
 from .attention import (  # noqa: F401
@@ -32,3 +35,4 @@ from .attention import (  # noqa: F401
     gather_tokens,
     merge_partials,
 )
+from . import paged_kv  # noqa: F401,E402

@@ -1,8 +1,8 @@
-"""GPU bit-exactness of the paged-KV write path: halo_kv_page_scatter (new
-tokens into their pages, §7 PagedAttention; §2 KV written once and reused)
-and halo_kv_page_copy (the copy of copy-on-write). The reference is numpy
-scatter into the pool layouts the header defines; nothing of the library's
-code is shared."""
+"""GPU bit-exactness of the paged-KV write path: halo_kv_page_scatter and
+halo_kv_page_scatter_kv (new tokens into their pages, §7 PagedAttention; §2
+KV written once and reused) and halo_kv_page_copy (the copy of
+copy-on-write), against the oracle's element-by-element scatter and page
+copy (oracle.paged_kv)."""
 
 import numpy as np
 import pytest
@@ -12,20 +12,10 @@ import oracle
 from gpu_helpers import assert_parity, oracle_for, params_of, run_library, to_device
 from paper_2509_02121_amd import halo
 from workloads import build_workload, make_config
-from workloads.synth import V_SLOT_OF_TOKEN
 
 pytestmark = pytest.mark.gpu
 
 PAGE = 16
-
-
-def _elem_index(kind, H, D, E, page, h, t, c):
-    """Flat pool index of (page, head h, token slot t, dim c), from the layouts
-    of the header: K [P][H][D/E][16][E], V [P][H][D][16] with permuted slots."""
-    base = (page * H + h) * PAGE * D
-    if kind == halo.HALO_POOL_K:
-        return base + ((c // E) * PAGE + t) * E + c % E
-    return base + c * PAGE + int(V_SLOT_OF_TOKEN[t])
 
 
 def _random_bits(shape, ity, rng):
@@ -40,30 +30,17 @@ def _int_type(dtype):
 
 def _scatter(dtype, D, H, n_pool, seqs, kind, rng, flag=None):
     """Scatter random-bit tokens into a random-bit pool on the GPU; returns
-    (pool bits after, expected bits, pool bits before). seqs: list of
-    (page ids, start, count). The expectation follows the header's rules: a
-    sequence whose range passes its page list is skipped whole, a page id
-    out of range skips that page's tokens."""
+    (pool bits after, expected bits from the oracle, pool bits before).
+    seqs: list of (page ids, start, count)."""
     ity = _int_type(dtype)
     E = 16 // (2 if dtype == torch.bfloat16 else 4)
     total = sum(c for _, _, c in seqs)
     pool_bits = _random_bits((n_pool * H * PAGE * D,), ity, rng)
     in_bits = _random_bits((max(total, 1), H, D), ity, rng)
-    exp = pool_bits.clone().numpy()
-    offs = np.zeros(len(seqs), np.int64)
-    acc = 0
-    for i, (pages, start, count) in enumerate(seqs):
-        offs[i] = acc
-        if start >= 0 and start + count <= len(pages) * PAGE:
-            for t in range(count):
-                p = start + t
-                page = int(pages[p // PAGE])
-                if not 0 <= page < n_pool:
-                    continue
-                for h in range(H):
-                    for c in range(D):
-                        exp[_elem_index(kind, H, D, E, page, h, p % PAGE, c)] = in_bits[acc + t, h, c]
-        acc += count
+    offs = np.concatenate([[0], np.cumsum([c for _, _, c in seqs])[:-1]]).astype(np.int64)
+    exp, exp_flag = oracle.paged_kv.scatter(pool_bits.numpy(), kind, H, D, E, n_pool, [p for p, _, _ in seqs],
+                                            [st for _, st, _ in seqs], [c for _, _, c in seqs], offs,
+                                            in_bits.numpy())
     dev = "cuda"
     pool = pool_bits.to(dev).view(dtype)
     src = in_bits.to(dev).view(dtype)
@@ -77,6 +54,8 @@ def _scatter(dtype, D, H, n_pool, seqs, kind, rng, flag=None):
                          torch.as_tensor(np.array([c for _, _, c in seqs], np.int32), device=dev),
                          torch.as_tensor(offs, device=dev), src, flag)
     torch.cuda.synchronize()
+    if flag is not None:
+        assert int(flag.item()) == int(exp_flag)
     return pool.view(ity).cpu().numpy(), exp, pool_bits.numpy()
 
 
@@ -190,8 +169,8 @@ def test_page_copy_bit_exact(gpu_lib, dtype, D):
     bits = _random_bits((n_pool * H * PAGE * D,), ity, rng)
     perm = rng.permutation(n_pool)
     src, dst = perm[:9].astype(np.int32), perm[9:18].astype(np.int32)
-    exp = bits.clone().numpy().reshape(n_pool, -1)
-    exp[dst] = exp[src]
+    exp, _ = oracle.paged_kv.page_copy(bits.numpy(), H * PAGE * D, n_pool, src, dst)
+    exp = exp.reshape(n_pool, -1)
     pool = bits.to("cuda").view(dtype)
     halo.kv_page_copy(pool, halo.make_params(H, H, D, dtype, n_pool, 0.125, dtype),
                       torch.as_tensor(src, device="cuda"), torch.as_tensor(dst, device="cuda"))

@@ -428,3 +428,77 @@ def test_gather_expected_is_concatenation():
     out = oracle.gather_tokens(segs, [2, 0, 1])
     assert out.shape == (8, 2, 4)
     assert np.array_equal(out[:5], segs[2]) and np.array_equal(out[5:], segs[0])
+
+
+# ---------------------------------------------------------------- paged KV write path
+
+PAGED_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paged_kv_layout.json")
+
+
+def test_paged_kv_golden_offsets():
+    """Hand-worked element offsets of both pool layouts."""
+    with open(PAGED_GOLDEN) as f:
+        cases = json.load(f)["cases"]
+    for cs in cases:
+        kind = oracle.paged_kv.POOL_K if cs["kind"] == "K" else oracle.paged_kv.POOL_V
+        got = oracle.paged_kv.elem_offset(kind, cs["H"], cs["D"], cs["E"], cs["page"], cs["h"], cs["t"], cs["c"])
+        assert got == cs["offset"], cs
+
+
+def test_paged_kv_slot_map_is_the_stated_permutation():
+    assert [oracle.paged_kv.v_slot(t) for t in range(16)] == [0, 1, 2, 3, 8, 9, 10, 11, 4, 5, 6, 7, 12, 13, 14, 15]
+
+
+@pytest.mark.parametrize("dtype,D", [(torch.bfloat16, 128), (torch.float32, 64)])
+def test_paged_kv_scatter_agrees_with_generator_readback(dtype, D):
+    """Write every segment's tokens with the oracle scatter, then read them
+    back with the input generator's tensor read-back (reshape and permute of
+    the pool, an independent statement of the same layouts): the logical
+    tokens come back. A transposed unit, a wrong slot order or a wrong tile
+    base fails this."""
+    w = build_workload("wr", 9, 4, 2, D, dtype, [37, 16, 5, 50], [[0, 1], [0, 2], [3]], poison=False)
+    ity = torch.int16 if dtype == torch.bfloat16 else torch.int32
+    E = 16 // torch.empty(0, dtype=dtype).element_size()
+    rng = np.random.default_rng(1)
+    info = np.iinfo(np.int16 if ity == torch.int16 else np.int32)
+    logical = {s: {kind: rng.integers(info.min, info.max, size=(int(w.seg_len[s]), 2, D), endpoint=True)
+                   for kind in (0, 1)} for s in range(4)}
+    for kind, pool in ((0, w.k_pool), (1, w.v_pool)):
+        flat = pool.view(ity).numpy().ravel()
+        segs = range(4)
+        src = np.concatenate([logical[s][kind] for s in segs]).astype(flat.dtype)
+        offs = np.concatenate([[0], np.cumsum([int(w.seg_len[s]) for s in segs])[:-1]])
+        out, flagged = oracle.paged_kv.scatter(flat, kind, 2, D, E, w.num_pool_pages,
+                                               [w.seg_pages[s] for s in segs], [0] * 4,
+                                               [int(w.seg_len[s]) for s in segs], offs, src)
+        assert not flagged
+        pool.view(ity).copy_(torch.as_tensor(out).view(pool.shape))
+    for s in range(4):
+        k, v = w.segment_kv(s)
+        assert np.array_equal(k.view(ity).numpy(), logical[s][0])
+        assert np.array_equal(v.view(ity).numpy(), logical[s][1])
+
+
+def test_paged_kv_scatter_rules():
+    """Only the written slots change; a range past the page list skips the
+    whole sequence, a bad page id skips its page; both are flagged."""
+    H, D, E, n_pool = 1, 8, 4, 6
+    pool = np.arange(n_pool * H * 16 * D, dtype=np.int64) * -1 - 1
+    src = np.arange(40 * H * D, dtype=np.int64).reshape(40, H, D)
+    out, flagged = oracle.paged_kv.scatter(pool, 0, H, D, E, n_pool, [[2, 4]], [14], [3], [0], src)
+    assert not flagged
+    changed = np.nonzero(out != pool)[0]
+    want = sorted(oracle.paged_kv.elem_offset(0, H, D, E, pg, 0, t, c)
+                  for pg, t in ((2, 14), (2, 15), (4, 0)) for c in range(D))
+    assert changed.tolist() == want
+    assert out[oracle.paged_kv.elem_offset(0, H, D, E, 4, 0, 0, 5)] == src[2, 0, 5]
+    out, flagged = oracle.paged_kv.scatter(pool, 1, H, D, E, n_pool, [[1], [0, 9]], [10, 12], [7, 8], [0, 7], src)
+    assert flagged
+    changed = set(np.nonzero(out != pool)[0].tolist())
+    want = {oracle.paged_kv.elem_offset(1, H, D, E, 0, 0, t, c) for t in range(12, 16) for c in range(D)}
+    assert changed == want          # sequence 0 (10 + 7 > 16) skipped; page 9 of sequence 1 skipped
+    out, flagged = oracle.paged_kv.page_copy(pool, H * 16 * D, n_pool, [1, 7], [3, 2])
+    assert flagged
+    pe = H * 16 * D
+    assert np.array_equal(out[3 * pe:4 * pe], pool[pe:2 * pe])
+    assert np.array_equal(np.delete(out, np.s_[3 * pe:4 * pe]), np.delete(pool, np.s_[3 * pe:4 * pe]))
