@@ -223,6 +223,56 @@ halo_status_t halo_kv_page_copy(void* pool, const halo_attn_params_t* params,
                                 const int32_t* src_pages, const int32_t* dst_pages,
                                 int32_t num_pages, int32_t* error_flag, void* stream);
 
+/* Prefix forest from token ids (host only, no device work). The prompts of
+ * a batch that share prefixes (§2 intra-batch prefix sharing: a shared
+ * prefix is computed once and its KV cache reused; §1: recurring prompts are
+ * detected) become the segments and paths of a halo_forest_t: a trie over
+ * page_size-token chunks of the prompts (RadixAttention's radix tree, §7, at
+ * page granularity, so that every shared boundary is page-aligned as the
+ * paged cache needs), compressed into segments. Chunk k of request r is
+ * shared by exactly the requests whose prompts agree with r's on every token
+ * up to the end of that chunk and whose chunk k has the same length; a
+ * segment is a maximal run of chunks shared by the same requests. So two
+ * requests share page_size * floor(lcp / page_size) tokens (lcp = their
+ * longest common prefix), or their whole prompts if these are identical.
+ * Only a segment that ends a prompt can end inside a page, and such a
+ * segment has no children.
+ *   prompt_indptr  [num_requests + 1] HOST int32, prompt_indptr[0] = 0,
+ *                  nondecreasing; request r's prompt is tokens[prompt_indptr[r]
+ *                  .. prompt_indptr[r+1]) (any int32 token ids; empty allowed).
+ * On success *tree (owned by the library until halo_prefix_tree_destroy)
+ * holds the forest and *info (may be NULL) its sizes. Segment ids follow a
+ * depth-first preorder with children in order of first appearance (request
+ * order, then position), so the result is deterministic. */
+typedef struct halo_prefix_tree halo_prefix_tree_t;
+
+typedef struct {
+  int32_t num_segments;
+  int32_t num_path_entries;   /* sum over requests of their path lengths */
+  int64_t num_pages;          /* sum over segments of ceil(seg_len / page_size) */
+  int64_t prompt_tokens;      /* sum of prompt lengths */
+  int64_t distinct_tokens;    /* sum of seg_len: tokens whose KV is stored and
+                                 prefilled once (prompt_tokens minus the
+                                 prefix-caching discount of §4.1) */
+} halo_prefix_tree_info_t;
+
+halo_status_t halo_prefix_tree_build(const int32_t* prompt_indptr, const int32_t* tokens,
+                                     int32_t num_requests, int32_t page_size,
+                                     halo_prefix_tree_t** tree, halo_prefix_tree_info_t* info);
+
+/* Copy the forest into caller-owned HOST arrays (any pointer may be NULL):
+ *   seg_len, seg_parent (-1 for a root segment), seg_refcount (requests whose
+ *   paths hold the segment), seg_src_request / seg_src_offset (the segment's
+ *   tokens are that request's prompt tokens from that offset on)  [num_segments];
+ *   req_seg_indptr [num_requests + 1], req_seg_ids [num_path_entries]: each
+ *   request's path, root first, in halo_forest_t form. */
+halo_status_t halo_prefix_tree_get(const halo_prefix_tree_t* tree, int32_t* seg_len,
+                                   int32_t* seg_parent, int32_t* seg_refcount,
+                                   int32_t* seg_src_request, int32_t* seg_src_offset,
+                                   int32_t* req_seg_indptr, int32_t* req_seg_ids);
+
+void halo_prefix_tree_destroy(halo_prefix_tree_t* tree);
+
 /* Plan statistics for callers and benchmarks (host memory, no device work). */
 typedef struct {
   int32_t is_prefill;

@@ -24,7 +24,8 @@ dot-product attention, softmax(scale * q k^T) v, with grouped heads (q head h
 reads kv head h // (H_q / H_kv)).
 
 ``paged_kv`` holds the reference of the paged-KV write path (token scatter
-into the pool layouts, page copy for copy-on-write).
+into the pool layouts, page copy for copy-on-write); ``forest`` the prefix
+forest of a batch of token-id prompts, by brute force.
 """
 
 from .attention import (  # noqa: F401
@@ -36,3 +37,4 @@ from .attention import (  # noqa: F401
     merge_partials,
 )
 from . import paged_kv  # noqa: F401,E402
+from . import forest  # noqa: F401,E402

@@ -44,11 +44,14 @@ def build(verbose=True):
     tmp = tempfile.mkdtemp(prefix="halo_build_")
     try:
         plan_o = os.path.join(tmp, "halo_plan.o")
+        forest_o = os.path.join(tmp, "halo_forest.o")
         kern_o = os.path.join(tmp, "halo_kernels.o")
         pages_o = os.path.join(tmp, "halo_pages.o")
         procs = [
             subprocess.Popen(["g++", "-std=c++17", "-O2", "-fPIC", "-Wall", "-Wextra",
                               "-I", INCLUDE, "-c", os.path.join(CSRC, "halo_plan.cpp"), "-o", plan_o]),
+            subprocess.Popen(["g++", "-std=c++17", "-O2", "-fPIC", "-Wall", "-Wextra",
+                              "-I", INCLUDE, "-c", os.path.join(CSRC, "halo_forest.cpp"), "-o", forest_o]),
             subprocess.Popen([HIPCC] + HIP_FLAGS + ["-I", INCLUDE, "-c",
                                                    os.path.join(CSRC, "halo_kernels.hip"), "-o", kern_o]),
             subprocess.Popen([HIPCC] + HIP_FLAGS + ["-I", INCLUDE, "-c",
@@ -58,7 +61,7 @@ def build(verbose=True):
         if any(rcs):
             raise RuntimeError(f"compilation failed (exit codes {rcs})")
         out_tmp = LIB_PATH + ".tmp"
-        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, kern_o, pages_o, "-o", out_tmp])
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, forest_o, kern_o, pages_o, "-o", out_tmp])
         os.replace(out_tmp, LIB_PATH)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)

@@ -62,8 +62,15 @@ EXPORTED_SYMBOLS = (
     "halo_plan_inspect",
     "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_kv_page_gather",
     "halo_kv_page_scatter", "halo_kv_page_scatter_kv", "halo_kv_page_copy",
+    "halo_prefix_tree_build", "halo_prefix_tree_get", "halo_prefix_tree_destroy",
     "halo_status_string", "halo_last_error_message",
 )
+
+
+class PrefixTreeInfo(ctypes.Structure):
+    _fields_ = [("num_segments", ctypes.c_int32), ("num_path_entries", ctypes.c_int32),
+                ("num_pages", ctypes.c_int64), ("prompt_tokens", ctypes.c_int64),
+                ("distinct_tokens", ctypes.c_int64)]
 
 
 class HaloError(RuntimeError):
@@ -132,6 +139,13 @@ def load_library(require_gpu=False):
     lib.halo_kv_page_scatter_kv.restype = ctypes.c_int
     lib.halo_kv_page_copy.argtypes = [vp, ctypes.POINTER(AttnParams), vp, vp, ctypes.c_int32, vp, vp]
     lib.halo_kv_page_copy.restype = ctypes.c_int
+    lib.halo_prefix_tree_build.argtypes = [vp, vp, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(vp),
+                                           ctypes.POINTER(PrefixTreeInfo)]
+    lib.halo_prefix_tree_build.restype = ctypes.c_int
+    lib.halo_prefix_tree_get.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.halo_prefix_tree_get.restype = ctypes.c_int
+    lib.halo_prefix_tree_destroy.argtypes = [vp]
+    lib.halo_prefix_tree_destroy.restype = None
     lib.halo_status_string.argtypes = [ctypes.c_int]
     lib.halo_status_string.restype = ctypes.c_char_p
     lib.halo_last_error_message.argtypes = []
@@ -244,6 +258,67 @@ class Plan:
 
     def __del__(self):
         self.close()
+
+
+class PrefixTree:
+    """halo_prefix_tree_build on a list of token-id prompts (host only).
+
+    Attributes (numpy int32): seg_len, seg_parent, seg_refcount,
+    seg_src_request, seg_src_offset, req_seg_indptr, req_seg_ids; ints
+    num_pages, prompt_tokens, distinct_tokens. forest_csr(page_ids) gives the
+    forest in the form Plan.from_csr takes."""
+
+    def __init__(self, prompts, page_size=16):
+        lib = load_library()
+        prompts = [np.asarray(p, dtype=np.int32).ravel() for p in prompts]
+        indptr = np.zeros(len(prompts) + 1, dtype=np.int32)
+        indptr[1:] = np.cumsum([len(p) for p in prompts])
+        tokens = np.ascontiguousarray(np.concatenate(prompts) if prompts else np.zeros(0, np.int32),
+                                      dtype=np.int32)
+        handle = ctypes.c_void_p()
+        info = PrefixTreeInfo()
+        _check(lib.halo_prefix_tree_build(_ptr(indptr), _ptr(tokens) if tokens.size else None,
+                                          len(prompts), int(page_size), ctypes.byref(handle), ctypes.byref(info)))
+        try:
+            S, P, R = info.num_segments, info.num_path_entries, len(prompts)
+            out = {n: np.zeros(S, np.int32) for n in ("seg_len", "seg_parent", "seg_refcount",
+                                                      "seg_src_request", "seg_src_offset")}
+            out["req_seg_indptr"] = np.zeros(R + 1, np.int32)
+            out["req_seg_ids"] = np.zeros(P, np.int32)
+            names = ("seg_len", "seg_parent", "seg_refcount", "seg_src_request", "seg_src_offset",
+                     "req_seg_indptr", "req_seg_ids")
+            _check(lib.halo_prefix_tree_get(handle, *[_ptr(out[n]) for n in names]))
+        finally:
+            lib.halo_prefix_tree_destroy(handle)
+        for n, a in out.items():
+            setattr(self, n, a)
+        self.page_size = int(page_size)
+        self.num_pages = int(info.num_pages)
+        self.prompt_tokens = int(info.prompt_tokens)
+        self.distinct_tokens = int(info.distinct_tokens)
+
+    @property
+    def num_segments(self):
+        return len(self.seg_len)
+
+    def paths(self):
+        return [self.req_seg_ids[self.req_seg_indptr[r]:self.req_seg_indptr[r + 1]].tolist()
+                for r in range(len(self.req_seg_indptr) - 1)]
+
+    def pages_per_segment(self):
+        return (self.seg_len + self.page_size - 1) // self.page_size
+
+    def forest_csr(self, seg_page_ids, q_len=None):
+        """The forest with the caller's page ids (seg_page_ids lists, segment
+        after segment, pages_per_segment() ids each)."""
+        indptr = np.zeros(self.num_segments + 1, dtype=np.int32)
+        indptr[1:] = np.cumsum(self.pages_per_segment())
+        ids = np.asarray(seg_page_ids, dtype=np.int32)
+        if ids.size != indptr[-1]:
+            raise ValueError(f"{indptr[-1]} page ids needed, got {ids.size}")
+        return dict(seg_len=self.seg_len.copy(), seg_page_indptr=indptr, seg_page_ids=ids,
+                    req_seg_indptr=self.req_seg_indptr.copy(), req_seg_ids=self.req_seg_ids.copy(),
+                    q_len=None if q_len is None else np.asarray(q_len, np.int32))
 
 
 def _stream_handle(stream):
