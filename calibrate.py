@@ -1,0 +1,238 @@
+"""Latency calibration curves of the attention path on one MI355X.
+
+    python calibrate.py [--quick] [--json OUT.json] [--md OUT.md]
+
+The paper's optimizer charges every LLM call a latency T_infer taken from
+calibrated throughput curves (§4.1, operator profiling: prefill and decode
+tokens mapped to latency), and applies a prefix-caching discount: prompt
+tokens covered by a cached, shared prefix are not charged as new work
+(§4.1, state-conditional estimator). This script measures the attention part
+of those curves for this library: the latency of one decode step, and of one
+chunked prefill, as a function of the shared prefix length P, the private
+suffix (or chunk) length S, the number of requests sharing each prefix G and
+the batch size R, on Llama-3-8B-shaped heads (32 query / 8 KV heads, d 128,
+bf16).
+
+Each point is a synthetic batch (R / G prefixes of P tokens, each shared by G
+requests, every request with S private tokens; pages placed at random in a
+pool of 1.25x the need), timed over single calls with HIP events on the
+call's stream, the median of the calls taken, inputs rotated over copies
+larger than the Infinity Cache so keys stream from HBM.
+
+A linear model is fitted by non-negative least squares (weighted for
+relative error):
+
+    T = c0 + c_kv * (distinct K/V bytes) + c_pair * (visible (query, key)
+        pairs x query heads) + c_row * (query rows x query heads)
+        + c_split * (1 if decode rows are split over several work items,
+          which adds the merge launch) + c_shared * (K/V bytes of prefixes
+          shared by more than one request)
+
+in which the prefix-caching discount is explicit: a prefix shared by G
+requests contributes its K/V bytes once, not G times. Checks: T grows with S
+and with P; at fixed P and S, a larger group is not slower; the fit's
+relative error. One JSON object is printed (and written with --json).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MALL_BYTES = 256 << 20
+HQ, HKV, D = 32, 8, 128
+ELT = 2        # bf16
+MONOTONE_TOL = 0.03
+
+DECODE_GRID = dict(requests=[64], group=[1, 4, 16, 64], prefix=[0, 512, 2048, 8192], suffix=[64, 256, 1024])
+PREFILL_GRID = dict(requests=[8, 32], group=["1", "all"], prefix=[0, 1024, 4096], suffix=[128, 512])
+QUICK_DECODE = dict(requests=[32], group=[1, 32], prefix=[0, 1024], suffix=[64, 1024])
+QUICK_PREFILL = dict(requests=[8], group=["all"], prefix=[0, 1024], suffix=[128, 256])
+
+
+def features(kind, requests, group, prefix, suffix):
+    """Model features of one point: 1, distinct K/V bytes, visible pairs x
+    query heads, query rows x query heads (a decode step has one query row
+    per request, a prefill chunk `suffix` rows, causal inside the chunk),
+    the split indicator (decode rows whose keys span a shared prefix and a
+    suffix, or more than 1024 private keys, go through the merge) and the
+    K/V bytes of shared prefixes."""
+    n_prefixes = requests // group if prefix > 0 else 0
+    kv_tokens = n_prefixes * prefix + requests * suffix
+    tok_bytes = 2 * HKV * D * ELT
+    shared_bytes = n_prefixes * prefix * tok_bytes if group > 1 else 0
+    if kind == "decode":
+        rows = requests
+        pairs = requests * (prefix + suffix)
+        split = 1.0 if (group > 1 and prefix > 0) or prefix + suffix > 1024 else 0.0
+    else:
+        rows = requests * suffix
+        pairs = requests * (suffix * prefix + suffix * (suffix + 1) // 2)
+        split = 0.0
+    return [1.0, float(kv_tokens * tok_bytes), float(pairs * HQ), float(rows * HQ), split, float(shared_bytes)]
+
+
+def fit(points):
+    """Non-negative least squares of the latency model on a list of
+    (features, latency_us); returns coefficients and relative errors."""
+    import numpy as np
+    from scipy.optimize import nnls
+    X = np.array([p[0] for p in points], dtype=np.float64)
+    y = np.array([p[1] for p in points], dtype=np.float64)
+    # weight by 1/y so that the fit minimises relative, not absolute, error
+    w = 1.0 / y
+    coef, _ = nnls(X * w[:, None], y * w)
+    pred = X @ coef
+    rel = np.abs(pred - y) / y
+    return coef.tolist(), rel.tolist()
+
+
+def predict(coef, kind, requests, group, prefix, suffix):
+    import numpy as np
+    return float(np.dot(coef, features(kind, requests, group, prefix, suffix)))
+
+
+def check_monotone(points, tol=MONOTONE_TOL):
+    """Violations of the expected orderings among measured points, each
+    given by its keys (kind, requests, group, prefix, suffix) -> latency:
+    longer suffix or prefix is not faster; a larger sharing group is not
+    slower (P > 0)."""
+    bad = []
+    for (kind, r, g, p, s), t in points.items():
+        for (kind2, r2, g2, p2, s2), t2 in points.items():
+            if (kind2, r2) != (kind, r):
+                continue
+            if g2 == g and p2 == p and s2 > s and t2 < t * (1 - tol):
+                bad.append(f"{kind} R={r} G={g} P={p}: S {s}->{s2} went {t:.1f}->{t2:.1f} us")
+            if g2 == g and s2 == s and p2 > p and t2 < t * (1 - tol):
+                bad.append(f"{kind} R={r} G={g} S={s}: P {p}->{p2} went {t:.1f}->{t2:.1f} us")
+            if p > 0 and p2 == p and s2 == s and g2 > g and t2 > t * (1 + tol):
+                bad.append(f"{kind} R={r} P={p} S={s}: G {g}->{g2} went {t:.1f}->{t2:.1f} us")
+    return bad
+
+
+def _measure(kind, requests, group, prefix, suffix, calls, seed):
+    import numpy as np
+    import torch
+    from paper_2509_02121_amd import halo
+    from workloads import build_workload
+    n_prefixes = requests // group if prefix > 0 else 0
+    seg_len = [prefix] * n_prefixes + [suffix] * requests
+    paths = [([r // group] if prefix > 0 else []) + [n_prefixes + r] for r in range(requests)]
+    q_len = None if kind == "decode" else np.full(requests, suffix, dtype=np.int32)
+    w = build_workload(f"cal_{kind}", seed, HQ, HKV, D, torch.bfloat16, seg_len, paths, q_len,
+                       value_scale=0.5, device="cuda")
+    params = halo.make_params(HQ, HKV, D, torch.bfloat16, w.num_pool_pages, w.scale, torch.bfloat16)
+    runner = halo.PrefixAttention(params, w.forest_csr(), "cuda")
+    pool_bytes = (w.k_pool.numel() + w.v_pool.numel()) * ELT
+    n_rep = max(1, min(16, -(-4 * MALL_BYTES // max(pool_bytes, 1))))
+    reps = [(w.q, w.k_pool, w.v_pool)] + [(w.q.clone(), w.k_pool.clone(), w.v_pool.clone())
+                                          for _ in range(n_rep - 1)]
+    stream = torch.cuda.current_stream()
+    outs = [runner.alloc_outputs(w.q) for _ in range(n_rep)]
+    fns = [runner.bind(*reps[i], *outs[i], stream) for i in range(n_rep)]
+    for i in range(10):
+        fns[i % n_rep]()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+    for i, (a, b) in enumerate(ev):
+        a.record(stream)
+        fns[i % n_rep]()
+        b.record(stream)
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
+    del reps, outs, fns, runner, w
+    torch.cuda.empty_cache()
+    return t[len(t) // 2]
+
+
+def run(grids, calls=50, log=print):
+    points = {}
+    for kind, grid in grids:
+        for r in grid["requests"]:
+            groups = sorted({r if g == "all" else int(g) for g in grid["group"]} & set(range(1, r + 1)))
+            groups = [g for g in groups if r % g == 0]
+            for g in groups:
+                for p in grid["prefix"]:
+                    if p == 0 and g != groups[0]:
+                        continue       # without a prefix the group size changes nothing
+                    for s in grid["suffix"]:
+                        t0 = time.perf_counter()
+                        us = _measure(kind, r, g, p, s, calls, seed=1 + len(points))
+                        points[(kind, r, g, p, s)] = us
+                        log(f"{kind} R={r} G={g} P={p} S={s}: {us:.1f} us "
+                            f"({time.perf_counter() - t0:.1f} s)")
+    return points
+
+
+def summarize(points):
+    out = {"model": "T_us = c0 + c_kv*kv_bytes + c_pair*pairs_x_hq + c_row*rows_x_hq + c_split*split "
+                    "+ c_shared*shared_kv_bytes",
+           "shape": {"num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": D, "dtype": "bf16"},
+           "points": [dict(kind=k[0], requests=k[1], group=k[2], prefix=k[3], suffix=k[4], us=round(v, 2))
+                      for k, v in points.items()]}
+    for kind in ("decode", "prefill"):
+        pts = [(features(*k), v) for k, v in points.items() if k[0] == kind]
+        if len(pts) < 4:
+            continue
+        coef, rel = fit(pts)
+        out[kind] = {"coef": dict(zip(("c0_us", "c_kv_us_per_byte", "c_pair_us", "c_row_us", "c_split_us",
+                                       "c_shared_us_per_byte"), coef)),
+                     "effective_kv_tbps": round(1.0 / coef[1] / 1e6, 3) if coef[1] > 0 else None,
+                     "max_rel_err": round(max(rel), 4), "median_rel_err": round(sorted(rel)[len(rel) // 2], 4)}
+    out["monotonicity_violations"] = check_monotone(points)
+    return out
+
+
+def to_markdown(summary, command):
+    lines = ["# Attention latency calibration (decode step and chunked prefill)", "",
+             "Command (repository root, one MI355X):", "", f"    {command}", "",
+             f"Heads {HQ}/{HKV}, d {D}, bf16. R requests, G sharing each prefix of P tokens, S private "
+             "tokens each (decode) or an S-token causal chunk each (prefill). Median of single calls.", "",
+             "| kind | R | G | P | S | us |", "|---|---|---|---|---|---|"]
+    for p in summary["points"]:
+        lines.append(f"| {p['kind']} | {p['requests']} | {p['group']} | {p['prefix']} | {p['suffix']} | {p['us']} |")
+    lines += ["", f"Model: `{summary['model']}` (non-negative least squares, relative error weighting).", ""]
+    for kind in ("decode", "prefill"):
+        if kind in summary:
+            s = summary[kind]
+            lines.append(f"- {kind}: {json.dumps(s['coef'])}; effective K/V streaming rate "
+                         f"{s['effective_kv_tbps']} TB/s; relative error max {s['max_rel_err']}, "
+                         f"median {s['median_rel_err']}.")
+    v = summary["monotonicity_violations"]
+    lines += ["", f"Monotonicity violations (tolerance {MONOTONE_TOL:.0%}): " + ("none." if not v else ""), ""]
+    lines += [f"- {x}" for x in v]
+    return "\n".join(lines) + "\n"
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--quick", action="store_true", help="a few points only")
+    ap.add_argument("--calls", type=int, default=50)
+    ap.add_argument("--json", default=None)
+    ap.add_argument("--md", default=None)
+    args = ap.parse_args()
+    import torch
+    from paper_2509_02121_amd import halo
+    halo.load_library(require_gpu=True)
+    torch.cuda.set_device(0)
+    grids = [("decode", QUICK_DECODE), ("prefill", QUICK_PREFILL)] if args.quick else \
+        [("decode", DECODE_GRID), ("prefill", PREFILL_GRID)]
+    points = run(grids, args.calls, log=lambda m: print(m, flush=True))
+    summary = summarize(points)
+    if args.json:
+        with open(args.json, "w") as f:
+            json.dump(summary, f, indent=1)
+    if args.md:
+        cmd = "python -u calibrate.py" + (" --quick" if args.quick else "") + (f" --md {args.md}" if args.md else "")
+        with open(args.md, "w") as f:
+            f.write(to_markdown(summary, cmd))
+    print(json.dumps({k: v for k, v in summary.items() if k != "points"}), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,51 @@
+"""CPU checks of the calibration helpers (calibrate.py): the feature counts
+of a point, the fit on synthetic latencies of known coefficients, and the
+monotonicity check on a planted violation."""
+
+import numpy as np
+
+import calibrate
+
+
+def test_features_count_kv_bytes_pairs_and_rows():
+    # 8 requests in 2 groups of 4 on 100-token prefixes, 10 private tokens each
+    f = calibrate.features("decode", 8, 4, 100, 10)
+    kv_tok = 2 * 100 + 8 * 10
+    tok = 2 * 8 * 128 * 2
+    assert f == [1.0, kv_tok * tok, 8 * 110 * 32, 8 * 32, 1.0, 2 * 100 * tok]
+    # one request per prefix: nothing shared, nothing split below 1024 keys
+    assert calibrate.features("decode", 8, 1, 100, 10)[4:] == [0.0, 0.0]
+    assert calibrate.features("decode", 8, 1, 1000, 100)[4] == 1.0
+    # prefill: 3-token causal chunks see the prefix and 1, 2, 3 chunk keys
+    f = calibrate.features("prefill", 2, 2, 5, 3)
+    assert f[2] == 2 * (3 * 5 + 6) * 32 and f[3] == 2 * 3 * 32
+    # no prefix: the group size does not matter
+    assert calibrate.features("decode", 8, 1, 0, 10) == calibrate.features("decode", 8, 8, 0, 10)
+
+
+def test_fit_recovers_known_coefficients():
+    rng = np.random.default_rng(0)
+    true = [3.0, 1 / 5e6, 2e-5, 1e-3, 4.0, 1e-8]
+    pts = []
+    for r in (16, 64):
+        for g in (1, 4, 16):
+            for p in (0, 512, 4096):
+                for s in (64, 1024):
+                    f = calibrate.features("decode", r, g, p, s)
+                    pts.append((f, float(np.dot(true, f)) * (1 + 0.01 * rng.standard_normal())))
+    coef, rel = calibrate.fit(pts)
+    assert max(rel) < 0.05
+    assert abs(coef[1] - true[1]) / true[1] < 0.1
+    pred = calibrate.predict(coef, "decode", 64, 16, 2048, 256)
+    want = float(np.dot(true, calibrate.features("decode", 64, 16, 2048, 256)))
+    assert abs(pred - want) / want < 0.05
+
+
+def test_monotonicity_check_flags_planted_violations():
+    pts = {("decode", 64, 1, 512, 64): 10.0, ("decode", 64, 1, 512, 256): 14.0,
+           ("decode", 64, 4, 512, 64): 9.0, ("decode", 64, 4, 512, 256): 12.0}
+    assert calibrate.check_monotone(pts) == []
+    pts[("decode", 64, 1, 512, 1024)] = 12.0          # longer suffix, faster: planted
+    pts[("decode", 64, 16, 512, 64)] = 11.0           # larger group, slower: planted
+    bad = calibrate.check_monotone(pts)
+    assert any("S 256->1024" in b for b in bad) and any("G 4->16" in b for b in bad)
