@@ -322,3 +322,41 @@ def test_copy_on_write_mid_page_prefix(gpu_lib, prefix_len):
     err = np.abs(o.double().cpu().numpy() - o_ref).max()
     assert err <= 2e-2, err
     assert np.abs(lse.double().cpu().numpy() - lse_ref).max() <= 1e-3
+
+
+def test_scatter_and_copy_at_high_page_ids(gpu_lib):
+    """Pages past the first 2^31 bytes of a pool (offsets that overflow 32
+    bits): a token range written into the last two pages and a page copied
+    into the third-to-last one land exactly there, per the oracle."""
+    print("case: write path at high page ids", flush=True)
+    dev = "cuda"
+    H, D, dtype = 1, 128, torch.bfloat16
+    page_elems = H * PAGE * D
+    n_pool = (3 << 30) // (page_elems * 2)            # 3 GiB of pool
+    assert (n_pool - 1) * page_elems * 2 > (1 << 31)
+    pool = torch.zeros(n_pool * page_elems, dtype=dtype, device=dev)
+    rng = np.random.default_rng(9)
+    src_page = _random_bits((page_elems,), torch.int16, rng)
+    pool.view(torch.int16)[5 * page_elems:6 * page_elems] = src_page.to(dev)
+    toks = _random_bits((20, H, D), torch.int16, rng)
+    params = halo.make_params(H, H, D, dtype, n_pool, 0.125, dtype)
+    pages = np.array([n_pool - 2, n_pool - 1], np.int32)
+    for kind in (halo.HALO_POOL_K, halo.HALO_POOL_V):
+        pool.view(torch.int16)[(n_pool - 3) * page_elems:].zero_()
+        halo.kv_page_scatter(pool, params, kind, torch.as_tensor(pages, device=dev),
+                             torch.tensor([0, 2], dtype=torch.int32, device=dev),
+                             torch.tensor([7], dtype=torch.int32, device=dev),
+                             torch.tensor([20], dtype=torch.int32, device=dev),
+                             torch.zeros(1, dtype=torch.int64, device=dev), toks.to(dev).view(dtype))
+        halo.kv_page_copy(pool, params, torch.tensor([5], dtype=torch.int32, device=dev),
+                          torch.tensor([n_pool - 3], dtype=torch.int32, device=dev))
+        torch.cuda.synchronize()
+        tail = pool.view(torch.int16)[(n_pool - 3) * page_elems:].cpu().numpy()
+        # the oracle on a 6-page pool whose pages 3, 4, 5 stand for the last three
+        small = np.zeros(6 * page_elems, np.int16)
+        small[0:page_elems] = src_page.numpy()
+        small, _ = oracle.paged_kv.page_copy(small, page_elems, 6, [0], [3])
+        small, _ = oracle.paged_kv.scatter(small, kind, H, D, 8, 6, [[4, 5]], [7], [20], [0], toks.numpy())
+        assert np.array_equal(tail, small[3 * page_elems:])
+    del pool
+    torch.cuda.empty_cache()
