@@ -205,6 +205,54 @@ def write_path_bench(args):
     print(json.dumps(line), flush=True)
 
 
+def gather_bench(args):
+    """Page gather of every segment of the workload (its distinct K/V working
+    set), one launch per pool, timed with events on the launch stream (one
+    JSON line). Algorithmic bytes: the gathered bytes read plus the same
+    bytes written."""
+    import numpy as np
+    import torch
+    from paper_2509_02121_amd import halo
+    from workloads import make_config
+
+    halo.load_library(require_gpu=True)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = make_config(args.workload, device=dev, poison=False)
+    params = halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages,
+                              w.scale, w.dtype)
+    S = len(w.seg_pages)
+    lens = np.asarray(w.seg_len, np.int64)
+    indptr = np.zeros(S + 1, np.int32)
+    indptr[1:] = np.cumsum([len(p) for p in w.seg_pages])
+    offs = np.zeros(S, np.int64)
+    offs[1:] = np.cumsum(lens)[:-1]
+    n_tok = int(lens.sum())
+    t = lambda a: torch.as_tensor(a, device=dev)
+    ids = t(np.concatenate(w.seg_pages).astype(np.int32))
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    out = torch.empty((n_tok, w.num_kv_heads, w.head_dim), dtype=w.dtype, device=dev)
+    stream = torch.cuda.current_stream()
+    res = {}
+    lens_d, indptr_d, offs_d = t(lens.astype(np.int32)), t(indptr), t(offs)
+    for name, pool, kind in (("k", w.k_pool, halo.HALO_POOL_K), ("v", w.v_pool, halo.HALO_POOL_V)):
+        call = halo.bind_kv_page_gather(pool, params, kind, ids, indptr_d, lens_d, offs_d, out, flag, stream)
+        res[name] = _time_launches(call, args.steps, args.warmup, stream)
+    torch.cuda.synchronize()
+    if int(flag.item()):
+        raise SystemExit("gather flagged bad input")
+    elt = w.k_pool.element_size()
+    nbytes = 2 * n_tok * w.num_kv_heads * w.head_dim * elt
+    gbps = lambda us: round(nbytes / (us * 1e-6) / 1e9, 1)
+    line = {"metric": "paged-KV gather: HBM GB/s per launch",
+            "config": {"workload": w.name, "segments": S, "tokens": n_tok, "steps": args.steps},
+            "bytes_per_launch": nbytes}
+    for name in ("k", "v"):
+        line["gather_" + name] = {"us": round(res[name], 2), "gbps": gbps(res[name]),
+                                  "frac": round(gbps(res[name]) / HBM_PEAK_GBPS, 4)}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -226,7 +274,16 @@ def main():
                     help="only time the paged-KV write path on the workload's page lists: each "
                          "request's newest token appended (decode) or its chunk written (prefill), "
                          "K and V pools, and a copy-on-write page copy per request")
+    ap.add_argument("--gather", action="store_true",
+                    help="only time the page gather of the workload's whole working set (every "
+                         "segment, K and V pools) into dense token-major buffers")
     args = ap.parse_args()
+    if args.gather:
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        gather_bench(args)
+        return
     if args.write_path:
         if args.gpus != 1:
             print("bench.py measures one GPU only", file=sys.stderr)

@@ -155,7 +155,8 @@ halo_status_t halo_prefix_attn_prefill(const halo_plan_t* plan, const void* devi
  * for t < seq_len[i], where token t lives in page page_ids[seq_page_indptr[i]
  * + t / page_size]. pool_kind says whether pool has the k_pool or the
  * v_pool layout. page_ids, seq_page_indptr, seq_len, out_token_offset and
- * out are DEVICE pointers; out is [*][num_kv_heads][head_dim] of kv_dtype.
+ * out are DEVICE pointers; out is [*][num_kv_heads][head_dim] of kv_dtype;
+ * pool and out must be 16-byte aligned.
  * Only params' num_kv_heads, head_dim, page_size, num_pool_pages and
  * kv_dtype are used. Every page of a sequence whose page count is not
  * ceil(seq_len/page_size), and every page whose id is outside

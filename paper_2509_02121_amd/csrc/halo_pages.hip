@@ -42,55 +42,93 @@ struct GatherArgs {
   int32_t v_layout;
 };
 
-// One block per (page slot, head) tile, grid-stride. W is an unsigned word of
-// the element's width, so every bit pattern (NaN payloads included) moves
-// unchanged.
-template <typename W>
+// The (page slot, head) tiles of all sequences, in order, are cut into equal
+// contiguous runs, one per wave, so a few long sequences among many short
+// ones spread over the whole grid. A wave finds the sequence of its first
+// tile by binary search over seq_page_indptr and walks forward from there.
+// Per tile it reads the tile in its stored order with 16-byte loads
+// (coalesced), stages it token-major in its own LDS buffer ([16][D + E]
+// words, rows 16-byte aligned) and writes the tile's tokens as dense rows,
+// 16 bytes per lane. K vectors hold E dims of one token and move whole; V
+// vectors hold one dim of E tokens and are split into single words on the
+// way into LDS. W is an unsigned word of the element's width, so every bit
+// pattern (NaN payloads included) moves unchanged.
+template <typename W, int D>
 __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
-  __shared__ W tile[16 * (128 + 1)];
-  const int D = a.head_dim;
-  const int64_t total_tiles = (int64_t)a.seq_page_indptr[a.num_seqs] * a.num_kv_heads;
+  constexpr int E = 16 / (int)sizeof(W);   // elements per 16-byte vector
+  constexpr int VPT = D / E;               // vectors per token and head
+  constexpr int NV = 16 * VPT / 64;        // vectors per lane for a tile
+  constexpr int ROW = D + E;               // staged row, in words (16-byte aligned)
+  __shared__ u32x4_t stage[4][16 * ROW / E];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int H = a.num_kv_heads;
+  const int64_t row = (int64_t)H * D;      // output elements per token
   const W* pool = static_cast<const W*>(a.pool);
   W* out = static_cast<W*>(a.out);
-  for (int64_t tl = blockIdx.x; tl < total_tiles; tl += gridDim.x) {
-    const int64_t slot = tl / a.num_kv_heads;
-    const int h = (int)(tl % a.num_kv_heads);
-    int lo = 0, hi = a.num_seqs - 1;   // last sequence whose first slot <= slot
+  W* st = reinterpret_cast<W*>(stage[wave]);
+
+  const int64_t total = (int64_t)a.seq_page_indptr[a.num_seqs] * H;
+  const int64_t waves = (int64_t)gridDim.x * 4;
+  const int64_t per = (total + waves - 1) / waves;
+  const int64_t w_id = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t t_begin = w_id * per;
+  const int64_t t_end = min(total, t_begin + per);
+  if (t_begin >= t_end) return;
+  int seq;
+  {
+    const int64_t slot = t_begin / H;
+    int lo = 0, hi = a.num_seqs - 1;     // last sequence whose first slot <= slot
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
       if (a.seq_page_indptr[mid] <= slot) lo = mid; else hi = mid - 1;
     }
-    const int len = a.seq_len[lo];
-    const int npages = a.seq_page_indptr[lo + 1] - a.seq_page_indptr[lo];
+    seq = lo;
+  }
+  int base = a.seq_page_indptr[seq], next = a.seq_page_indptr[seq + 1];
+  for (int64_t tl = t_begin; tl < t_end; ++tl) {
+    const int slot = (int)(tl / H), h = (int)(tl % H);
+    while (slot >= next) {             // later sequences (empty ones are passed over)
+      ++seq;
+      base = next;
+      next = a.seq_page_indptr[seq + 1];
+    }
+    const int len = a.seq_len[seq];
     const int pid = a.page_ids[slot];
-    if (len < 0 || npages != (len + 15) / 16 || pid < 0 || pid >= a.num_pool_pages) {
-      if (threadIdx.x == 0 && a.error_flag) a.error_flag[0] = 1;
+    if (len < 0 || next - base != (len + 15) / 16 || pid < 0 || pid >= a.num_pool_pages) {
+      if (lane == 0 && a.error_flag) a.error_flag[0] = 1;
       continue;
     }
-    const int t0 = (int)(slot - a.seq_page_indptr[lo]) * 16;
+    const int t0 = (slot - base) * 16;
     const int n = min(16, len - t0);
-    const int64_t out_tok = a.out_token_offset[lo] + t0;
-    const W* src = pool + ((int64_t)pid * a.num_kv_heads + h) * 16 * D;
-    // Read the whole (page, head) tile coalesced, in its stored order, and
-    // place element (token t, dim c) at tile[t][c] (row stride D + 1).
-    constexpr int E = 16 / (int)sizeof(W);
-    for (int e = threadIdx.x; e < 16 * D; e += blockDim.x) {
-      int t, c;
-      if (!a.v_layout) {           // K: [D/E][16][E]
-        c = (e / (16 * E)) * E + e % E;
-        t = (e / E) % 16;
-      } else {                     // V: [D][16], slots hold tokens 0-3, 8-11, 4-7, 12-15
-        c = e >> 4;
-        t = v_token_at_slot(e & 15);
+    const W* src = pool + ((int64_t)pid * H + h) * 16 * D;
+    u32x4_t v[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = reinterpret_cast<const u32x4_t*>(src)[lane + 64 * i];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = lane + 64 * i;
+      if (!a.v_layout) {             // K: vector idx = (dims j*E.., token t)
+        const int j = idx / 16, t = idx % 16;
+        *reinterpret_cast<u32x4_t*>(st + t * ROW + j * E) = v[i];
+      } else {                       // V: vector idx = (dim c, slots part*E..)
+        const int c = idx / (16 / E), part = idx % (16 / E);
+        const W* e = reinterpret_cast<const W*>(&v[i]);
+#pragma unroll
+        for (int q = 0; q < E; ++q) st[v_token_at_slot(part * E + q) * ROW + c] = e[q];
       }
-      tile[t * (D + 1) + c] = src[e];
     }
-    __syncthreads();
-    for (int e = threadIdx.x; e < n * D; e += blockDim.x) {
-      const int tok = e / D, c = e - tok * D;
-      out[((out_tok + tok) * a.num_kv_heads + h) * D + c] = tile[tok * (D + 1) + c];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    W* dst = out + (a.out_token_offset[seq] + t0) * row + (int64_t)h * D;
+    for (int idx = lane; idx < n * VPT; idx += 64) {
+      const int tok = idx / VPT, j = idx % VPT;
+      *reinterpret_cast<u32x4_t*>(dst + tok * row + j * E) =
+          *reinterpret_cast<const u32x4_t*>(st + tok * ROW + j * E);
     }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
@@ -302,13 +340,20 @@ extern "C" halo_status_t halo_kv_page_gather(const void* pool, const halo_attn_p
                pool_kind == HALO_POOL_V ? 1 : 0};
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  const int blocks = 2048;
-  if (params->kv_dtype == HALO_BF16)
-    hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, st, g);
-  else if (params->kv_dtype == HALO_F32)
-    hipLaunchKernelGGL(gather_kernel<uint32_t>, dim3(blocks), dim3(256), 0, st, g);
-  else
+  if (!aligned16(pool) || !aligned16(out))
+    return fail(HALO_ERR_INVALID_ARGUMENT, "pool and out must be 16-byte aligned");
+  // 2048 workgroups of four waves; each wave takes an equal run of tiles.
+  const dim3 grid(2048);
+  const bool d128 = params->head_dim == 128;
+  if (params->kv_dtype == HALO_BF16) {
+    if (d128) hipLaunchKernelGGL((gather_kernel<uint16_t, 128>), grid, dim3(256), 0, st, g);
+    else hipLaunchKernelGGL((gather_kernel<uint16_t, 64>), grid, dim3(256), 0, st, g);
+  } else if (params->kv_dtype == HALO_F32) {
+    if (d128) hipLaunchKernelGGL((gather_kernel<uint32_t, 128>), grid, dim3(256), 0, st, g);
+    else hipLaunchKernelGGL((gather_kernel<uint32_t, 64>), grid, dim3(256), 0, st, g);
+  } else {
     return fail(HALO_ERR_UNSUPPORTED, "kv_dtype must be HALO_F32 or HALO_BF16");
+  }
   return hip_check("gather launch");
 }
 

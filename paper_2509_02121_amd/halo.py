@@ -395,6 +395,22 @@ def kv_page_copy(pool, params, src_pages, dst_pages, error_flag=None, stream=Non
                                   _stream_handle(stream)))
 
 
+def bind_kv_page_gather(pool, params, pool_kind, page_ids, seq_page_indptr, seq_len, out_token_offset, out,
+                        error_flag=None, stream=None):
+    """kv_page_gather as a zero-argument callable (see bind_kv_page_scatter)."""
+    load_library()
+    args = (pool.data_ptr(), ctypes.byref(params), int(pool_kind), page_ids.data_ptr(), seq_page_indptr.data_ptr(),
+            seq_len.data_ptr(), out_token_offset.data_ptr(), int(seq_page_indptr.numel() - 1), out.data_ptr(),
+            error_flag.data_ptr() if error_flag is not None else None, _stream_handle(stream))
+    fn = _LIB.halo_kv_page_gather
+
+    def call():
+        st = fn(*args)
+        if st != HALO_OK:
+            _check(st)
+    return call
+
+
 def bind_kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq_start, seq_count,
                          in_token_offset, src, error_flag=None, stream=None):
     """A zero-argument callable that enqueues kv_page_scatter with every
