@@ -87,3 +87,23 @@ def test_gather_flags_bad_page_ids_and_skips_them(gpu_lib):
     assert (out[256:256 + 16].float() == 7.0).all()             # the bad page left untouched
     rest = _expected(w, [1], halo.HALO_POOL_K)[16:]
     assert np.array_equal(_bits(out[256 + 16:256 + 16 + rest.shape[0]]), _bits(rest))
+
+
+@pytest.mark.parametrize("dtype,D", [(torch.bfloat16, 128), (torch.float32, 64), (torch.bfloat16, 64)])
+@pytest.mark.parametrize("kind", [halo.HALO_POOL_K, halo.HALO_POOL_V])
+def test_gather_skewed_and_empty_sequences(gpu_lib, dtype, D, kind):
+    """Empty sequences between others, one long sequence among many short
+    ones, lengths ending inside a page: every token lands once, in order, and
+    nothing is written past the last token (the work is cut into equal runs
+    of tiles, so runs start and end inside sequences)."""
+    print(f"case: gather skewed {dtype} d{D} kind {kind}", flush=True)
+    rng = np.random.default_rng(D + kind)
+    seg_len = [0, 3000, 0, 0, 17, 1, 16, 0, 33] + [int(x) for x in rng.integers(0, 40, size=300)] + [0]
+    w = to_device(build_workload("skew", 3, 2, 2, D, dtype, seg_len, [[s] for s in range(len(seg_len))],
+                                 poison=False))
+    seqs = list(range(len(seg_len)))
+    out = _gather(w, seqs, kind)
+    exp = _expected(w, seqs, kind)
+    n = exp.shape[0]
+    assert np.array_equal(_bits(out[:n]), _bits(exp))
+    assert (out[n:].float() == 7.0).all(), "gather wrote past the last token"
