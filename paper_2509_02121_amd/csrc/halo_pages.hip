@@ -42,6 +42,26 @@ struct GatherArgs {
   int32_t v_layout;
 };
 
+// The last index s < n with indptr[s] <= x, for a nondecreasing indptr with
+// indptr[0] <= x (wave-uniform x): the wave compares 64 evenly spaced
+// entries at once and keeps the bracket that holds the answer, so up to 4095
+// entries take two rounds of loads where a binary search takes twelve.
+__device__ __forceinline__ int last_at_or_below(const int32_t* indptr, int n, int64_t x, int lane) {
+  int lo = 0, len = n;
+  while (len > 64) {
+    const int stride = (len + 63) / 64;
+    const int off = lane * stride;
+    const bool hit = off < len && indptr[lo + off] <= x;
+    const uint64_t mask = __ballot(hit);
+    const int top = 63 - __clzll(mask);          // lane 0 always hits
+    lo += top * stride;
+    len = min(stride, len - top * stride);
+  }
+  const bool hit = lane < len && indptr[lo + lane] <= x;
+  const uint64_t mask = __ballot(hit);
+  return lo + 63 - __clzll(mask);
+}
+
 // The (page slot, head) tiles of all sequences, in order, are cut into equal
 // contiguous runs, one per wave, so a few long sequences among many short
 // ones spread over the whole grid. A wave finds the sequence of its first
@@ -74,16 +94,7 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
   const int64_t t_begin = w_id * per;
   const int64_t t_end = min(total, t_begin + per);
   if (t_begin >= t_end) return;
-  int seq;
-  {
-    const int64_t slot = t_begin / H;
-    int lo = 0, hi = a.num_seqs - 1;     // last sequence whose first slot <= slot
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.seq_page_indptr[mid] <= slot) lo = mid; else hi = mid - 1;
-    }
-    seq = lo;
-  }
+  int seq = last_at_or_below(a.seq_page_indptr, a.num_seqs, t_begin / H, lane);
   int base = a.seq_page_indptr[seq], next = a.seq_page_indptr[seq + 1];
   for (int64_t tl = t_begin; tl < t_end; ++tl) {
     const int slot = (int)(tl / H), h = (int)(tl % H);
