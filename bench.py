@@ -310,7 +310,7 @@ def main():
                           "copy_gbps_read_plus_write": round(2 * n * 4 / (ms / 1e3) / 1e9, 1)}), flush=True)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
+        print(f"bench.py measures one GPU only (the library has no multi-GPU path); got --gpus {args.gpus}",
               file=sys.stderr)
         sys.exit(2)
 
