@@ -173,6 +173,37 @@ def _dtype_code(dtype):
     raise ValueError(f"unsupported dtype {dtype}")
 
 
+def _torch_dtype(code):
+    import torch
+    return {HALO_F32: torch.float32, HALO_BF16: torch.bfloat16}[code]
+
+
+def _gpu(t, name, dtype=None, min_numel=None):
+    """Check that t is a contiguous GPU tensor (of dtype, with at least
+    min_numel elements): the C ABI takes raw pointers, so a strided view, a
+    host tensor or another element type would be read as garbage."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs at least {min_numel}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    return t
+
+
+def _page_lists(page_ids, seq_page_indptr):
+    """Check the int32 page lists; returns the number of sequences."""
+    import torch
+    _gpu(seq_page_indptr, "seq_page_indptr", torch.int32, 1)
+    _gpu(page_ids, "page_ids", torch.int32)
+    return int(seq_page_indptr.numel() - 1)
+
+
 def make_params(num_q_heads, num_kv_heads, head_dim, kv_dtype, num_pool_pages, sm_scale,
                 out_dtype=None, page_size=16):
     """AttnParams from Python values (dtypes as torch dtypes)."""
@@ -327,7 +358,22 @@ def _stream_handle(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _check_run(plan, device_meta, q, k_pool, v_pool, o, lse, workspace):
+    import torch
+    kv = _torch_dtype(plan.params.kv_dtype)
+    _gpu(device_meta, "device_meta")
+    _gpu(q, "q", kv)
+    _gpu(k_pool, "k_pool", kv)
+    _gpu(v_pool, "v_pool", kv)
+    _gpu(o, "o", _torch_dtype(plan.params.out_dtype), q.numel())
+    if lse is not None:
+        _gpu(lse, "lse", torch.float32, q.numel() // max(1, plan.params.head_dim))
+    if workspace is not None:
+        _gpu(workspace, "workspace")
+
+
 def _run(fn, plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream):
+    _check_run(plan, device_meta, q, k_pool, v_pool, o, lse, workspace)
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(fn(plan._handle, device_meta.data_ptr(), q.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(),
@@ -345,10 +391,48 @@ def prefix_attn_prefill(plan, device_meta, q, k_pool, v_pool, o, lse, workspace,
     _run(_LIB.halo_prefix_attn_prefill, plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream)
 
 
+def _check_gather(pool, params, page_ids, seq_page_indptr, seq_len, out_token_offset, out, error_flag):
+    import torch
+    kv = _torch_dtype(params.kv_dtype)
+    n = _page_lists(page_ids, seq_page_indptr)
+    _gpu(pool, "pool", kv)
+    _gpu(seq_len, "seq_len", torch.int32, n)
+    _gpu(out_token_offset, "out_token_offset", torch.int64, n)
+    _gpu(out, "out", kv)
+    if error_flag is not None:
+        _gpu(error_flag, "error_flag", torch.int32, 1)
+
+
+def _check_scatter(pools, params, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset, srcs,
+                   error_flag):
+    import torch
+    kv = _torch_dtype(params.kv_dtype)
+    n = _page_lists(page_ids, seq_page_indptr)
+    for i, t in enumerate(pools):
+        _gpu(t, f"pool {i}", kv)
+    for i, t in enumerate(srcs):
+        _gpu(t, f"input {i}", kv)
+    _gpu(seq_start, "seq_start", torch.int32, n)
+    _gpu(seq_count, "seq_count", torch.int32, n)
+    _gpu(in_token_offset, "in_token_offset", torch.int64, n)
+    if error_flag is not None:
+        _gpu(error_flag, "error_flag", torch.int32, 1)
+
+
+def _check_copy(pool, params, src_pages, dst_pages, error_flag):
+    import torch
+    _gpu(pool, "pool", _torch_dtype(params.kv_dtype))
+    _gpu(src_pages, "src_pages", torch.int32)
+    _gpu(dst_pages, "dst_pages", torch.int32, src_pages.numel())
+    if error_flag is not None:
+        _gpu(error_flag, "error_flag", torch.int32, 1)
+
+
 def kv_page_gather(pool, params, pool_kind, page_ids, seq_page_indptr, seq_len, out_token_offset,
                    out, error_flag=None, stream=None):
     """halo_kv_page_gather on torch tensors (int arrays on the GPU)."""
     load_library()
+    _check_gather(pool, params, page_ids, seq_page_indptr, seq_len, out_token_offset, out, error_flag)
     _check(_LIB.halo_kv_page_gather(pool.data_ptr(), ctypes.byref(params), int(pool_kind),
                                     page_ids.data_ptr(), seq_page_indptr.data_ptr(), seq_len.data_ptr(),
                                     out_token_offset.data_ptr(), int(seq_page_indptr.numel() - 1),
@@ -361,6 +445,8 @@ def kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq_star
                     in_token_offset, src, error_flag=None, stream=None):
     """halo_kv_page_scatter on torch tensors (int arrays on the GPU)."""
     load_library()
+    _check_scatter([pool], params, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset, [src],
+                   error_flag)
     _check(_LIB.halo_kv_page_scatter(pool.data_ptr(), ctypes.byref(params), int(pool_kind),
                                      page_ids.data_ptr(), seq_page_indptr.data_ptr(), seq_start.data_ptr(),
                                      seq_count.data_ptr(), in_token_offset.data_ptr(),
@@ -371,6 +457,8 @@ def kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq_star
 
 def _scatter_kv_args(k_pool, v_pool, params, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset,
                      k_src, v_src, error_flag, stream):
+    _check_scatter([k_pool, v_pool], params, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset,
+                   [k_src, v_src], error_flag)
     return (k_pool.data_ptr(), v_pool.data_ptr(), ctypes.byref(params), page_ids.data_ptr(),
             seq_page_indptr.data_ptr(), seq_start.data_ptr(), seq_count.data_ptr(), in_token_offset.data_ptr(),
             int(seq_page_indptr.numel() - 1), k_src.data_ptr(), v_src.data_ptr(),
@@ -389,6 +477,7 @@ def kv_page_scatter_kv(k_pool, v_pool, params, page_ids, seq_page_indptr, seq_st
 def kv_page_copy(pool, params, src_pages, dst_pages, error_flag=None, stream=None):
     """halo_kv_page_copy on torch tensors (int arrays on the GPU)."""
     load_library()
+    _check_copy(pool, params, src_pages, dst_pages, error_flag)
     _check(_LIB.halo_kv_page_copy(pool.data_ptr(), ctypes.byref(params), src_pages.data_ptr(),
                                   dst_pages.data_ptr(), int(src_pages.numel()),
                                   error_flag.data_ptr() if error_flag is not None else None,
@@ -399,6 +488,7 @@ def bind_kv_page_gather(pool, params, pool_kind, page_ids, seq_page_indptr, seq_
                         error_flag=None, stream=None):
     """kv_page_gather as a zero-argument callable (see bind_kv_page_scatter)."""
     load_library()
+    _check_gather(pool, params, page_ids, seq_page_indptr, seq_len, out_token_offset, out, error_flag)
     args = (pool.data_ptr(), ctypes.byref(params), int(pool_kind), page_ids.data_ptr(), seq_page_indptr.data_ptr(),
             seq_len.data_ptr(), out_token_offset.data_ptr(), int(seq_page_indptr.numel() - 1), out.data_ptr(),
             error_flag.data_ptr() if error_flag is not None else None, _stream_handle(stream))
@@ -417,6 +507,8 @@ def bind_kv_page_scatter(pool, params, pool_kind, page_ids, seq_page_indptr, seq
     pointer converted once (for tight timing loops); the tensors and params
     must stay alive while it is used."""
     load_library()
+    _check_scatter([pool], params, page_ids, seq_page_indptr, seq_start, seq_count, in_token_offset, [src],
+                   error_flag)
     args = (pool.data_ptr(), ctypes.byref(params), int(pool_kind), page_ids.data_ptr(),
             seq_page_indptr.data_ptr(), seq_start.data_ptr(), seq_count.data_ptr(),
             in_token_offset.data_ptr(), int(seq_page_indptr.numel() - 1), src.data_ptr(),
@@ -448,6 +540,7 @@ def bind_kv_page_scatter_kv(k_pool, v_pool, params, page_ids, seq_page_indptr, s
 def bind_kv_page_copy(pool, params, src_pages, dst_pages, error_flag=None, stream=None):
     """kv_page_copy as a zero-argument callable (see bind_kv_page_scatter)."""
     load_library()
+    _check_copy(pool, params, src_pages, dst_pages, error_flag)
     args = (pool.data_ptr(), ctypes.byref(params), src_pages.data_ptr(), dst_pages.data_ptr(),
             int(src_pages.numel()), error_flag.data_ptr() if error_flag is not None else None,
             _stream_handle(stream))
@@ -490,6 +583,7 @@ class PrefixAttention:
         The tensors must stay alive while the callable is used."""
         fn = _LIB.halo_prefix_attn_prefill if self.plan.is_prefill else _LIB.halo_prefix_attn_decode
         ws = self.workspace
+        _check_run(self.plan, self.meta, q, k_pool, v_pool, o, lse, ws)
         args = (self.plan._handle, self.meta.data_ptr(), q.data_ptr(), k_pool.data_ptr(),
                 v_pool.data_ptr(), o.data_ptr(), lse.data_ptr() if lse is not None else None,
                 ws.data_ptr() if ws is not None else None,

@@ -353,3 +353,31 @@ def test_run_calls_reject_bad_arguments_without_touching_the_gpu(lib):
     assert rc == halo.HALO_ERR_INVALID_ARGUMENT
     rc = lib.halo_kv_page_copy(fake, ctypes.byref(params), fake, fake, 0, None, None)
     assert rc == halo.HALO_OK
+
+
+def test_binding_rejects_tensors_the_abi_would_misread():
+    """The binding checks what the C ABI cannot: host tensors, strided views
+    and wrong element types raise before anything is launched."""
+    import torch
+    halo.load_library()
+    params = halo.make_params(4, 2, 64, torch.bfloat16, 8, 0.125)
+    host = torch.zeros(8 * 2 * 16 * 64, dtype=torch.bfloat16)
+    i32 = torch.zeros(4, dtype=torch.int32)
+    i64 = torch.zeros(4, dtype=torch.int64)
+    with pytest.raises(ValueError, match="on the GPU"):
+        halo.kv_page_gather(host, params, halo.HALO_POOL_K, i32, i32, i32, i64, host)
+    with pytest.raises(ValueError, match="on the GPU"):
+        halo.kv_page_copy(host, params, i32, i32)
+    with pytest.raises(ValueError, match="on the GPU"):
+        halo.kv_page_scatter_kv(host, host, params, i32, i32, i32, i32, i64, host, host)
+    with pytest.raises(TypeError):
+        halo.kv_page_scatter(host.numpy().view("int16"), params, halo.HALO_POOL_V, i32, i32, i32, i32, i64, host)
+    # each rule of the check, on host tensors (layout and type come before the device)
+    with pytest.raises(ValueError, match="contiguous"):
+        halo._gpu(host.view(-1, 64).t(), "pool")
+    with pytest.raises(ValueError, match="int32"):
+        halo._gpu(i64, "page_ids", torch.int32)
+    with pytest.raises(ValueError, match="at least 5"):
+        halo._gpu(i32, "seq_len", torch.int32, 5)
+    with pytest.raises(ValueError, match="on the GPU"):
+        halo._gpu(i32, "seq_len", torch.int32, 4)
