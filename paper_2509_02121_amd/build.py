@@ -18,6 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libhalo_attn.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
+DRIVER_SRC = os.path.join(ROOT, "tests", "abi_driver", "decode.cpp")
+DRIVER_BIN = os.path.join(ROOT, "tests", "abi_driver", "decode")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -63,6 +65,11 @@ def build(verbose=True):
         out_tmp = LIB_PATH + ".tmp"
         _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, forest_o, kern_o, pages_o, "-o", out_tmp])
         os.replace(out_tmp, LIB_PATH)
+        # the C-ABI driver of the tests (host code against the built library)
+        _run(["g++", "-std=c++17", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE,
+              "-I", "/opt/rocm/include", DRIVER_SRC, "-o", DRIVER_BIN, "-L", PKG, "-lhalo_attn",
+              "-L", "/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,$ORIGIN/../../paper_2509_02121_amd",
+              "-Wl,-rpath,/opt/rocm/lib"])
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
     return LIB_PATH
