@@ -31,7 +31,10 @@ relative error):
 in which the prefix-caching discount is explicit: a prefix shared by G
 requests contributes its K/V bytes once, not G times. Checks: T grows with S
 and with P; at fixed P and S, a larger group is not slower; the fit's
-relative error. One JSON object is printed (and written with --json).
+relative error, on the grid and on held-out workloads predicted from their
+forests (forest_features works on any batch, e.g. one built from token ids
+by halo_prefix_tree_build). One JSON object is printed (and written with
+--json).
 """
 
 import argparse
@@ -50,6 +53,9 @@ ELT = 2        # bf16
 MONOTONE_TOL = 0.03
 
 DECODE_GRID = dict(requests=[64], group=[1, 4, 16, 64], prefix=[0, 512, 2048, 8192], suffix=[64, 256, 1024])
+# large batches in few sharing groups (the regime of serving many replicas of
+# one workflow); kept small so the sweep stays within seconds per point
+DECODE_GRID_WIDE = dict(requests=[512], group=[8, 64, 512], prefix=[2048, 8192], suffix=[64, 256])
 PREFILL_GRID = dict(requests=[8, 32], group=["1", "all"], prefix=[0, 1024, 4096], suffix=[128, 512])
 QUICK_DECODE = dict(requests=[32], group=[1, 32], prefix=[0, 1024], suffix=[64, 1024])
 QUICK_PREFILL = dict(requests=[8], group=["all"], prefix=[0, 1024], suffix=[128, 256])
@@ -75,6 +81,47 @@ def features(kind, requests, group, prefix, suffix):
         pairs = requests * (suffix * prefix + suffix * (suffix + 1) // 2)
         split = 0.0
     return [1.0, float(kv_tokens * tok_bytes), float(pairs * HQ), float(rows * HQ), split, float(shared_bytes)]
+
+
+def forest_features(seg_len, req_paths, q_len=None, num_q_heads=None, num_kv_heads=None, head_dim=None, elt=ELT):
+    """The model's features for any batch given as a forest (segment lengths
+    and per-request paths, e.g. from halo_prefix_tree_build on token ids;
+    q_len for a prefill whose last segment per path is the chunk). Shared
+    segments (on more than one path) count once in the K/V bytes: the
+    prefix-caching discount of the cost model."""
+    num_q_heads = HQ if num_q_heads is None else num_q_heads
+    num_kv_heads = HKV if num_kv_heads is None else num_kv_heads
+    head_dim = D if head_dim is None else head_dim
+    seg_len = [int(x) for x in seg_len]
+    tok_bytes = 2 * num_kv_heads * head_dim * elt
+    refs = [0] * len(seg_len)
+    for path in req_paths:
+        for s in path:
+            refs[s] += 1
+    kv_bytes = sum(seg_len) * tok_bytes
+    shared_bytes = sum(n for n, r in zip(seg_len, refs) if r > 1) * tok_bytes
+    rows = pairs = 0
+    split = 0.0
+    for r, path in enumerate(req_paths):
+        keys = sum(seg_len[s] for s in path)
+        if q_len is None:
+            rows += 1
+            pairs += keys
+            private = sum(seg_len[s] for s in path if refs[s] == 1)
+            if keys > private or private > 1024:
+                split = 1.0
+        else:
+            n = int(q_len[r])
+            rows += n
+            pairs += n * (keys - n) + n * (n + 1) // 2
+    return [1.0, float(kv_bytes), float(pairs * num_q_heads), float(rows * num_q_heads), split,
+            float(shared_bytes)]
+
+
+def predict_forest(coef, seg_len, req_paths, q_len=None, **shape):
+    """Predicted latency (us) of one call on a batch given as a forest."""
+    import numpy as np
+    return float(np.dot(coef, forest_features(seg_len, req_paths, q_len, **shape)))
 
 
 def fit(points):
@@ -127,7 +174,16 @@ def _measure(kind, requests, group, prefix, suffix, calls, seed):
     q_len = None if kind == "decode" else np.full(requests, suffix, dtype=np.int32)
     w = build_workload(f"cal_{kind}", seed, HQ, HKV, D, torch.bfloat16, seg_len, paths, q_len,
                        value_scale=0.5, device="cuda")
-    params = halo.make_params(HQ, HKV, D, torch.bfloat16, w.num_pool_pages, w.scale, torch.bfloat16)
+    return _time_workload(w, calls)
+
+
+def _time_workload(w, calls):
+    """Median of single calls on a workload (inputs rotated past the
+    Infinity Cache)."""
+    import torch
+    from paper_2509_02121_amd import halo
+    params = halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages, w.scale,
+                              w.dtype)
     runner = halo.PrefixAttention(params, w.forest_csr(), "cuda")
     pool_bytes = (w.k_pool.numel() + w.v_pool.numel()) * ELT
     n_rep = max(1, min(16, -(-4 * MALL_BYTES // max(pool_bytes, 1))))
@@ -169,6 +225,32 @@ def run(grids, calls=50, log=print):
     return points
 
 
+HELD_OUT = ("llama8b_decode", "two_level_tree_decode", "llama70b_batch_decode", "chunked_prefill")
+
+
+def held_out(summary, calls=50, log=print):
+    """Measure the named workloads of the calibrated head shape (forests the
+    grid does not contain) and compare with the fitted model's prediction
+    from their forests. Curves are per model shape, as the paper keeps them
+    per model and hardware configuration."""
+    from workloads import make_config
+    out = []
+    for name in HELD_OUT:
+        w = make_config(name, device="cuda")
+        if (w.num_q_heads, w.num_kv_heads, w.head_dim) != (HQ, HKV, D):
+            del w
+            continue                   # curves are per model shape
+        kind = "prefill" if w.is_prefill else "decode"
+        coef = list(summary[kind]["coef"].values())
+        pred = predict_forest(coef, w.seg_len, w.req_paths, w.q_len, num_q_heads=w.num_q_heads,
+                              num_kv_heads=w.num_kv_heads, head_dim=w.head_dim)
+        us = _time_workload(w, calls)
+        out.append(dict(workload=name, kind=kind, us=round(us, 2), predicted_us=round(pred, 2),
+                        rel_err=round((pred - us) / us, 4)))
+        log(f"held out {name}: {us:.1f} us measured, {pred:.1f} us predicted")
+    return out
+
+
 def summarize(points):
     out = {"model": "T_us = c0 + c_kv*kv_bytes + c_pair*pairs_x_hq + c_row*rows_x_hq + c_split*split "
                     "+ c_shared*shared_kv_bytes",
@@ -189,7 +271,7 @@ def summarize(points):
 
 
 def to_markdown(summary, command):
-    lines = ["# Attention latency calibration (decode step and chunked prefill)", "",
+    lines = [f"# Attention latency calibration (decode step and chunked prefill), {HQ}/{HKV} heads", "",
              "Command (repository root, one MI355X):", "", f"    {command}", "",
              f"Heads {HQ}/{HKV}, d {D}, bf16. R requests, G sharing each prefix of P tokens, S private "
              "tokens each (decode) or an S-token causal chunk each (prefill). Median of single calls.", "",
@@ -203,6 +285,12 @@ def to_markdown(summary, command):
             lines.append(f"- {kind}: {json.dumps(s['coef'])}; effective K/V streaming rate "
                          f"{s['effective_kv_tbps']} TB/s; relative error max {s['max_rel_err']}, "
                          f"median {s['median_rel_err']}.")
+    if summary.get("held_out"):
+        lines += ["", "Held-out workloads (forests outside the grid), measured and predicted from their forests "
+                  "(`forest_features`):", "", "| workload | measured (us) | predicted (us) | error |",
+                  "|---|---|---|---|"]
+        for h in summary["held_out"]:
+            lines.append(f"| {h['workload']} | {h['us']} | {h['predicted_us']} | {h['rel_err']:+.1%} |")
     v = summary["monotonicity_violations"]
     lines += ["", f"Monotonicity violations (tolerance {MONOTONE_TOL:.0%}): " + ("none." if not v else ""), ""]
     lines += [f"- {x}" for x in v]
@@ -210,25 +298,33 @@ def to_markdown(summary, command):
 
 
 def main():
+    global HQ, HKV
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--quick", action="store_true", help="a few points only")
     ap.add_argument("--calls", type=int, default=50)
     ap.add_argument("--json", default=None)
     ap.add_argument("--md", default=None)
+    ap.add_argument("--q-heads", type=int, default=HQ)
+    ap.add_argument("--kv-heads", type=int, default=HKV)
     args = ap.parse_args()
+    HQ, HKV = args.q_heads, args.kv_heads
     import torch
     from paper_2509_02121_amd import halo
     halo.load_library(require_gpu=True)
     torch.cuda.set_device(0)
     grids = [("decode", QUICK_DECODE), ("prefill", QUICK_PREFILL)] if args.quick else \
-        [("decode", DECODE_GRID), ("prefill", PREFILL_GRID)]
+        [("decode", DECODE_GRID), ("decode", DECODE_GRID_WIDE), ("prefill", PREFILL_GRID)]
     points = run(grids, args.calls, log=lambda m: print(m, flush=True))
     summary = summarize(points)
+    if not args.quick:
+        summary["held_out"] = held_out(summary, args.calls, log=lambda m: print(m, flush=True))
     if args.json:
         with open(args.json, "w") as f:
             json.dump(summary, f, indent=1)
     if args.md:
-        cmd = "python -u calibrate.py" + (" --quick" if args.quick else "") + (f" --md {args.md}" if args.md else "")
+        cmd = "python -u calibrate.py" + (" --quick" if args.quick else "") + \
+            (f" --q-heads {HQ} --kv-heads {HKV}" if (HQ, HKV) != (32, 8) else "") + \
+            (f" --md {args.md}" if args.md else "") + (f" --json {args.json}" if args.json else "")
         with open(args.md, "w") as f:
             f.write(to_markdown(summary, cmd))
     print(json.dumps({k: v for k, v in summary.items() if k != "points"}), flush=True)

@@ -49,3 +49,29 @@ def test_monotonicity_check_flags_planted_violations():
     pts[("decode", 64, 16, 512, 64)] = 11.0           # larger group, slower: planted
     bad = calibrate.check_monotone(pts)
     assert any("S 256->1024" in b for b in bad) and any("G 4->16" in b for b in bad)
+
+
+def test_forest_features_agree_with_the_grid_features():
+    """A uniform forest (R requests, groups of G on P-token prefixes, S
+    private tokens) gives the grid point's features, decode and prefill."""
+    for (r, g, p, s) in [(8, 4, 100, 10), (8, 1, 100, 10), (8, 8, 0, 10), (6, 3, 1000, 100)]:
+        n_pre = r // g if p > 0 else 0
+        seg_len = [p] * n_pre + [s] * r
+        paths = [([i // g] if p > 0 else []) + [n_pre + i] for i in range(r)]
+        assert calibrate.forest_features(seg_len, paths) == calibrate.features("decode", r, g, p, s)
+        assert calibrate.forest_features(seg_len, paths, [s] * r)[:4] == \
+            calibrate.features("prefill", r, g, p, s)[:4]
+
+
+def test_forest_prediction_from_token_ids_discounts_shared_prefixes():
+    """Through the prefix-tree builder: the same prompts predicted with their
+    shared prefix counted once are cheaper than the flattened batch."""
+    from paper_2509_02121_amd import halo
+    rng = np.random.default_rng(5)
+    prefix = rng.integers(0, 1000, size=2048).tolist()
+    prompts = [prefix + rng.integers(0, 1000, size=int(n)).tolist() for n in rng.integers(64, 512, size=64)]
+    tree = halo.PrefixTree(prompts, 16)
+    coef = [3.0, 1.4e-7, 1.3e-6, 2.9e-3, 4.6, 2.4e-8]
+    shared = calibrate.predict_forest(coef, tree.seg_len, tree.paths())
+    flat = calibrate.predict_forest(coef, [len(p) for p in prompts], [[r] for r in range(len(prompts))])
+    assert tree.distinct_tokens < tree.prompt_tokens and shared < flat
