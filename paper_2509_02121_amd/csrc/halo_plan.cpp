@@ -222,16 +222,25 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
 
   if (!prefill) {
     const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, kMaxSpanKeys) / 32 * 32;
-    // Private chunks: 1024 keys when that still leaves >= 512 items (two per
-    // CU; fewer partials to write and merge), else 512.
-    int64_t items_at_1024 = 0;
-    for (int r = 0; r < R; ++r) {
-      int64_t priv = 0;
-      for (int32_t i = path_begin(r); i < path_end(r); ++i)
-        if (refs[f.req_seg_ids[i]] == 1) priv += f.seg_len[f.req_seg_ids[i]];
-      items_at_1024 += ceil_div(priv, 1024) * Hkv;
-    }
-    const int kc_private_default = items_at_1024 >= 2 * kNumCUs ? 1024 : 512;
+    // Private chunks: the longest of 1024, 512 and 256 keys that still
+    // leaves >= 3 items per CU (longer chunks write and merge fewer
+    // partials; with fewer items a CU has too few loads in flight), else 256.
+    auto private_items = [&](int64_t kc) {
+      int64_t n = 0;
+      for (int r = 0; r < R; ++r) {
+        int64_t priv = 0;
+        for (int32_t i = path_begin(r); i < path_end(r); ++i)
+          if (refs[f.req_seg_ids[i]] == 1) priv += f.seg_len[f.req_seg_ids[i]];
+        n += ceil_div(priv, kc) * Hkv;
+      }
+      return n;
+    };
+    int kc_private_default = 256;
+    for (int kc : {1024, 512})
+      if (private_items(kc) >= 3 * kNumCUs) {
+        kc_private_default = kc;
+        break;
+      }
     const int kc_private = env_int("HALO_KC_PRIVATE", kc_private_default, 32, kMaxSpanKeys) / 32 * 32;
     for (int r = 0; r < R; ++r) {
       int64_t keys = 0;
