@@ -148,6 +148,11 @@ __device__ __forceinline__ f32x8_t to_frag(const float (&p)[8], f32x8_t*) {
 __device__ __forceinline__ void store4(float* dst, f32x4_t v) {
   *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
 }
+// Partial results are read once, by the merge launch that follows on
+// another XCD: write them past the caches.
+__device__ __forceinline__ void store4_nt(float* dst, f32x4_t v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<f32x4_t*>(dst));
+}
 __device__ __forceinline__ void store4(__bf16* dst, f32x4_t v) {
   typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
   bf16x4_t r;
@@ -505,8 +510,8 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
       const int64_t prow = row.slot;
       float* dst = a.part_o + prow * D + 4 * grp;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) store4(dst + 16 * b, acc[b] * inv);
-      if (grp == 0) a.part_lse[prow] = lse2;
+      for (int b = 0; b < NB; ++b) store4_nt(dst + 16 * b, acc[b] * inv);
+      if (grp == 0) __builtin_nontemporal_store(lse2, a.part_lse + prow);
     }
   } else if (has_row) {
     TO* dst = static_cast<TO*>(a.o) + (int64_t)row.q_row * D + 4 * grp;
@@ -561,11 +566,11 @@ __device__ __forceinline__ void merge_split(const AttnArgs& a, const Item& it, c
     for (int q = 0; q < kMaxSplit; ++q)
       if (q < split) o += sq[q] * *reinterpret_cast<const f32x4_t*>(red0 + q * kRed + (b * 64 + lane) * 4);
     o *= inv;
-    if (it.part_base >= 0) store4(a.part_o + slot * D + 16 * b + 4 * grp, o);
+    if (it.part_base >= 0) store4_nt(a.part_o + slot * D + 16 * b + 4 * grp, o);
     else store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 16 * b + 4 * grp, o);
   }
   if (part == 0 && grp == 0) {
-    if (it.part_base >= 0) a.part_lse[slot] = lse2;
+    if (it.part_base >= 0) __builtin_nontemporal_store(lse2, a.part_lse + slot);
     else if (a.lse) a.lse[q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
   }
 }
@@ -991,8 +996,8 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
       for (int b = 0; b < NO; ++b)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          store4(dst + 32 * b + 8 * q, f32x4_t{acc[b][4 * q], acc[b][4 * q + 1], acc[b][4 * q + 2], acc[b][4 * q + 3]} * inv);
-      if (h == 0) a.part_lse[prow] = lse2;
+          store4_nt(dst + 32 * b + 8 * q, f32x4_t{acc[b][4 * q], acc[b][4 * q + 1], acc[b][4 * q + 2], acc[b][4 * q + 3]} * inv);
+      if (h == 0) __builtin_nontemporal_store(lse2, a.part_lse + prow);
     } else {
       TO* dst = static_cast<TO*>(a.o) + (int64_t)row.q_row * D + 4 * h;
 #pragma unroll
