@@ -309,8 +309,12 @@ halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st
  *   rows:   n_rows   x {q_row = token * num_q_heads + head, chunk position,
  *                       merge entry or -1, partial slot or -1}
  *   merge_rows [n_merge], merge_indptr [n_merge + 1], merge_parts: the
- *   partial slots combined into each listed output row; the slots of entry
- *   m are merge_indptr[m] .. merge_indptr[m + 1] - 1.
+ *   workspace slots of the partials combined into each listed output row,
+ *   entry m's at merge_parts[merge_indptr[m] .. merge_indptr[m + 1] - 1].
+ *   With k0 = min(8, most partials of an entry), entry m's k-th partial
+ *   (k < k0) sits at slot k * n_merge + m, so the merge finds it without
+ *   reading the list; later partials take consecutive slots after
+ *   k0 * n_merge.
  * *image stays valid until halo_plan_destroy. */
 typedef struct {
   uint64_t seg_page_off, seg_len, page_ids, items, wide_items, spans, rows;

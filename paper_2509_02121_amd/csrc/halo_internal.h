@@ -25,6 +25,9 @@ constexpr int kNumCUs = 256;
 constexpr int kItemOverheadKeys = 64;
 // Keys consumed per inner step: two pages of 16 (one K=32 MFMA for P*V).
 constexpr int kKeysPerStep = 32;
+// Partials per merge entry that sit at fixed workspace slots (k * n_merge + m)
+// and that the merge kernel loads together with the entry's metadata.
+constexpr int kMergeK0 = 8;
 
 // One work item: up to 16 query rows (narrow, one wavefront) or up to 256
 // (wide, one workgroup) against a list of key spans. 64 bytes, read by the
@@ -127,6 +130,8 @@ struct halo_plan {
   int32_t n_merge_parts = 0;
   int32_t n_pages = 0;
   int64_t n_part_rows = 0;
+  int64_t n_part_slots = 0;     // workspace slots (>= n_part_rows)
+  int32_t merge_k0 = 0;         // partials per merge entry at slots k * n_merge + m
   int64_t distinct_kv_tokens = 0;
   int64_t visible_pairs = 0;
   size_t workspace_bytes = 0;

@@ -1055,53 +1055,58 @@ struct MergeArgs {
   const float* part_lse;
   const int32_t* merge_rows;
   const int32_t* merge_indptr;
+  const int32_t* merge_parts;
   void* o;
   float* lse;
   int32_t n_merge;
+  int32_t k0;   // partials of entry r at slots k * n_merge + r for k < k0
 };
 
 // Output rows whose keys were split over several items. Partials hold the
 // normalized o_i and lse_i (log2) of disjoint key sets:
 //   M = max_i lse_i,  w_i = 2^(lse_i - M),  O = sum w_i o_i / sum w_i,
 //   LSE = (M + log2 sum w_i) * ln 2
-// which is exact in real arithmetic (shared == unshared, §3 "Scope"). The
-// partials of merge entry r sit in slots merge_indptr[r] ..
-// merge_indptr[r + 1] - 1, so a row needs one metadata load before its
-// partials. One group of D/4 threads per row, 4 dims per thread; the LSEs
-// and partials of up to 8 slots are fetched together so the loads overlap.
+// which is exact in real arithmetic (shared == unshared, §3 "Scope").
+// Merge entry r has merge_indptr[r + 1] - merge_indptr[r] partials; its
+// first k0 sit at slots k * n_merge + r, so they are loaded together with
+// the entry's metadata (one round trip); slots past the entry's count are
+// read too (in bounds: the workspace holds k0 * n_merge of them) and dropped
+// by integer selects, which fast math cannot fold away whatever bits they
+// hold. Further partials (entries with more than k0) come from the slot
+// list merge_parts. One group of D/4 threads per row, 4 dims per thread.
 template <int D, typename TO>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
   constexpr int TPR = D / 4;
   constexpr int RPB = 256 / TPR;
-  constexpr int kBatch = 8;
+  constexpr int kBatch = kMergeK0;
   const int r = blockIdx.x * RPB + threadIdx.x / TPR;
   const int t = threadIdx.x % TPR;
   if (r >= a.n_merge) return;
   const int q_row = a.merge_rows[r];
   const int p0 = a.merge_indptr[r], p1 = a.merge_indptr[r + 1];
+  uint32_t lb[kBatch];
+  uint4 vb[kBatch];
+#pragma unroll
+  for (int k = 0; k < kBatch; ++k) {
+    if (k < a.k0) {
+      const int64_t slot = (int64_t)k * a.n_merge + r;
+      lb[k] = __builtin_bit_cast(uint32_t, a.part_lse[slot]);
+      vb[k] = *reinterpret_cast<const uint4*>(a.part_o + slot * D + 4 * t);
+    } else {
+      lb[k] = 0;
+      vb[k] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
   float mx = kNegInf;
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
   // online over batches of parts: rescale when the running max moves
-  for (int pb = p0; pb < p1; pb += kBatch) {
-    int pid[kBatch];
-    float l[kBatch];
-#pragma unroll
-    for (int k = 0; k < kBatch; ++k) pid[k] = pb + k < p1 ? pb + k : -1;
-#pragma unroll
-    for (int k = 0; k < kBatch; ++k) l[k] = pid[k] >= 0 ? a.part_lse[pid[k]] : kNegInf;
-    f32x4_t v[kBatch];
-#pragma unroll
-    for (int k = 0; k < kBatch; ++k) {
-      const float4 x = pid[k] >= 0 ? *reinterpret_cast<const float4*>(a.part_o + (int64_t)pid[k] * D + 4 * t)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
-      v[k] = f32x4_t{x.x, x.y, x.z, x.w};
-    }
+  auto fold = [&](const float (&l)[kBatch], const f32x4_t (&v)[kBatch]) {
     float bm = kNegInf;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) bm = fmaxf(bm, l[k]);
     const float m_new = fmaxf(mx, bm);
-    if (m_new == kNegInf) continue;
+    if (m_new == kNegInf) return;
     const float alpha = mx == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mx - m_new);
     acc *= alpha;
     wsum *= alpha;
@@ -1112,6 +1117,37 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
       acc += w * v[k];
     }
     mx = m_new;
+  };
+  {
+    const int n = p1 - p0;
+    const uint32_t neg_inf_bits = 0xff800000u;
+    float l[kBatch];
+    f32x4_t v[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const bool keep = k < n && k < a.k0;
+      l[k] = __builtin_bit_cast(float, keep ? lb[k] : neg_inf_bits);
+      const uint4 x = keep ? vb[k] : make_uint4(0u, 0u, 0u, 0u);
+      v[k] = f32x4_t{__builtin_bit_cast(float, x.x), __builtin_bit_cast(float, x.y),
+                     __builtin_bit_cast(float, x.z), __builtin_bit_cast(float, x.w)};
+    }
+    fold(l, v);
+  }
+  for (int pb = p0 + a.k0; pb < p1; pb += kBatch) {
+    int pid[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) pid[k] = pb + k < p1 ? a.merge_parts[pb + k] : -1;
+    float l[kBatch];
+    f32x4_t v[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) l[k] = pid[k] >= 0 ? a.part_lse[pid[k]] : kNegInf;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const float4 x = pid[k] >= 0 ? *reinterpret_cast<const float4*>(a.part_o + (int64_t)pid[k] * D + 4 * t)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+      v[k] = f32x4_t{x.x, x.y, x.z, x.w};
+    }
+    fold(l, v);
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
   store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 4 * t, acc * inv);
@@ -1179,9 +1215,9 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
   const uint8_t* m = static_cast<const uint8_t*>(device_meta);
   const int D = p.head_dim;
   float* part_o = static_cast<float*>(workspace);
-  float* part_lse = plan->n_part_rows
+  float* part_lse = plan->n_part_slots
                         ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
-                                                   align256((size_t)plan->n_part_rows * D * sizeof(float)))
+                                                   align256((size_t)plan->n_part_slots * D * sizeof(float)))
                         : nullptr;
   AttnArgs args{q, k_pool, v_pool, o, lse, part_o, part_lse,
                 reinterpret_cast<const int32_t*>(m + L.seg_page_off),
@@ -1198,7 +1234,8 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),
                   reinterpret_cast<const int32_t*>(m + L.merge_indptr),
-                  o, lse, plan->n_merge};
+                  reinterpret_cast<const int32_t*>(m + L.merge_parts),
+                  o, lse, plan->n_merge, plan->merge_k0};
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();   // clear any stale error of the caller
   const bool out_f32 = p.out_dtype == HALO_F32;

@@ -493,21 +493,40 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   // partial results (several, or one from an item that also holds
   // multi-part rows); the merge kernel combines them after the attention
   // kernels.
-  // The partials of one merge entry get consecutive workspace slots, so the
-  // merge reads a row's partials as one range.
+  // Workspace slots: the first k0 = min(kMergeK0, most partials of an entry)
+  // partials of merge entry m sit at slots k * n_merge + m, so the merge
+  // kernel finds them from m alone and loads them in the same round trip as
+  // the entry's metadata; partials past k0 take consecutive slots after
+  // k0 * n_merge. merge_parts lists every entry's slots in order.
   std::vector<int32_t> merge_rows, merge_indptr{0}, merge_parts;
+  int64_t n_slots = 0;
+  int32_t merge_k0 = 0;
   if (!prefill) {
     std::vector<int32_t> merge_of(n_q_rows * Hq, -1);
     std::vector<int32_t> slot_of_part(part_rows, -1);
+    size_t most = 0;
     for (int64_t qr = 0; qr < n_q_rows * Hq; ++qr) {
       if (row_parts[qr].empty()) continue;   // written by a final item
       merge_of[qr] = (int32_t)merge_rows.size();
       merge_rows.push_back((int32_t)qr);
-      for (int32_t pid : row_parts[qr]) {
-        slot_of_part[pid] = (int32_t)merge_parts.size();
-        merge_parts.push_back((int32_t)merge_parts.size());
+      most = std::max(most, row_parts[qr].size());
+    }
+    const int64_t nm = (int64_t)merge_rows.size();
+    merge_k0 = (int32_t)std::min<size_t>(kMergeK0, most);
+    int64_t next = merge_k0 * nm;
+    for (int64_t m = 0; m < nm; ++m) {
+      const std::vector<int32_t>& parts = row_parts[merge_rows[m]];
+      for (size_t k = 0; k < parts.size(); ++k) {
+        const int64_t slot = (int64_t)k < merge_k0 ? (int64_t)k * nm + m : next++;
+        slot_of_part[parts[k]] = (int32_t)slot;
+        merge_parts.push_back((int32_t)slot);
       }
       merge_indptr.push_back((int32_t)merge_parts.size());
+    }
+    n_slots = next;
+    if (n_slots > (int64_t)std::numeric_limits<int32_t>::max()) {
+      delete plan;
+      return fail(HALO_ERR_INVALID_ARGUMENT, "too many partial slots");
     }
     for (const std::vector<Item>* list : {&items, &witems})
       for (const Item& it : *list)
@@ -637,9 +656,11 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   plan->n_merge_parts = (int32_t)merge_parts.size();
   plan->n_merge = (int32_t)merge_rows.size();
   plan->n_part_rows = part_rows;
+  plan->n_part_slots = n_slots;
+  plan->merge_k0 = merge_k0;
   const size_t D = (size_t)p.head_dim;
   plan->workspace_bytes =
-      part_rows ? align_up(part_rows * D * sizeof(float), 256) + align_up(part_rows * sizeof(float), 256) : 0;
+      n_slots ? align_up(n_slots * D * sizeof(float), 256) + align_up(n_slots * sizeof(float), 256) : 0;
 
   // Pack the device metadata image.
   MetaLayout L;

@@ -180,8 +180,23 @@ def _check_plan(w, plan):
     for i, r_ in enumerate(mrows.tolist()):
         got_parts = set(m["merge_parts"][m["merge_indptr"][i]:m["merge_indptr"][i + 1]].tolist())
         assert got_parts == by_row.get(r_, set())
-        # an entry's partials fill its slot range
-        assert got_parts == set(range(m["merge_indptr"][i], m["merge_indptr"][i + 1]))
+    # slots: the first k0 = min(8, most partials of an entry) partials of entry
+    # e at k * n_merge + e, the rest consecutive after k0 * n_merge
+    nm = len(mrows)
+    counts = np.diff(m["merge_indptr"])
+    k0 = min(8, int(counts.max())) if nm else 0
+    nxt = k0 * nm
+    for e in range(nm):
+        slots = m["merge_parts"][m["merge_indptr"][e]:m["merge_indptr"][e + 1]].tolist()
+        for k, sl in enumerate(slots):
+            if k < k0:
+                assert sl == k * nm + e, "fixed slot of an entry's first partials"
+            else:
+                assert sl == nxt, "overflow slots are consecutive"
+                nxt += 1
+    assert len(np.unique(m["merge_parts"])) == len(m["merge_parts"])
+    d = w.head_dim
+    assert plan.workspace_bytes == (0 if nxt == 0 else -(-nxt * d * 4 // 256) * 256 + -(-nxt * 4 // 256) * 256)
     st = plan.stats()
     assert st["visible_pairs"] == int(eh.sum())
     assert st["num_items"] == n_narrow and st["num_wide_items"] == len(items) - n_narrow
@@ -198,6 +213,16 @@ def test_plan_covers_configs(lib, index):
         assert plan.workspace_bytes > 0
     else:
         assert plan.workspace_bytes == 0 and len(m["merge_rows"]) == 0
+
+
+def test_plan_merge_overflow_slots(lib, monkeypatch):
+    """Short shared chunks give every Llama-8B-shaped row more than 8
+    partials: the first 8 at fixed slots, the rest in the overflow range."""
+    monkeypatch.setenv("HALO_KC_SHARED", "96")
+    w = make_config(1)
+    plan = halo.Plan.from_csr(_params(w), w.forest_csr())
+    m = _check_plan(w, plan)
+    assert np.diff(m["merge_indptr"]).min() > 8
 
 
 @pytest.mark.parametrize("seed", range(8))
