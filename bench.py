@@ -22,7 +22,12 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
-DEFAULT_WORKLOAD = "llama8b_decode"
+# The largest single-GPU workload: 1024 requests of a 70B-shaped layer (64 q /
+# 8 kv heads, d = 128, bf16) in 8 groups of 128 sharing 8192-token prefixes,
+# suffixes U{256..2048}.
+DEFAULT_WORKLOAD = "llama70b_batch_decode"
+# Measured in the same run, after the headline, each with its own roofline.
+SECONDARY_WORKLOADS = ("llama8b_decode", "two_level_tree_decode", "chunked_prefill")
 MALL_BYTES = 256 << 20
 
 
@@ -50,54 +55,85 @@ def algorithmic_bytes(w, stats):
     return kv + pages + q + o + lse
 
 
-def cpu_baseline(w, min_seconds=10.0):
-    """The fp64 oracle on the host cores over the same batch (decode: the
-    whole batch, repeated until min_seconds; prefill: whole requests until
-    min_seconds)."""
-    import numpy as np
-    import oracle
+def _cpu_info():
+    import os
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = 1
-    seg_k, seg_v = {}, {}
-    for s in range(len(w.seg_len)):
-        k, v = w.segment_kv(s)
-        seg_k[s] = k.double().numpy()
-        seg_v[s] = v.double().numpy()
-    q = w.q.double().cpu().numpy()
-    tokens = 0
-    passes = 0
-    t0 = time.perf_counter()
-    if not w.is_prefill:
-        while True:
-            oracle.decode(q, seg_k, seg_v, w.req_paths, w.scale)
-            tokens += w.num_requests
-            passes += 1
-            if time.perf_counter() - t0 >= min_seconds:
-                break
-        sample = f"whole {w.num_requests}-request batch x {passes} pass(es)"
-    else:
-        r = 0
-        while True:
-            a, b = w.q_rows_of_request(r)
-            oracle.prefill(q[a:b], w.q_len[r:r + 1], seg_k, seg_v, [w.req_paths[r]], w.scale)
-            tokens += b - a
-            passes += 1
-            r = (r + 1) % w.num_requests
-            if time.perf_counter() - t0 >= min_seconds:
-                break
-        sample = f"{passes} request(s) of {int(w.q_len[0])} new tokens each"
-    dt = time.perf_counter() - t0
     model = ""
     try:
         with open("/proc/cpuinfo") as f:
             model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
     except OSError:  # pragma: no cover
         pass
-    return {"value": tokens / dt, "unit": "query-tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": sample, "seconds": round(dt, 3),
+    return int(threads), model
+
+
+def _request_order(w):
+    """Requests in the order the CPU baseline samples them: strided over the
+    batch (0, R/8, 2R/8, ..., then 1, 1 + R/8, ...), so a bounded sample
+    covers every prefix group and the whole suffix-length range."""
+    R = w.num_requests
+    stride = max(1, R // 8)
+    return [r for off in range(stride) for r in range(off, R, stride)]
+
+
+def cpu_baseline(w, min_seconds=10.0):
+    """The fp64 oracle, as it stands, on the host cores: a bounded sample of
+    the same workload, one request at a time.
+
+    Each sampled request's segments are upcast to fp64 outside the timed
+    region (segments shared by several sampled requests are upcast once, and
+    nothing is upcast for requests outside the sample, so host memory stays
+    bounded on the largest batch); only the oracle call is timed. Requests are
+    taken in a strided order until min_seconds of oracle time have passed.
+    The rate is query-tokens per second of oracle time."""
+    import numpy as np
+    import oracle
+    threads, model = _cpu_info()
+    refs = {}
+    for path in w.req_paths:
+        for s in path:
+            refs[s] = refs.get(s, 0) + 1
+    shared64 = {}
+
+    def kv64(s):
+        # segments on several paths are upcast once and kept; private ones
+        # are upcast for their one request and dropped after it
+        if s in shared64:
+            return shared64[s]
+        k, v = w.segment_kv(s)
+        kv = (k.double().numpy(), v.double().numpy())
+        if refs.get(s, 0) > 1:
+            shared64[s] = kv
+        return kv
+
+    q = w.q.double().cpu().numpy()
+    tokens = 0
+    done = []
+    busy = 0.0
+    order = _request_order(w)
+    while busy < min_seconds:
+        r = order[len(done) % len(order)]
+        path = w.req_paths[r]
+        seg_k = {s: kv64(s)[0] for s in path}
+        seg_v = {s: kv64(s)[1] for s in path}
+        a, b = w.q_rows_of_request(r)
+        t0 = time.perf_counter()
+        if w.is_prefill:
+            oracle.prefill(q[a:b], w.q_len[r:r + 1], seg_k, seg_v, [path], w.scale)
+        else:
+            oracle.decode(q[a:b], seg_k, seg_v, [path], w.scale)
+        busy += time.perf_counter() - t0
+        tokens += b - a
+        done.append(r)
+    keys = int(sum(sum(int(w.seg_len[s]) for s in w.req_paths[r]) for r in done))
+    sample = (f"{len(done)} of {w.num_requests} requests (strided order), {tokens} query tokens, "
+              f"{keys} keys per head group in total; fp64 upcast outside the timed region")
+    return {"value": tokens / busy, "unit": "query-tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": sample, "seconds": round(busy, 3),
             "host_cpus": len(os.sched_getaffinity(0)), "os_cpu_count": os.cpu_count(),
             "cpu_model": model, "blas_threads": int(threads)}
 
@@ -262,6 +298,8 @@ def main():
     ap.add_argument("--replicas", type=int, default=0, help="input copies to rotate over (0: auto)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="time only --workload (no secondary workloads in the line)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch (from rocprofv3 counters), if present")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -316,13 +354,88 @@ def main():
 
     import torch
     from paper_2509_02121_amd import halo
-    from workloads import make_config
 
     halo.load_library(require_gpu=True)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = make_config(args.workload, device=dev)
-    if args.pool_fill > 0:
+    head = measure_workload(args.workload, args, dev, pool_fill=args.pool_fill,
+                            with_cpu=not args.no_cpu_baseline, percentiles=True)
+    secondary = {}
+    if not args.no_secondary and not args.pool_fill:
+        for name in SECONDARY_WORKLOADS:
+            if name != args.workload:
+                secondary[name] = measure_workload(name, args, dev, with_cpu=False, percentiles=False)
+
+    w = head.pop("_workload")
+    line = {
+        "metric": "shared-prefix attention: query-tokens/s + effective HBM GB/s (% roofline)",
+        "value": head["value"],
+        "unit": "query-tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "gpu_ms_per_step": head["gpu_ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": head["dtype"],
+        "data": "synthetic",
+        "per_call_us": head["per_call_us"],
+        "effective_hbm_gbps": head["effective_hbm_gbps"],
+        "hbm_roofline_frac": head["hbm_roofline_frac"],
+        "config": head["config"],
+        "host_plan": head["host_plan"],
+        "roofline": head["roofline"],
+        "cpu_baseline": head["cpu_baseline"],
+    }
+    if head["cpu_baseline"]:
+        line["speedup_vs_oracle"] = round(head["value"] / head["cpu_baseline"]["value"], 1)
+    if secondary:
+        line["secondary"] = {k: {f: v[f] for f in ("value", "unit", "dtype", "ms_per_step", "gpu_ms_per_step",
+                                                   "effective_hbm_gbps", "config", "host_plan", "roofline")}
+                             for k, v in secondary.items()}
+    del w
+    print(json.dumps(line), flush=True)
+
+
+def _plan_timing(halo, params, csr, device_meta, stream, repeats=7):
+    """Host cost of one batch step's plan: halo_plan_create (median of
+    `repeats` runs on this host) and the metadata upload (HIP events on the
+    stream around halo_plan_upload from pageable host memory)."""
+    import torch
+    ts = []
+    plan = None
+    for _ in range(repeats):
+        t0 = time.perf_counter()
+        plan = halo.Plan.from_csr(params, csr)
+        ts.append((time.perf_counter() - t0) * 1e3)
+    ts.sort()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    ups = []
+    for _ in range(3):
+        torch.cuda.synchronize()
+        e0.record(stream)
+        plan.upload(device_meta, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ups.append(e0.elapsed_time(e1) * 1e3)
+    ups.sort()
+    return {"plan_ms": round(ts[len(ts) // 2], 4), "plan_ms_min": round(ts[0], 4), "repeats": repeats,
+            "meta_upload_bytes": int(plan.device_meta_bytes), "upload_us": round(ups[1], 1),
+            "workspace_bytes": int(plan.workspace_bytes)}
+
+
+def measure_workload(name, args, dev, pool_fill=0.0, with_cpu=False, percentiles=False):
+    """Time one workload's library call (one step = one call over the whole
+    batch) and derive its roofline figures."""
+    import torch
+    from paper_2509_02121_amd import halo
+    from workloads import make_config
+
+    w = make_config(name, device=dev)
+    if pool_fill > 0:
         # same forest and values, in a pool of pool_fill x (free memory): the
         # needed pages land at random over the whole pool
         page_bytes = (w.k_pool[0].numel() + w.v_pool[0].numel()) * w.k_pool.element_size()
@@ -330,12 +443,15 @@ def main():
         del w
         torch.cuda.empty_cache()
         free = torch.cuda.mem_get_info(dev)[0]
-        target = int(args.pool_fill * free) // page_bytes
-        w = make_config(args.workload, device=dev, extra_pages=max(0, target - have))
+        target = int(pool_fill * free) // page_bytes
+        w = make_config(name, device=dev, extra_pages=max(0, target - have))
     params = halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages,
                               w.scale, w.dtype)
-    runner = halo.PrefixAttention(params, w.forest_csr(), dev)
+    csr = w.forest_csr()
+    runner = halo.PrefixAttention(params, csr, dev)
     stats = runner.plan.stats()
+    stream = torch.cuda.current_stream()
+    host_plan = _plan_timing(halo, params, csr, runner.meta, stream)
 
     pool_bytes = (w.k_pool.numel() + w.v_pool.numel()) * w.k_pool.element_size()
     n_rep = args.replicas or max(1, min(16, -(-4 * MALL_BYTES // max(pool_bytes, 1))))
@@ -343,7 +459,6 @@ def main():
     for _ in range(n_rep - 1):
         reps.append((w.q.clone(), w.k_pool.clone(), w.v_pool.clone()))
     outs = [runner.alloc_outputs(w.q) for _ in range(n_rep)]
-    stream = torch.cuda.current_stream()
 
     calls = [runner.bind(reps[i][0], reps[i][1], reps[i][2], outs[i][0], outs[i][1], stream)
              for i in range(n_rep)]
@@ -367,17 +482,19 @@ def main():
     wall_ms = (t1 - t0) * 1e3 / args.steps
     gpu_ms = ev0.elapsed_time(ev1) / args.steps
 
-    # Spread of single calls (a separate pass, one event pair per call).
-    per_call = []
-    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-             for _ in range(min(args.steps, 200))]
-    for i, (a, b) in enumerate(pairs):
-        a.record(stream)
-        step(i)
-        b.record(stream)
-    torch.cuda.synchronize()
-    per_call = sorted(a.elapsed_time(b) * 1e3 for a, b in pairs)
-    pct = lambda f: round(per_call[min(len(per_call) - 1, int(f * len(per_call)))], 2)
+    per_call_us = None
+    if percentiles:
+        # spread of single calls (a separate pass, one event pair per call)
+        pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(min(args.steps, 200))]
+        for i, (a, b) in enumerate(pairs):
+            a.record(stream)
+            step(i)
+            b.record(stream)
+        torch.cuda.synchronize()
+        per_call = sorted(a.elapsed_time(b) * 1e3 for a, b in pairs)
+        pct = lambda f: round(per_call[min(len(per_call) - 1, int(f * len(per_call)))], 2)
+        per_call_us = {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9), "calls": len(per_call)}
 
     q_tokens = w.q.shape[0]
     alg_bytes = algorithmic_bytes(w, stats)
@@ -392,7 +509,7 @@ def main():
         with open(args.traffic_json) as f:
             tr = json.load(f)
         sha = source_sha256()
-        if tr.get("_kernel_source_sha256") == sha and w.name in tr and not args.pool_fill:
+        if tr.get("_kernel_source_sha256") == sha and w.name in tr and not pool_fill:
             traffic = tr[w.name]["bytes_per_call"]
     except (OSError, ValueError, KeyError):
         traffic = None
@@ -416,39 +533,36 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "kernel": kernel_desc, "algorithmic_bytes": alg_bytes}
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, args.cpu_seconds)
-
-    line = {
-        "metric": "shared-prefix attention: query-tokens/s + effective HBM GB/s (% roofline)",
+    cpu = cpu_baseline(w, args.cpu_seconds) if with_cpu else None
+    res = {
         "value": round(value, 1),
         "unit": "query-tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
         "ms_per_step": round(wall_ms, 5),
         "gpu_ms_per_step": round(gpu_ms, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
-        "data": "synthetic",
-        "per_call_us": {"p10": pct(0.1), "median": pct(0.5), "p90": pct(0.9), "calls": len(per_call)},
+        "per_call_us": per_call_us,
         "effective_hbm_gbps": round(eff_gbps, 1),
         "hbm_roofline_frac": round(eff_gbps / HBM_PEAK_GBPS, 4),
         "config": {"workload": w.name, "requests": w.num_requests, "query_tokens": q_tokens,
                    "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
                    "head_dim": w.head_dim, "page_size": w.page_size,
                    "distinct_kv_tokens": stats["distinct_kv_tokens"], "replicas": n_rep,
-                   "work_items": stats["num_items"], "merge_rows": stats["num_merge_rows"],
+                   "work_items": stats["num_items"], "wide_items": stats["num_wide_items"],
+                   "merge_rows": stats["num_merge_rows"], "partial_rows": stats["num_partial_rows"],
                    "pool_gb": round(pool_bytes / 1e9, 2), "pool_pages": int(w.num_pool_pages)},
+        "host_plan": host_plan,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
-    if cpu:
-        line["speedup_vs_oracle"] = round(value / cpu["value"], 1)
-    print(json.dumps(line), flush=True)
+    # free the device memory of this workload before the next one
+    del calls, outs, reps, runner
+    if with_cpu or percentiles:
+        res["_workload"] = w
+    else:
+        del w
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
 
 
 if __name__ == "__main__":

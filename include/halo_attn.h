@@ -153,8 +153,10 @@ halo_status_t halo_prefix_attn_prefill(const halo_plan_t* plan, const void* devi
  * of one pool into a dense token-major buffer, bit for bit.
  *   out[out_token_offset[i] + t][h][:] = token t of sequence i, head h
  * for t < seq_len[i], where token t lives in page page_ids[seq_page_indptr[i]
- * + t / page_size]. pool_kind says whether pool has the k_pool or the
- * v_pool layout. page_ids, seq_page_indptr, seq_len, out_token_offset and
+ * + t / page_size]. seq_page_indptr [num_seqs + 1] is nondecreasing and need
+ * not start at 0 (a slice of a larger page list works): the slots
+ * seq_page_indptr[0] .. seq_page_indptr[num_seqs] - 1 of page_ids are read.
+ * pool_kind says whether pool has the k_pool or the v_pool layout. page_ids, seq_page_indptr, seq_len, out_token_offset and
  * out are DEVICE pointers; out is [*][num_kv_heads][head_dim] of kv_dtype;
  * pool and out must be 16-byte aligned.
  * Only params' num_kv_heads, head_dim, page_size, num_pool_pages and
@@ -284,7 +286,7 @@ typedef struct {
   int64_t num_query_rows;     /* rows of q / o */
   int64_t distinct_kv_tokens; /* sum of segment lengths, each segment once */
   int64_t visible_pairs;      /* sum over query rows and q heads of visible keys */
-  int32_t num_wide_items;     /* wide work items (one 4-wave workgroup, <= 256 rows) */
+  int32_t num_wide_items;     /* wide work items (one 8-wave workgroup, <= 256 rows) */
   int32_t wide_row_blocks;    /* 1 when the plan has wide items (32 query rows per wave), else 0 */
 } halo_plan_stats_t;
 

@@ -98,7 +98,7 @@ struct MetaLayout {
   size_t page_ids = 0;       // int32 [total pages]
   size_t items = 0;          // Item  [n_narrow_blocks * narrow_slots]  narrow, by workgroup slot
   size_t item_recs = 0;      // ItemRec, one per narrow slot
-  size_t wide_items = 0;     // Item  [n_wide]      wide (one 4-wave workgroup)
+  size_t wide_items = 0;     // Item  [n_wide]      wide (one kWideWaves-wave workgroup)
   size_t spans = 0;          // Span  [n_spans]
   size_t rows = 0;           // Row   [n_rows]
   size_t merge_rows = 0;     // int32 [n_merge] output row (q_row) per merge entry

@@ -87,17 +87,23 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
   W* out = static_cast<W*>(a.out);
   W* st = reinterpret_cast<W*>(stage[wave]);
 
-  const int64_t total = (int64_t)a.seq_page_indptr[a.num_seqs] * H;
+  // page-list slots first .. last-1 are tiled; first need not be 0 (a
+  // slice of a larger page list)
+  const int first = a.seq_page_indptr[0];
+  const int64_t total = ((int64_t)a.seq_page_indptr[a.num_seqs] - first) * H;
   const int64_t waves = (int64_t)gridDim.x * 4;
   const int64_t per = (total + waves - 1) / waves;
   const int64_t w_id = (int64_t)blockIdx.x * 4 + wave;
   const int64_t t_begin = w_id * per;
   const int64_t t_end = min(total, t_begin + per);
   if (t_begin >= t_end) return;
-  int seq = last_at_or_below(a.seq_page_indptr, a.num_seqs, t_begin / H, lane);
+  // indptr[0] <= first + t_begin / H, so the search returns a sequence in
+  // [0, num_seqs); the walk below stops at num_seqs - 1 at the latest, since
+  // every slot is < indptr[num_seqs]
+  int seq = last_at_or_below(a.seq_page_indptr, a.num_seqs, first + t_begin / H, lane);
   int base = a.seq_page_indptr[seq], next = a.seq_page_indptr[seq + 1];
   for (int64_t tl = t_begin; tl < t_end; ++tl) {
-    const int slot = (int)(tl / H), h = (int)(tl % H);
+    const int slot = first + (int)(tl / H), h = (int)(tl % H);
     while (slot >= next) {             // later sequences (empty ones are passed over)
       ++seq;
       base = next;

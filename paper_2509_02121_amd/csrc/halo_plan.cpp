@@ -4,17 +4,20 @@
 //
 // Decode (arXiv 2509.02121 §2, intra-batch prefix sharing): a segment on the
 // path of two or more requests is "shared". Its query rows -- every (request,
-// q head) pair of one kv head -- are stacked 16 to a work item, so each of the
-// segment's pages is read for 16 rows at a time instead of once per request
-// (the grouped prefix pass). Segments on one path only are "private"; each
-// request's private keys are split into chunks (the suffix pass). Every item
-// over a subset of a row's keys writes a partial (o, lse); rows with several
-// partials are combined by the log-sum-exp merge, rows with exactly one write
-// their final result directly.
+// q head) pair of one kv head -- are stacked into one work item per row
+// group, so each of the segment's pages is read once per row group instead of
+// once per request (the grouped prefix pass): up to 16 rows in a narrow item
+// (one wavefront), or up to 256 in a wide item (one 8-wave workgroup sharing
+// the key stream through LDS) when the shared work is large. Segments on one
+// path only are "private"; each request's private keys are split into chunks
+// (the suffix pass). Every item over a subset of a row's keys writes a
+// partial (o, lse); rows with several partials are combined by the
+// log-sum-exp merge, rows with exactly one write their final result directly.
 //
-// Prefill (§4.1, prefix caching): each item holds 16 (query, head) rows of one
-// request and walks all of that request's keys, the cached prefix first and
-// its own chunk last, causally; results are final.
+// Prefill (§4.1, prefix caching): each item holds the (query, head) rows of
+// one request and one kv head -- up to 256 in a wide item for bf16, 16 in a
+// narrow item otherwise -- and walks all of that request's keys, the cached
+// prefix first and its own chunk last, causally; results are final.
 
 #include <stdlib.h>
 

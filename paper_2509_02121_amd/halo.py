@@ -243,6 +243,7 @@ class Plan:
         self.device_meta_bytes = meta.value
         self.workspace_bytes = ws.value
         self.is_prefill = q_len is not None
+        self.num_query_rows = int(self.stats()["num_query_rows"])
 
     @classmethod
     def from_csr(cls, params, csr):
@@ -358,16 +359,47 @@ def _stream_handle(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _pool_elems(params):
+    """Elements of one page pool: num_pool_pages x H_kv x page_size x d."""
+    return int(params.num_pool_pages) * params.num_kv_heads * params.page_size * params.head_dim
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
 def _check_run(plan, device_meta, q, k_pool, v_pool, o, lse, workspace):
+    """Every buffer a run call reads or writes is checked against the plan's
+    sizes before any launch: the kernels index q, o and lse by the plan's
+    query rows and the pools by its page ids, so an undersized tensor would
+    be read or written out of bounds. Sizes are checked first, then layout,
+    element type and device."""
     import torch
-    kv = _torch_dtype(plan.params.kv_dtype)
+    p = plan.params
+    kv = _torch_dtype(p.kv_dtype)
+    rows = plan.num_query_rows * p.num_q_heads
+    need = [(device_meta, "device_meta", plan.device_meta_bytes, "bytes"),
+            (k_pool, "k_pool", _pool_elems(p), "elements"), (v_pool, "v_pool", _pool_elems(p), "elements"),
+            (o, "o", rows * p.head_dim, "elements")]
+    if lse is not None:
+        need.append((lse, "lse", rows, "elements"))
+    if q.numel() != rows * p.head_dim:
+        raise ValueError(f"q has {q.numel()} elements, the plan has {plan.num_query_rows} query rows x "
+                         f"{p.num_q_heads} heads x {p.head_dim} = {rows * p.head_dim}")
+    for t, name, n, unit in need:
+        have = _nbytes(t) if unit == "bytes" else t.numel()
+        if have < n:
+            raise ValueError(f"{name} has {have} {unit}, the plan needs at least {n}")
+    ws = _nbytes(workspace) if workspace is not None else 0
+    if ws < plan.workspace_bytes:
+        raise ValueError(f"workspace has {ws} bytes, the plan needs {plan.workspace_bytes}")
     _gpu(device_meta, "device_meta")
     _gpu(q, "q", kv)
     _gpu(k_pool, "k_pool", kv)
     _gpu(v_pool, "v_pool", kv)
-    _gpu(o, "o", _torch_dtype(plan.params.out_dtype), q.numel())
+    _gpu(o, "o", _torch_dtype(p.out_dtype))
     if lse is not None:
-        _gpu(lse, "lse", torch.float32, q.numel() // max(1, plan.params.head_dim))
+        _gpu(lse, "lse", torch.float32)
     if workspace is not None:
         _gpu(workspace, "workspace")
 
@@ -394,8 +426,8 @@ def prefix_attn_prefill(plan, device_meta, q, k_pool, v_pool, o, lse, workspace,
 def _check_gather(pool, params, page_ids, seq_page_indptr, seq_len, out_token_offset, out, error_flag):
     import torch
     kv = _torch_dtype(params.kv_dtype)
+    _gpu(pool, "pool", kv, _pool_elems(params))
     n = _page_lists(page_ids, seq_page_indptr)
-    _gpu(pool, "pool", kv)
     _gpu(seq_len, "seq_len", torch.int32, n)
     _gpu(out_token_offset, "out_token_offset", torch.int64, n)
     _gpu(out, "out", kv)
@@ -407,9 +439,12 @@ def _check_scatter(pools, params, page_ids, seq_page_indptr, seq_start, seq_coun
                    error_flag):
     import torch
     kv = _torch_dtype(params.kv_dtype)
-    n = _page_lists(page_ids, seq_page_indptr)
+    for i, t in enumerate(pools):
+        if t.numel() < _pool_elems(params):
+            raise ValueError(f"pool {i} has {t.numel()} elements, needs at least {_pool_elems(params)}")
     for i, t in enumerate(pools):
         _gpu(t, f"pool {i}", kv)
+    n = _page_lists(page_ids, seq_page_indptr)
     for i, t in enumerate(srcs):
         _gpu(t, f"input {i}", kv)
     _gpu(seq_start, "seq_start", torch.int32, n)
@@ -421,7 +456,7 @@ def _check_scatter(pools, params, page_ids, seq_page_indptr, seq_start, seq_coun
 
 def _check_copy(pool, params, src_pages, dst_pages, error_flag):
     import torch
-    _gpu(pool, "pool", _torch_dtype(params.kv_dtype))
+    _gpu(pool, "pool", _torch_dtype(params.kv_dtype), _pool_elems(params))
     _gpu(src_pages, "src_pages", torch.int32)
     _gpu(dst_pages, "dst_pages", torch.int32, src_pages.numel())
     if error_flag is not None:
@@ -568,8 +603,21 @@ class PrefixAttention:
         self.meta = torch.empty(max(self.plan.device_meta_bytes, 256), dtype=torch.uint8, device=self.device)
         self.workspace = (torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=self.device)
                           if self.plan.workspace_bytes else None)
-        self.plan.upload(self.meta)
+        upload_stream = torch.cuda.current_stream(self.device)
+        self.plan.upload(self.meta, upload_stream)
+        # runs on another stream wait for this event, so they never read
+        # device_meta before the copy has landed
+        self._uploaded = torch.cuda.Event()
+        self._uploaded.record(upload_stream)
+        self._upload_stream = upload_stream
         self.out_dtype = {HALO_F32: torch.float32, HALO_BF16: torch.bfloat16}[params.out_dtype]
+
+    def _after_upload(self, stream):
+        """Make `stream` (None: the current stream) wait for the metadata upload."""
+        import torch
+        s = stream if stream is not None else torch.cuda.current_stream(self.device)
+        if s != self._upload_stream:
+            s.wait_event(self._uploaded)
 
     def alloc_outputs(self, q):
         import torch
@@ -584,6 +632,7 @@ class PrefixAttention:
         fn = _LIB.halo_prefix_attn_prefill if self.plan.is_prefill else _LIB.halo_prefix_attn_decode
         ws = self.workspace
         _check_run(self.plan, self.meta, q, k_pool, v_pool, o, lse, ws)
+        self._after_upload(stream)
         args = (self.plan._handle, self.meta.data_ptr(), q.data_ptr(), k_pool.data_ptr(),
                 v_pool.data_ptr(), o.data_ptr(), lse.data_ptr() if lse is not None else None,
                 ws.data_ptr() if ws is not None else None,
@@ -600,5 +649,6 @@ class PrefixAttention:
             o, lse_new = self.alloc_outputs(q)
             lse = lse if lse is not None else lse_new
         fn = prefix_attn_prefill if self.plan.is_prefill else prefix_attn_decode
+        self._after_upload(stream)
         fn(self.plan, self.meta, q, k_pool, v_pool, o, lse, self.workspace, stream)
         return o, lse

@@ -406,3 +406,53 @@ def test_binding_rejects_tensors_the_abi_would_misread():
         halo._gpu(i32, "seq_len", torch.int32, 5)
     with pytest.raises(ValueError, match="on the GPU"):
         halo._gpu(i32, "seq_len", torch.int32, 4)
+
+
+def test_binding_rejects_buffers_smaller_than_the_plan(lib):
+    """Run calls check every buffer against the plan before any launch: the
+    kernels index q, o and lse by the plan's query rows and the pools by its
+    page ids, so an undersized tensor would be read or written out of
+    bounds. Host tensors of the right size get as far as the device check."""
+    import torch
+    params = halo.make_params(4, 2, 64, torch.float32, 3, 0.125)
+    plan = halo.Plan.from_csr(params, _csr(GOOD["seg_len"], GOOD["pages"], GOOD["paths"]))
+    R = plan.num_query_rows
+    pool = 3 * 2 * 16 * 64
+    meta = torch.zeros(plan.device_meta_bytes, dtype=torch.uint8)
+    ws = torch.zeros(plan.workspace_bytes, dtype=torch.uint8)
+    q = torch.zeros(R, 4, 64)
+    kp = torch.zeros(pool)
+    o = torch.zeros(R, 4, 64)
+    lse = torch.zeros(R, 4)
+
+    def run(**kw):
+        a = dict(device_meta=meta, q=q, k_pool=kp, v_pool=kp, o=o, lse=lse, workspace=ws)
+        a.update(kw)
+        halo._check_run(plan, **a)
+
+    with pytest.raises(ValueError, match="on the GPU"):
+        run()
+    with pytest.raises(ValueError, match="device_meta has"):
+        run(device_meta=meta[:-1])
+    with pytest.raises(ValueError, match="q has"):
+        run(q=torch.zeros(R + 1, 4, 64))
+    with pytest.raises(ValueError, match="k_pool has"):
+        run(k_pool=kp[:-1])
+    with pytest.raises(ValueError, match="v_pool has"):
+        run(v_pool=kp[:-64])
+    with pytest.raises(ValueError, match="o has"):
+        run(o=torch.zeros(R, 4, 63))
+    with pytest.raises(ValueError, match="lse has"):
+        run(lse=torch.zeros(R * 4 - 1))
+    with pytest.raises(ValueError, match="workspace has"):
+        run(workspace=ws[:-1])
+    with pytest.raises(ValueError, match="workspace has"):
+        run(workspace=None)
+    i32 = torch.zeros(4, dtype=torch.int32)
+    i64 = torch.zeros(4, dtype=torch.int64)
+    with pytest.raises(ValueError, match="pool has"):
+        halo.kv_page_gather(kp[:-1], params, halo.HALO_POOL_K, i32, i32, i32, i64, kp)
+    with pytest.raises(ValueError, match="pool 1 has"):
+        halo.kv_page_scatter_kv(kp, kp[:-1], params, i32, i32, i32, i32, i64, kp, kp)
+    with pytest.raises(ValueError, match="pool has"):
+        halo.kv_page_copy(kp[:-1], params, i32, i32)

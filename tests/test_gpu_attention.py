@@ -228,6 +228,12 @@ def test_workspace_too_small_is_rejected(gpu_lib):
     pa = halo.PrefixAttention(params_of(w), w.forest_csr())
     o, lse = pa.alloc_outputs(w.q)
     small = torch.empty(pa.plan.workspace_bytes - 256, dtype=torch.uint8, device="cuda")
-    with pytest.raises(halo.HaloError) as e:
+    # the binding refuses it before the call ...
+    with pytest.raises(ValueError, match="workspace has"):
         halo.prefix_attn_decode(pa.plan, pa.meta, w.q, w.k_pool, w.v_pool, o, lse, small)
-    assert e.value.status == halo.HALO_ERR_WORKSPACE_TOO_SMALL
+    # ... and so does the C ABI itself
+    st = halo._LIB.halo_prefix_attn_decode(pa.plan._handle, pa.meta.data_ptr(), w.q.data_ptr(),
+                                           w.k_pool.data_ptr(), w.v_pool.data_ptr(), o.data_ptr(),
+                                           lse.data_ptr(), small.data_ptr(), small.numel(),
+                                           halo._stream_handle(None))
+    assert st == halo.HALO_ERR_WORKSPACE_TOO_SMALL

@@ -4,6 +4,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from gpu_helpers import params_of, to_device
 from paper_2509_02121_amd import halo
 from workloads import build_workload, make_config
@@ -33,8 +34,16 @@ def _gather(w, seqs, kind, error_flag=None, pages_override=None):
 
 
 def _expected(w, seqs, kind):
-    parts = [w.segment_kv(s)[0 if kind == halo.HALO_POOL_K else 1] for s in seqs]
-    return torch.cat(parts) if parts else torch.zeros(0)
+    """oracle.gather_tokens over the logical per-segment arrays (read back out
+    of the pools by the generator's own reshape, not by the library)."""
+    which = 0 if kind == halo.HALO_POOL_K else 1
+    arrays = {s: w.segment_kv(s)[which] for s in set(seqs)}
+    if not seqs:
+        return torch.zeros(0)
+    exp = oracle.gather_tokens({s: a.numpy() if a.dtype != torch.bfloat16 else a.view(torch.int16).numpy()
+                                for s, a in arrays.items()}, seqs)
+    t = torch.from_numpy(np.ascontiguousarray(exp))
+    return t.view(torch.bfloat16) if w.dtype == torch.bfloat16 else t
 
 
 def _bits(t):
@@ -107,3 +116,35 @@ def test_gather_skewed_and_empty_sequences(gpu_lib, dtype, D, kind):
     n = exp.shape[0]
     assert np.array_equal(_bits(out[:n]), _bits(exp))
     assert (out[n:].float() == 7.0).all(), "gather wrote past the last token"
+
+
+@pytest.mark.parametrize("kind", [halo.HALO_POOL_K, halo.HALO_POOL_V])
+def test_gather_sliced_page_list(gpu_lib, kind):
+    """seq_page_indptr need not start at 0: a slice of a larger page list
+    (here sequences 3.. of a longer list, indptr and page ids passed as
+    views into the full arrays) gathers exactly those sequences."""
+    print(f"case: gather sliced page list kind {kind}", flush=True)
+    w = to_device(make_config(1))
+    seqs = list(range(len(w.seg_len)))
+    pages = [np.asarray(w.seg_pages[s], np.int32) for s in seqs]
+    indptr = np.zeros(len(seqs) + 1, np.int32)
+    indptr[1:] = np.cumsum([len(p) for p in pages])
+    lens = np.array([int(w.seg_len[s]) for s in seqs], np.int32)
+    sub = seqs[3:]
+    offs = np.zeros(len(sub), np.int64)
+    offs[1:] = np.cumsum(lens[3:])[:-1]
+    dev = "cuda"
+    total = int(lens[3:].sum())
+    out = torch.full((total + 3, w.num_kv_heads, w.head_dim), 7.0, dtype=w.dtype, device=dev)
+    pool = w.k_pool if kind == halo.HALO_POOL_K else w.v_pool
+    ids_full = torch.as_tensor(np.concatenate(pages), device=dev)
+    indptr_full = torch.as_tensor(indptr, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    halo.kv_page_gather(pool, params_of(w), kind, ids_full, indptr_full[3:],
+                        torch.as_tensor(lens[3:], device=dev), torch.as_tensor(offs, device=dev), out, flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 0
+    out = out.cpu()
+    exp = _expected(w, sub, kind)
+    assert np.array_equal(_bits(out[:total]), _bits(exp))
+    assert (out[total:].float() == 7.0).all(), "gather wrote past the last token"
