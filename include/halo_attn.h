@@ -149,6 +149,28 @@ halo_status_t halo_prefix_attn_prefill(const halo_plan_t* plan, const void* devi
                                        void* workspace, size_t workspace_bytes,
                                        void* stream);
 
+/* Largest workspace (bytes) halo_prefix_attn_decode_noalloc can serve. */
+#define HALO_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* halo_prefix_attn_decode for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. Same arguments and result as halo_prefix_attn_decode, without
+ * the workspace: the partial results go to a scratch array of
+ * HALO_NOALLOC_SCRATCH_BYTES that the library holds in device memory of its
+ * own, one per GPU (a static device variable, so each GPU the library runs
+ * on holds it until the process ends). The call allocates nothing and
+ * calls no allocating routine; its first call on a device looks up that
+ * device's copy of the array (hipGetSymbolAddress) and keeps the address.
+ * A plan whose workspace_bytes exceeds HALO_NOALLOC_SCRATCH_BYTES is
+ * rejected with HALO_ERR_WORKSPACE_TOO_SMALL and nothing is launched. Every
+ * call on one GPU shares that GPU's array and nothing in it has to start at
+ * zero (every partial is written before it is read); calls that overlap in
+ * time on one GPU (several streams, several host threads) race on it and
+ * must be serialised by the caller. */
+halo_status_t halo_prefix_attn_decode_noalloc(const halo_plan_t* plan, const void* device_meta,
+                                              const void* q, const void* k_pool, const void* v_pool,
+                                              void* o, float* lse, void* stream);
+
 /* Page gather (§7 PagedAttention): copy the tokens of num_seqs page lists out
  * of one pool into a dense token-major buffer, bit for bit.
  *   out[out_token_offset[i] + t][h][:] = token t of sequence i, head h

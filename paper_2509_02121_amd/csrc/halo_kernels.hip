@@ -26,7 +26,9 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
+#include <mutex>
 #include <string>
 
 #include "halo_internal.h"
@@ -1284,4 +1286,60 @@ extern "C" halo_status_t halo_prefix_attn_prefill(const halo_plan_t* plan, const
                                                   size_t workspace_bytes, void* stream) {
   return run_attention(plan, true, device_meta, q, k_pool, v_pool, o, lse, workspace, workspace_bytes,
                        stream);
+}
+
+// ---------------------------------------------------------------- no-alloc decode
+// Partial-result scratch of halo_prefix_attn_decode_noalloc: device memory of
+// the library's own, one copy per GPU, held until the process ends. In host
+// code `scratch` names a host-side stand-in, never a device address: the
+// device address of each GPU's copy comes from hipGetSymbolAddress, looked up
+// once per device and kept in g_scratch_ptr.
+static __device__ __align__(256) uint8_t scratch[HALO_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The device address of the current device's scratch array (looked up on the
+// first call on each device, with that device current).
+halo_status_t scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(HALO_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(HALO_ERR_UNSUPPORTED, "device index " + std::to_string(dev) + " beyond the scratch table");
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !p)
+        return fail(HALO_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return HALO_OK;
+}
+}  // namespace
+
+extern "C" halo_status_t halo_prefix_attn_decode_noalloc(const halo_plan_t* plan, const void* device_meta,
+                                                         const void* q, const void* k_pool,
+                                                         const void* v_pool, void* o, float* lse,
+                                                         void* stream) {
+  clear_error();
+  if (!plan) return fail(HALO_ERR_INVALID_ARGUMENT, "plan must not be NULL");
+  if (plan->workspace_bytes > HALO_NOALLOC_SCRATCH_BYTES)
+    return fail(HALO_ERR_WORKSPACE_TOO_SMALL,
+                "the plan needs " + std::to_string(plan->workspace_bytes) + " bytes of workspace; the no-alloc "
+                "entry point holds " + std::to_string((size_t)HALO_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  if (plan->workspace_bytes > 0) {
+    halo_status_t st = scratch_of_current_device(&ws);
+    if (st != HALO_OK) return st;
+  }
+  return run_attention(plan, false, device_meta, q, k_pool, v_pool, o, lse, ws,
+                       ws ? (size_t)HALO_NOALLOC_SCRATCH_BYTES : 0, stream);
 }

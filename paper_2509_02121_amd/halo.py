@@ -60,7 +60,8 @@ class PlanLayout(ctypes.Structure):
 EXPORTED_SYMBOLS = (
     "halo_plan_create", "halo_plan_upload", "halo_plan_destroy", "halo_plan_get_stats",
     "halo_plan_inspect",
-    "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_kv_page_gather",
+    "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_prefix_attn_decode_noalloc",
+    "halo_kv_page_gather",
     "halo_kv_page_scatter", "halo_kv_page_scatter_kv", "halo_kv_page_copy",
     "halo_prefix_tree_build", "halo_prefix_tree_get", "halo_prefix_tree_destroy",
     "halo_status_string", "halo_last_error_message",
@@ -128,6 +129,8 @@ def load_library(require_gpu=False):
         fn = getattr(lib, name)
         fn.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         fn.restype = ctypes.c_int
+    lib.halo_prefix_attn_decode_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.halo_prefix_attn_decode_noalloc.restype = ctypes.c_int
     lib.halo_kv_page_gather.argtypes = [vp, ctypes.POINTER(AttnParams), ctypes.c_int, vp, vp, vp, vp,
                                         ctypes.c_int32, vp, vp, vp]
     lib.halo_kv_page_gather.restype = ctypes.c_int
@@ -368,7 +371,7 @@ def _nbytes(t):
     return t.numel() * t.element_size()
 
 
-def _check_run(plan, device_meta, q, k_pool, v_pool, o, lse, workspace):
+def _check_run(plan, device_meta, q, k_pool, v_pool, o, lse, workspace, library_workspace=False):
     """Every buffer a run call reads or writes is checked against the plan's
     sizes before any launch: the kernels index q, o and lse by the plan's
     query rows and the pools by its page ids, so an undersized tensor would
@@ -391,7 +394,7 @@ def _check_run(plan, device_meta, q, k_pool, v_pool, o, lse, workspace):
         if have < n:
             raise ValueError(f"{name} has {have} {unit}, the plan needs at least {n}")
     ws = _nbytes(workspace) if workspace is not None else 0
-    if ws < plan.workspace_bytes:
+    if not library_workspace and ws < plan.workspace_bytes:
         raise ValueError(f"workspace has {ws} bytes, the plan needs {plan.workspace_bytes}")
     _gpu(device_meta, "device_meta")
     _gpu(q, "q", kv)
@@ -421,6 +424,24 @@ def prefix_attn_decode(plan, device_meta, q, k_pool, v_pool, o, lse, workspace, 
 def prefix_attn_prefill(plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream=None):
     """halo_prefix_attn_prefill on torch tensors (all on one GPU)."""
     _run(_LIB.halo_prefix_attn_prefill, plan, device_meta, q, k_pool, v_pool, o, lse, workspace, stream)
+
+
+# Largest workspace the no-alloc decode entry point serves (HALO_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def prefix_attn_decode_noalloc(plan, device_meta, q, k_pool, v_pool, o, lse, stream=None):
+    """halo_prefix_attn_decode_noalloc on torch tensors: decode with the
+    library's own per-GPU scratch instead of a workspace (no allocation).
+    Calls that overlap in time on one GPU share that scratch and race."""
+    if plan.workspace_bytes > NOALLOC_SCRATCH_BYTES:
+        raise ValueError(f"the plan needs {plan.workspace_bytes} bytes of workspace; the no-alloc entry "
+                         f"point holds {NOALLOC_SCRATCH_BYTES}")
+    _check_run(plan, device_meta, q, k_pool, v_pool, o, lse, None, library_workspace=True)
+    _check(_LIB.halo_prefix_attn_decode_noalloc(plan._handle, device_meta.data_ptr(), q.data_ptr(),
+                                                k_pool.data_ptr(), v_pool.data_ptr(), o.data_ptr(),
+                                                lse.data_ptr() if lse is not None else None,
+                                                _stream_handle(stream)))
 
 
 def _check_gather(pool, params, page_ids, seq_page_indptr, seq_len, out_token_offset, out, error_flag):
