@@ -289,6 +289,98 @@ def gather_bench(args):
     print(json.dumps(line), flush=True)
 
 
+def probe_bench(args):
+    """Context microbenchmarks (one JSON line): the HBM read rate of random
+    4 KB tiles with the suffix pass's loads, the dense bf16 MFMA rate, and
+    the v_exp_f32 rate with and without MFMAs on the same wave. Each figure
+    is the mean of `steps` launches timed with HIP events on the launch
+    stream after `warmup` launches."""
+    import numpy as np
+    import torch
+    from paper_2509_02121_amd import probe
+
+    probe.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    steps, warmup = max(3, min(args.steps, 20)), max(1, min(args.warmup, 3))
+    res = {"metric": "context microbenchmarks (gfx950)", "steps": steps}
+
+    # --- stream read: a 4 GiB pool (16x the Infinity Cache), every tile once
+    # per launch, in a seeded random order (or in address order)
+    pool_bytes = 4 << 30
+    n_tiles = pool_bytes // 4096
+    pool = torch.empty(pool_bytes, dtype=torch.uint8, device=dev)
+    pool.view(torch.int32).fill_(0x3c003c00)
+    rng = np.random.Generator(np.random.PCG64(11))
+    perm = torch.as_tensor(rng.permutation(n_tiles).astype(np.int32), device=dev)
+    seq = torch.arange(n_tiles, dtype=torch.int32, device=dev)
+    out = torch.empty(1 << 16, dtype=torch.int32, device=dev)
+    rows = []
+    configs = [  # (order, stages, waves per SIMD, non-temporal, steps per item)
+        ("random", 2, 2, 1, 32), ("random", 2, 2, 0, 32), ("random", 3, 2, 1, 32), ("random", 2, 1, 1, 32),
+        ("random", 3, 1, 1, 32), ("random", 4, 1, 1, 32), ("random", 2, 2, 1, 8), ("random", 3, 2, 1, 8),
+        ("address", 2, 2, 1, 32), ("address", 3, 2, 1, 32),
+        # independent items (metadata round trip, own pipeline, drain), without
+        # and with the per-step MFMA/softmax work
+        ("random", 10, 2, 1, 32), ("random", 11, 2, 1, 32), ("random", 10, 2, 1, 16), ("random", 11, 2, 1, 16),
+        # the same with the suffix pass's K/V tile access pattern
+        ("random", 12, 2, 1, 32), ("random", 13, 2, 1, 32),
+        # one item per wave, a workgroup per 8 items (not persistent)
+        ("random", 13, 2, 1, -32),
+    ]
+    for order, stages, wps, nt, spi in configs:
+        blocks = 256 if wps == 2 else 512
+        if spi < 0:       # one item per wave: as many workgroups as items / 8
+            spi = -spi
+            blocks = n_tiles // (4 * spi) // 8
+        call = probe.bind_stream_read(pool, perm if order == "random" else seq, spi, stages, wps, nt, blocks,
+                                      out, stream)
+        us = _time_launches(call, steps, warmup, stream)
+        gbps = pool_bytes / (us * 1e-6) / 1e9
+        mode = {10: "items", 11: "items+compute", 12: "items kv-pattern",
+                13: "items+compute kv-pattern"}.get(stages, "stream")
+        rows.append({"order": order, "mode": mode, "stages": 2 if stages >= 10 else stages,
+                     "waves_per_simd": wps, "nontemporal": nt,
+                     "steps_per_item": spi, "blocks": blocks, "bytes_in_flight_per_cu":
+                     ((2 if stages >= 10 else stages) - 1) * 16384 * 4 * wps, "us": round(us, 1),
+                     "gbps": round(gbps, 1),
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4)})
+        print(f"stream {rows[-1]}", file=sys.stderr, flush=True)
+    res["stream_read"] = {"bytes_per_launch": pool_bytes, "tile_bytes": 4096, "configs": rows}
+    del pool, perm, seq
+    torch.cuda.empty_cache()
+
+    # --- MFMA: 1024 blocks of 4 waves, 8 independent chains per wave
+    fout = torch.empty(1024 * 256, dtype=torch.float32, device=dev)
+    mf = {}
+    for shape, flop in ((32, 32 * 32 * 16 * 2), (16, 16 * 16 * 32 * 2)):
+        iters = 4000
+        call = probe.bind_mfma(shape, iters, 1024, fout, stream)
+        us = _time_launches(call, steps, warmup, stream)
+        tflops = 1024 * 4 * iters * 8 * flop / (us * 1e-6) / 1e12
+        mf[f"{shape}x{shape}x{16 if shape == 32 else 32}_bf16"] = {
+            "us": round(us, 1), "tflops": round(tflops, 1), "frac_of_2500": round(tflops / BF16_MFMA_PEAK_TFLOPS, 4)}
+    res["mfma"] = mf
+
+    # --- v_exp_f32: 16 chains per lane; one 32x32x16 MFMA per M exps
+    ex = []
+    for blocks in (256, 512):
+        for m in (0, 8, 4, 2):
+            iters = 4000
+            call = probe.bind_exp(m, iters, blocks, fout, stream)
+            us = _time_launches(call, steps, warmup, stream)
+            cycles = us * 1e-6 * 2.4e9                     # at the 2.4 GHz peak clock
+            waves_per_simd = blocks * 4 / 1024
+            n_exp = iters * 16 * waves_per_simd            # exps issued per SIMD
+            n_mfma = iters * (16 // m if m else 0) * waves_per_simd
+            ex.append({"blocks": blocks, "waves_per_simd": waves_per_simd, "exp_per_mfma": m,
+                       "us": round(us, 1), "cycles_per_exp": round(cycles / n_exp, 2),
+                       "cycles_per_mfma": round(cycles / n_mfma, 2) if m else None})
+    res["exp"] = ex
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -312,10 +404,19 @@ def main():
                     help="only time the paged-KV write path on the workload's page lists: each "
                          "request's newest token appended (decode) or its chunk written (prefill), "
                          "K and V pools, and a copy-on-write page copy per request")
+    ap.add_argument("--probe", action="store_true",
+                    help="only run the context microbenchmarks: random 4 KB tile reads with the suffix "
+                         "pass's loads, the bf16 MFMA rate and the v_exp_f32 rate")
     ap.add_argument("--gather", action="store_true",
                     help="only time the page gather of the workload's whole working set (every "
                          "segment, K and V pools) into dense token-major buffers")
     args = ap.parse_args()
+    if args.probe:
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        probe_bench(args)
+        return
     if args.gather:
         if args.gpus != 1:
             print("bench.py measures one GPU only", file=sys.stderr)

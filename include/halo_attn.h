@@ -115,6 +115,50 @@ halo_status_t halo_plan_create(const halo_attn_params_t* params,
                                size_t* device_meta_bytes,
                                size_t* workspace_bytes);
 
+/* Tuning of the work decomposition (every field 0 or -1 means "chosen by
+ * the planner from the batch"). The result never depends on these: any
+ * valid setting gives the same attention, up to summation order.
+ *   kc_shared        keys per chunk of a shared segment in narrow items
+ *                    (multiple of 32, <= 1024; 0: 512)
+ *   kc_private       keys per chunk of a request's private keys (multiple of
+ *                    32, <= 1024; 0: 1024, 512 or 256, the longest that
+ *                    leaves >= 3 items per CU)
+ *   wide             -1: wide items (256-row MFMA workgroups over one key
+ *                    stream) when the shared work is large; 0: never; 1:
+ *                    always (bf16 only)
+ *   wide_rows        rows per wide item (multiple of 32, <= 256; 0: from the
+ *                    sharing groups' sizes; prefill: 256)
+ *   kc_wide          keys per chunk of a shared segment in wide items
+ *                    (multiple of 32; 0: the longest of 2048, 1024, ... that
+ *                    gives >= wide_min_items items)
+ *   wide_min_items   see kc_wide (0: 128)
+ *   shared_unit      narrow items of one shared chunk kept together on one
+ *                    workgroup (0: 4)
+ *   items_per_block  narrow items per workgroup, at most one per wave
+ *                    (0: one per wave, 8 for bf16 and 4 for fp32) */
+typedef struct {
+  int32_t kc_shared;
+  int32_t kc_private;
+  int32_t wide;
+  int32_t wide_rows;
+  int32_t kc_wide;
+  int32_t wide_min_items;
+  int32_t shared_unit;
+  int32_t items_per_block;
+} halo_plan_options_t;
+
+/* Fill *options with the defaults (every field "chosen by the planner"). */
+void halo_plan_options_default(halo_plan_options_t* options);
+
+/* halo_plan_create with explicit tuning options (NULL: the defaults). An
+ * out-of-range option is rejected with HALO_ERR_INVALID_ARGUMENT. */
+halo_status_t halo_plan_create_with_options(const halo_attn_params_t* params,
+                                            const halo_forest_t* forest,
+                                            const halo_plan_options_t* options,
+                                            halo_plan_t** plan,
+                                            size_t* device_meta_bytes,
+                                            size_t* workspace_bytes);
+
 /* Copy the plan's metadata (page ids, work lists) into device_meta, a caller-owned 256-byte aligned device buffer of at least
  * device_meta_bytes, asynchronously on stream. The plan must stay alive
  * until the copy has completed. */

@@ -18,6 +18,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libhalo_attn.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
+# Context microbenchmarks (measurement only), a library of their own.
+PROBE_LIB_PATH = os.path.join(PKG, "libhalo_probe.so")
 DRIVER_SRC = os.path.join(ROOT, "tests", "abi_driver", "decode.cpp")
 DRIVER_BIN = os.path.join(ROOT, "tests", "abi_driver", "decode")
 
@@ -49,6 +51,7 @@ def build(verbose=True):
         forest_o = os.path.join(tmp, "halo_forest.o")
         kern_o = os.path.join(tmp, "halo_kernels.o")
         pages_o = os.path.join(tmp, "halo_pages.o")
+        probe_o = os.path.join(tmp, "halo_probe.o")
         procs = [
             subprocess.Popen(["g++", "-std=c++17", "-O2", "-fPIC", "-Wall", "-Wextra",
                               "-I", INCLUDE, "-c", os.path.join(CSRC, "halo_plan.cpp"), "-o", plan_o]),
@@ -58,6 +61,8 @@ def build(verbose=True):
                                                    os.path.join(CSRC, "halo_kernels.hip"), "-o", kern_o]),
             subprocess.Popen([HIPCC] + HIP_FLAGS + ["-I", INCLUDE, "-c",
                                                    os.path.join(CSRC, "halo_pages.hip"), "-o", pages_o]),
+            subprocess.Popen([HIPCC] + HIP_FLAGS + ["-I", INCLUDE, "-c",
+                                                   os.path.join(CSRC, "halo_probe.hip"), "-o", probe_o]),
         ]
         rcs = [p.wait() for p in procs]
         if any(rcs):
@@ -65,6 +70,9 @@ def build(verbose=True):
         out_tmp = LIB_PATH + ".tmp"
         _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", plan_o, forest_o, kern_o, pages_o, "-o", out_tmp])
         os.replace(out_tmp, LIB_PATH)
+        probe_tmp = PROBE_LIB_PATH + ".tmp"
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", probe_o, "-o", probe_tmp])
+        os.replace(probe_tmp, PROBE_LIB_PATH)
         # the C-ABI driver of the tests (host code against the built library)
         _run(["g++", "-std=c++17", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE,
               "-I", "/opt/rocm/include", DRIVER_SRC, "-o", DRIVER_BIN, "-L", PKG, "-lhalo_attn",

@@ -120,9 +120,7 @@ struct halo_plan {
   int32_t wide_rb = 0;       // 1 when the plan has wide items (32 rows per wave), else 0
   int32_t wide_group = 1;    // wide items that share pages, kept on one XCD
   int32_t n_narrow_blocks = 0;  // workgroups the narrow items are dealt to (a multiple of 8)
-  int32_t narrow_slots = 0;     // item slots per narrow workgroup (slot k: waves
-                                // k*narrow_split .. k*narrow_split + narrow_split - 1)
-  int32_t narrow_split = 1;     // waves sharing one narrow item
+  int32_t narrow_slots = 0;     // item slots per narrow workgroup (slot k: wave k)
   int32_t n_shared_items = 0;
   int32_t n_merge = 0;
   int32_t n_spans = 0;

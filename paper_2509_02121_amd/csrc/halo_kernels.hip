@@ -46,8 +46,6 @@ typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLn2 = 0.69314718055994530942f;
-// Most waves that may share one narrow item.
-constexpr int kMaxSplit = 8;
 constexpr float kLog2e = 1.44269504088896340736f;
 
 // ---------------------------------------------------------------- fragments
@@ -215,8 +213,7 @@ struct AttnArgs {
   int32_t n_wide;
   int32_t wide_blocks;     // grid blocks of the wide role (n_wide padded, see xcd_remap)
   int32_t narrow_blocks;   // grid blocks of the narrow role (a multiple of 8)
-  int32_t narrow_slots;    // item slots per narrow workgroup
-  int32_t narrow_split;    // waves sharing one narrow item (block waves / narrow_slots)
+  int32_t narrow_slots;    // item slots per narrow workgroup (one per wave)
   int32_t wide_group;      // consecutive wide items kept on one XCD
   int32_t num_kv_heads;
   float scale_log2;   // sm_scale * log2(e)
@@ -297,13 +294,8 @@ struct StepRegs {
 //  * Loads are software-pipelined: the operands of step i+1 are in flight
 //    while step i is computed, and the next span's page ids are loaded when
 //    its predecessor starts.
-//  * split > 1: `split` waves share the item, wave `part` walking the item's
-//    steps part, part + split, ...; instead of writing the output it leaves
-//    its unnormalized accumulator, running max and sum in `red` (LDS) for
-//    merge_split.
 template <typename T, int D, typename TO, bool NT, int P>
-__device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, const ItemRec* rec, int lane,
-                                         int split, int part, float* red) {
+__device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, const ItemRec* rec, int lane) {
   using F = typename FragOf<T>::type;
   constexpr int NS = D / 32;   // QK steps over d
   constexpr int NB = D / 16;   // PV output blocks over d
@@ -384,7 +376,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
   cur.ke = it.s0_key_end;
   cur.causal = it.s0_causal;
   cur.vpid = vpid0;
-  int gs = part;   // index of this wave's next step among the item's steps
+  int gs = 0;      // index of the next step among the item's steps
   int sb = 0;      // index of cur's first step
   auto advance = [&]() {
     // position of the next step to issue, moving on to the span holding it
@@ -395,7 +387,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
       wait_vmcnt<0>();
     }
     StepPos p = step_at(cur, cur.kb + (gs - sb) * kKeysPerStep);
-    gs += split;
+    ++gs;
     return p;
   };
 
@@ -494,16 +486,6 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
   }
 
   lsum = rows_sum(lsum);
-  if (split > 1) {
-    // red: [NB][64 lanes][4] accumulator, then per row its max and sum
-#pragma unroll
-    for (int b = 0; b < NB; ++b) *reinterpret_cast<f32x4_t*>(red + (b * 64 + lane) * 4) = acc[b];
-    if (grp == 0) {
-      red[NB * 256 + col] = m;
-      red[NB * 256 + 16 + col] = lsum;
-    }
-    return;
-  }
   const bool has_row = col < it.n_rows;
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   const float lse2 = lsum > 0.f ? m + __log2f(lsum) : kNegInf;
@@ -528,80 +510,20 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
 // one wave per SIMD.
 template <typename T> constexpr int block_waves() { return sizeof(T) == 2 ? 8 : 4; }
 
-// Floats of one wave's hand-off area for a shared item: the [D/16][64][4]
-// accumulator, then 16 row maxima and 16 row sums.
-template <int D> constexpr int red_floats() { return (D / 16) * 256 + 32; }
-
-// Combines the `split` partial results that the waves of one item left in
-// LDS (red0: the first of them), with the exact rule
-//   M = max_q m_q, s_q = 2^(m_q - M), O = sum_q s_q acc_q / sum_q s_q l_q,
-// and writes the item's rows. Wave `part` of the item writes the output
-// blocks part, part + split, ... (the LSE with part 0).
-template <typename T, int D, typename TO>
-__device__ __forceinline__ void merge_split(const AttnArgs& a, const Item& it, const ItemRec* rec, int lane,
-                                            int split, int part, const float* red0) {
-  constexpr int NB = D / 16;
-  constexpr int kRed = red_floats<D>();
-  const int col = lane & 15, grp = lane >> 4;
-  float sq[kMaxSplit];
-  float M = kNegInf;
-#pragma unroll
-  for (int q = 0; q < kMaxSplit; ++q) {
-    sq[q] = q < split ? red0[q * kRed + NB * 256 + col] : kNegInf;
-    M = fmaxf(M, sq[q]);
-  }
-  float L = 0.f;
-#pragma unroll
-  for (int q = 0; q < kMaxSplit; ++q) {
-    sq[q] = (q < split && sq[q] != kNegInf) ? __builtin_amdgcn_exp2f(sq[q] - M) : 0.f;
-    if (q < split) L += sq[q] * red0[q * kRed + NB * 256 + 16 + col];
-  }
-  const bool has_row = col < it.n_rows;
-  if (!has_row) return;
-  const int q_row = rec->q_row[col];
-  const int64_t slot = rec->aux[col];
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-  const float lse2 = L > 0.f ? M + __log2f(L) : kNegInf;
-  for (int b = part; b < NB; b += split) {
-    f32x4_t o = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int q = 0; q < kMaxSplit; ++q)
-      if (q < split) o += sq[q] * *reinterpret_cast<const f32x4_t*>(red0 + q * kRed + (b * 64 + lane) * 4);
-    o *= inv;
-    if (it.part_base >= 0) store4_nt(a.part_o + slot * D + 16 * b + 4 * grp, o);
-    else store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 16 * b + 4 * grp, o);
-  }
-  if (part == 0 && grp == 0) {
-    if (it.part_base >= 0) __builtin_nontemporal_store(lse2, a.part_lse + slot);
-    else if (a.lse) a.lse[q_row] = lse2 == kNegInf ? kNegInf : lse2 * kLn2;
-  }
-}
-
 // Narrow workgroup `block` runs the items in its narrow_slots slots (dealt
-// by the planner; n_rows = 0 marks an empty slot). With narrow_split = 1
-// each wave runs one item and waves of empty slots exit. With
-// narrow_split = s > 1, waves s*k .. s*k + s - 1 share item k: they walk its
-// steps interleaved, hand their partial results over in LDS and merge them,
-// so an item's chain of dependent steps is s times shorter.
+// by the planner; n_rows = 0 marks an empty slot), one per wave; waves of
+// empty slots exit.
 template <typename T, int D, typename TO>
-__device__ __forceinline__ void narrow_block(const AttnArgs& a, int block, float* red_all) {
+__device__ __forceinline__ void narrow_block(const AttnArgs& a, int block) {
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
-  const int split = a.narrow_split;
-  const int slot = wave / split, part = wave - slot * split;
-  const int64_t item_id = (int64_t)block * a.narrow_slots + slot;
+  const int64_t item_id = (int64_t)block * a.narrow_slots + wave;
+  if (wave >= a.narrow_slots) return;
   const Item it = a.items[item_id];
+  if (it.n_rows <= 0) return;
   const ItemRec* rec = a.item_recs + item_id;
-  const bool has = it.n_rows > 0;
-  if (split == 1 && !has) return;
-  if (has) {
-    float* red = red_all + wave * red_floats<D>();
-    if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, rec, lane, split, part, red);
-    else run_item<T, D, TO, false, 2>(a, it, rec, lane, split, part, red);
-  }
-  if (split == 1) return;
-  __syncthreads();
-  if (has) merge_split<T, D, TO>(a, it, rec, lane, split, part, red_all + slot * split * red_floats<D>());
+  if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, rec, lane);
+  else run_item<T, D, TO, false, 2>(a, it, rec, lane);
 }
 
 // ---------------------------------------------------------------- wide items
@@ -1027,10 +949,8 @@ __global__ __launch_bounds__(64 * block_waves<T>())
 __attribute__((amdgpu_waves_per_eu(block_waves<T>() / 4)))
 void attn_kernel(AttnArgs a) {
   static_assert(RB == 0 || block_waves<T>() == kWideWaves, "wide items need kWideWaves-wave blocks");
-  // one LDS area for whichever role the block takes: the wide ring, or the
-  // hand-off of shared narrow items
-  constexpr int kRedBytes = block_waves<T>() * red_floats<D>() * 4;
-  constexpr int kSmem = RB > 0 && wide_ring_bytes<D>() > kRedBytes ? wide_ring_bytes<D>() : kRedBytes;
+  // the wide role's LDS ring (narrow items use no LDS)
+  constexpr int kSmem = RB > 0 ? wide_ring_bytes<D>() : 16;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kSmem];
   const int b = blockIdx.x;
   const int x = b & 7, r = b >> 3;
@@ -1044,9 +964,10 @@ void attn_kernel(AttnArgs a) {
       if (item < a.n_wide) wide_item<D, TO>(a, item, smem);
       return;
     }
-    narrow_block<T, D, TO>(a, (r - w_upto) * 8 + x, reinterpret_cast<float*>(smem));
+    narrow_block<T, D, TO>(a, (r - w_upto) * 8 + x);
   } else {
-    narrow_block<T, D, TO>(a, b, reinterpret_cast<float*>(smem));
+    (void)smem;
+    narrow_block<T, D, TO>(a, b);
   }
 }
 
@@ -1230,7 +1151,7 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                 reinterpret_cast<const Item*>(m + L.wide_items),
                 reinterpret_cast<const Span*>(m + L.spans),
                 reinterpret_cast<const Row*>(m + L.rows),
-                plan->n_items, plan->n_wide, 0, plan->n_narrow_blocks, plan->narrow_slots, plan->narrow_split,
+                plan->n_items, plan->n_wide, 0, plan->n_narrow_blocks, plan->narrow_slots,
                 plan->wide_group,
                 p.num_kv_heads, p.sm_scale * kLog2e};
   MergeArgs margs{part_o, part_lse,

@@ -39,15 +39,6 @@ thread_local std::string g_last_error;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-int env_int(const char* name, int dflt, int lo, int hi) {
-  const char* v = getenv(name);
-  if (!v || !*v) return dflt;
-  long x = strtol(v, nullptr, 10);
-  if (x < lo) x = lo;
-  if (x > hi) x = hi;
-  return (int)x;
-}
-
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 }  // namespace
 
@@ -169,13 +160,56 @@ void pieces(int32_t seg, int32_t len, int32_t chunk, std::vector<Span>& out) {
 
 }  // namespace
 
+extern "C" void halo_plan_options_default(halo_plan_options_t* o) {
+  if (!o) return;
+  o->kc_shared = 0;
+  o->kc_private = 0;
+  o->wide = -1;
+  o->wide_rows = 0;
+  o->kc_wide = 0;
+  o->wide_min_items = 0;
+  o->shared_unit = 0;
+  o->items_per_block = 0;
+}
+
+namespace {
+halo_status_t check_options(const halo_plan_options_t& o) {
+  auto bad = [](const char* what) { return fail(HALO_ERR_INVALID_ARGUMENT, std::string("options: ") + what); };
+  if (o.kc_shared < 0 || o.kc_shared % 32 || o.kc_shared > kMaxSpanKeys)
+    return bad("kc_shared is 0 or a multiple of 32 up to 1024");
+  if (o.kc_private < 0 || o.kc_private % 32 || o.kc_private > kMaxSpanKeys)
+    return bad("kc_private is 0 or a multiple of 32 up to 1024");
+  if (o.wide < -1 || o.wide > 1) return bad("wide is -1, 0 or 1");
+  if (o.wide_rows < 0 || o.wide_rows % 32 || o.wide_rows > kMaxWideRows)
+    return bad("wide_rows is 0 or a multiple of 32 up to 256");
+  if (o.kc_wide < 0 || o.kc_wide % 32 || o.kc_wide > (1 << 16)) return bad("kc_wide is 0 or a multiple of 32 up to 65536");
+  if (o.wide_min_items < 0) return bad("wide_min_items must be >= 0");
+  if (o.shared_unit < 0 || o.shared_unit > 64) return bad("shared_unit is 0..64");
+  if (o.items_per_block < 0 || o.items_per_block > 8) return bad("items_per_block is 0..8");
+  return HALO_OK;
+}
+}  // namespace
+
 extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
                                           const halo_forest_t* forest, halo_plan_t** plan_out,
                                           size_t* device_meta_bytes, size_t* workspace_bytes) {
+  return halo_plan_create_with_options(params, forest, nullptr, plan_out, device_meta_bytes, workspace_bytes);
+}
+
+extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t* params,
+                                                       const halo_forest_t* forest,
+                                                       const halo_plan_options_t* options,
+                                                       halo_plan_t** plan_out, size_t* device_meta_bytes,
+                                                       size_t* workspace_bytes) {
   clear_error();
   if (!plan_out) return fail(HALO_ERR_INVALID_ARGUMENT, "plan must not be NULL");
   *plan_out = nullptr;
-  halo_status_t st = validate(params, forest);
+  halo_plan_options_t opt;
+  halo_plan_options_default(&opt);
+  if (options) opt = *options;
+  halo_status_t st = check_options(opt);
+  if (st != HALO_OK) return st;
+  st = validate(params, forest);
   if (st != HALO_OK) return st;
   const halo_attn_params_t& p = *params;
   const halo_forest_t& f = *forest;
@@ -224,7 +258,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   int32_t n_chunks = 0;
 
   if (!prefill) {
-    const int kc_shared = env_int("HALO_KC_SHARED", 512, 32, kMaxSpanKeys) / 32 * 32;
+    const int kc_shared = opt.kc_shared > 0 ? opt.kc_shared : 512;
     // Private chunks: the longest of 1024, 512 and 256 keys that still
     // leaves >= 3 items per CU (longer chunks write and merge fewer
     // partials; with fewer items a CU has too few loads in flight), else 256.
@@ -244,7 +278,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         kc_private_default = kc;
         break;
       }
-    const int kc_private = env_int("HALO_KC_PRIVATE", kc_private_default, 32, kMaxSpanKeys) / 32 * 32;
+    const int kc_private = opt.kc_private > 0 ? opt.kc_private : kc_private_default;
     for (int r = 0; r < R; ++r) {
       int64_t keys = 0;
       for (int32_t i = path_begin(r); i < path_end(r); ++i) keys += f.seg_len[f.req_seg_ids[i]];
@@ -271,9 +305,8 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         wsum += w;
         wrows += w * (double)refs[s] * G;
       }
-    const int wide_env = env_int("HALO_WIDE", -1, 0, 1);
     const bool wide = p.kv_dtype == HALO_BF16 &&
-                      (wide_env == 1 || (wide_env == -1 && shared_work >= 16.0 * (1 << 20)));
+                      (opt.wide == 1 || (opt.wide == -1 && shared_work >= 16.0 * (1 << 20)));
     int rows_per = kRowsPerItem;
     int kc = kc_shared;
     if (wide) {
@@ -282,11 +315,11 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
       // rows per wide item: the row-weighted group size rounded up to whole
       // 32-row waves, at most one workgroup
       rows_per = (int)std::min<double>(kMaxWideRows, std::max(32.0, std::ceil(avg_rows / 32.0) * 32.0));
-      rows_per = env_int("HALO_WIDE_ROWS", rows_per, 32, kMaxWideRows) / 32 * 32;
+      if (opt.wide_rows > 0) rows_per = opt.wide_rows;
       // row groups of one shared chunk read the same pages: keep up to 8 of
       // them on one XCD
       plan->wide_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / rows_per)));
-      const int min_items = env_int("HALO_WIDE_MIN_ITEMS", 128, 1, 1 << 30);
+      const int min_items = opt.wide_min_items > 0 ? opt.wide_min_items : 128;
       kc = 2 * kMaxSpanKeys;
       while (kc > 128) {
         int64_t n = 0;
@@ -296,7 +329,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
         if (n >= min_items) break;
         kc /= 2;
       }
-      kc = env_int("HALO_KC_WIDE", kc, 32, 1 << 16) / 32 * 32;
+      if (opt.kc_wide > 0) kc = opt.kc_wide;
     }
     for (int s = 0; s < S; ++s) {
       if (refs[s] < 2 || f.seg_len[s] == 0) continue;
@@ -362,10 +395,10 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
     }
   } else {
     // Prefill: bf16 rows go to wide items of up to kMaxWideRows (query, head) rows.
-    const bool wide = p.kv_dtype == HALO_BF16 && env_int("HALO_WIDE", 1, 0, 1) == 1;
+    const bool wide = p.kv_dtype == HALO_BF16 && opt.wide != 0;
     plan->wide_rb = wide ? 1 : 0;
     plan->wide_group = 1;
-    const int rows_per = wide ? env_int("HALO_WIDE_ROWS", kMaxWideRows, 32, kMaxWideRows) / 32 * 32 : kRowsPerItem;
+    const int rows_per = wide ? (opt.wide_rows > 0 ? opt.wide_rows : kMaxWideRows) : kRowsPerItem;
     for (int r = 0; r < R; ++r) {
       const int32_t n = f.q_len[r];
       if (n == 0) continue;
@@ -542,7 +575,7 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   }
 
   // Narrow items are dealt to workgroups ahead of time: workgroup b has
-  // `slots` item slots (one per wave, or one per narrow_split waves), and
+  // `slots` item slots (one per wave), and
   // item b * slots + k, if not empty, runs in slot k. A CU ingests only
   // ~30 GB/s from HBM (~70 GB/s from L2), so a small batch is spread over
   // every CU (at least 256 workgroups of 8 waves, one per CU) and items go
@@ -556,18 +589,15 @@ extern "C" halo_status_t halo_plan_create(const halo_attn_params_t* params,
   if (!items.empty()) {
     const int waves = narrow_items_per_block(p.kv_dtype);
     const int64_t n = (int64_t)items.size();
-    int split = env_int("HALO_SPLIT", 1, 1, waves);
-    while (waves % split) --split;
-    plan->narrow_split = split;
-    const int slots = waves / split;
-    const int cap = env_int("HALO_ITEMS_PER_BLOCK", slots, 1, slots);
+    const int slots = waves;
+    const int cap = opt.items_per_block > 0 ? std::min(opt.items_per_block, slots) : slots;
     int64_t nb = std::max<int64_t>((n + cap - 1) / cap, std::min<int64_t>(n, kNumCUs));
     nb = (nb + 7) / 8 * 8;
     if (nb * slots > (int64_t)std::numeric_limits<int32_t>::max()) {
       delete plan;
       return fail(HALO_ERR_INVALID_ARGUMENT, "too many narrow work items");
     }
-    const int shared_unit = std::min(cap, env_int("HALO_SHARED_UNIT", 4, 1, 64));
+    const int shared_unit = std::min(cap, opt.shared_unit > 0 ? opt.shared_unit : 4);
     // work units: runs of up to shared_unit items of one chunk, or one item
     struct Unit { int32_t first, count, chunk; int64_t cost; };
     std::vector<Unit> units;

@@ -57,8 +57,17 @@ class PlanLayout(ctypes.Structure):
             "n_narrow_blocks", "narrow_slots")]
 
 
+class PlanOptions(ctypes.Structure):
+    """halo_plan_options_t: tuning of the work decomposition (0 / -1 = chosen
+    by the planner); see include/halo_attn.h."""
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "kc_shared", "kc_private", "wide", "wide_rows", "kc_wide", "wide_min_items", "shared_unit",
+        "items_per_block")]
+
+
 EXPORTED_SYMBOLS = (
-    "halo_plan_create", "halo_plan_upload", "halo_plan_destroy", "halo_plan_get_stats",
+    "halo_plan_create", "halo_plan_create_with_options", "halo_plan_options_default", "halo_plan_upload",
+    "halo_plan_destroy", "halo_plan_get_stats",
     "halo_plan_inspect",
     "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_prefix_attn_decode_noalloc",
     "halo_kv_page_gather",
@@ -117,6 +126,12 @@ def load_library(require_gpu=False):
     lib.halo_plan_create.argtypes = [ctypes.POINTER(AttnParams), ctypes.POINTER(Forest),
                                      ctypes.POINTER(vp), ctypes.POINTER(sz), ctypes.POINTER(sz)]
     lib.halo_plan_create.restype = ctypes.c_int
+    lib.halo_plan_create_with_options.argtypes = [ctypes.POINTER(AttnParams), ctypes.POINTER(Forest),
+                                                  ctypes.POINTER(PlanOptions), ctypes.POINTER(vp),
+                                                  ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    lib.halo_plan_create_with_options.restype = ctypes.c_int
+    lib.halo_plan_options_default.argtypes = [ctypes.POINTER(PlanOptions)]
+    lib.halo_plan_options_default.restype = None
     lib.halo_plan_upload.argtypes = [vp, vp, sz, vp]
     lib.halo_plan_upload.restype = ctypes.c_int
     lib.halo_plan_destroy.argtypes = [vp]
@@ -227,7 +242,9 @@ class Plan:
     """A validated forest plus the work lists of one batch step (host)."""
 
     def __init__(self, params, seg_len, seg_page_indptr, seg_page_ids, req_seg_indptr,
-                 req_seg_ids, q_len=None):
+                 req_seg_ids, q_len=None, options=None):
+        """options: None (the planner's choices) or a dict of
+        halo_plan_options_t fields to set."""
         lib = load_library()
         self.params = params
         keep = [_i32(x) for x in (seg_len, seg_page_indptr, seg_page_ids, req_seg_indptr,
@@ -239,8 +256,17 @@ class Plan:
         meta = ctypes.c_size_t()
         ws = ctypes.c_size_t()
         self._handle = None
-        _check(lib.halo_plan_create(ctypes.byref(params), ctypes.byref(forest), ctypes.byref(handle),
-                                    ctypes.byref(meta), ctypes.byref(ws)))
+        opts = None
+        if options:
+            opts = PlanOptions()
+            lib.halo_plan_options_default(ctypes.byref(opts))
+            for k, v in options.items():
+                if k not in dict(PlanOptions._fields_):
+                    raise ValueError(f"unknown plan option {k}")
+                setattr(opts, k, int(v))
+        _check(lib.halo_plan_create_with_options(ctypes.byref(params), ctypes.byref(forest),
+                                                 ctypes.byref(opts) if opts is not None else None,
+                                                 ctypes.byref(handle), ctypes.byref(meta), ctypes.byref(ws)))
         self._handle = handle
         self._keep = keep
         self.device_meta_bytes = meta.value
@@ -249,9 +275,9 @@ class Plan:
         self.num_query_rows = int(self.stats()["num_query_rows"])
 
     @classmethod
-    def from_csr(cls, params, csr):
+    def from_csr(cls, params, csr, options=None):
         return cls(params, csr["seg_len"], csr["seg_page_indptr"], csr["seg_page_ids"],
-                   csr["req_seg_indptr"], csr["req_seg_ids"], csr.get("q_len"))
+                   csr["req_seg_indptr"], csr["req_seg_ids"], csr.get("q_len"), options)
 
     def stats(self):
         st = PlanStats()
@@ -616,10 +642,10 @@ class PrefixAttention:
     current stream and returns (o, lse).
     """
 
-    def __init__(self, params, csr, device="cuda"):
+    def __init__(self, params, csr, device="cuda", options=None):
         import torch
         load_library(require_gpu=True)
-        self.plan = Plan.from_csr(params, csr)
+        self.plan = Plan.from_csr(params, csr, options)
         self.device = torch.device(device)
         self.meta = torch.empty(max(self.plan.device_meta_bytes, 256), dtype=torch.uint8, device=self.device)
         self.workspace = (torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=self.device)

@@ -18,8 +18,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "halo_attn.h")
 
 
-def _declared_functions():
-    text = open(HEADER).read()
+def _declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return set(re.findall(r"\b(halo_[a-z_]+)\s*\(", text))
 
@@ -39,6 +39,20 @@ def test_library_exports_every_declared_symbol(lib):
     assert not missing, missing
     for name in declared:
         assert getattr(lib, name) is not None
+
+
+def test_probe_library_exports_every_declared_symbol():
+    """The context microbenchmark library (include/halo_probe.h) loads
+    without a GPU and exports what its header declares."""
+    from paper_2509_02121_amd import probe
+    declared = _declared_functions(os.path.join(ROOT, "include", "halo_probe.h"))
+    assert declared == set(probe.EXPORTED_SYMBOLS)
+    plib = probe.load()
+    out = subprocess.run(["nm", "-D", "--defined-only", probe.PROBE_LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    assert declared <= set(re.findall(r"\b(halo_[a-z_]+)\b", out))
+    for name in declared:
+        assert getattr(plib, name) is not None
 
 
 @pytest.mark.parametrize("lang,std", [("c", "-std=c99"), ("c++", "-std=c++11")])
@@ -101,7 +115,7 @@ def _check_plan(w, plan):
     slot_items = m["items"].reshape(-1, 16)
     assert len(slot_items) == m["n_narrow_blocks"] * m["narrow_slots"] and m["n_narrow_blocks"] % 8 == 0
     waves = 8 if w.dtype.itemsize == 2 else 4
-    assert m["narrow_slots"] in (0, 1, 2, 4, 8) and m["narrow_slots"] <= waves
+    assert m["narrow_slots"] in (0, waves)
     used = slot_items[:, 1] > 0
     recs = m["item_recs"].reshape(-1, 64)
     for it, rc in zip(slot_items[used], recs[used]):
@@ -215,12 +229,11 @@ def test_plan_covers_configs(lib, index):
         assert plan.workspace_bytes == 0 and len(m["merge_rows"]) == 0
 
 
-def test_plan_merge_overflow_slots(lib, monkeypatch):
+def test_plan_merge_overflow_slots(lib):
     """Short shared chunks give every Llama-8B-shaped row more than 8
     partials: the first 8 at fixed slots, the rest in the overflow range."""
-    monkeypatch.setenv("HALO_KC_SHARED", "96")
     w = make_config(1)
-    plan = halo.Plan.from_csr(_params(w), w.forest_csr())
+    plan = halo.Plan.from_csr(_params(w), w.forest_csr(), {"kc_shared": 96})
     m = _check_plan(w, plan)
     assert np.diff(m["merge_indptr"]).min() > 8
 
@@ -456,3 +469,42 @@ def test_binding_rejects_buffers_smaller_than_the_plan(lib):
         halo.kv_page_scatter_kv(kp, kp[:-1], params, i32, i32, i32, i32, i64, kp, kp)
     with pytest.raises(ValueError, match="pool has"):
         halo.kv_page_copy(kp[:-1], params, i32, i32)
+
+
+def test_plan_options_are_checked(lib):
+    """Tuning options change the work decomposition only; out-of-range ones
+    are refused."""
+    params = halo.AttnParams(4, 2, 64, 16, 3, halo.HALO_F32, halo.HALO_F32, 0.125)
+    csr = _csr(GOOD["seg_len"], GOOD["pages"], GOOD["paths"])
+    for bad in ({"kc_shared": 100}, {"kc_shared": 2048}, {"kc_private": 1056}, {"wide": 2},
+                {"wide_rows": 48}, {"kc_wide": -32}, {"wide_min_items": -1}, {"shared_unit": 65},
+                {"items_per_block": 9}):
+        with pytest.raises(halo.HaloError) as e:
+            halo.Plan.from_csr(params, csr, bad)
+        assert e.value.status == halo.HALO_ERR_INVALID_ARGUMENT and "options" in str(e.value)
+    with pytest.raises(ValueError):
+        halo.Plan.from_csr(params, csr, {"no_such_option": 1})
+
+
+@pytest.mark.parametrize("opts", [{"wide": 1, "wide_rows": 64, "kc_wide": 256}, {"wide": 0},
+                                  {"kc_shared": 96, "shared_unit": 1}, {"kc_private": 64, "items_per_block": 3},
+                                  {"wide": 1, "wide_min_items": 100000}, {"kc_private": 1024}])
+def test_plan_options_keep_the_coverage(lib, opts):
+    w = make_config(1)
+    _check_plan(w, halo.Plan.from_csr(_params(w), w.forest_csr(), opts))
+
+
+def test_plan_options_change_the_decomposition(lib):
+    """Each option reaches the planner: the work lists differ from the
+    default plan's in the way the option names."""
+    w = make_config(1)
+    def inspect(opts=None):
+        return halo.Plan.from_csr(_params(w), w.forest_csr(), opts).inspect()
+    base = inspect()
+    wide, narrow = inspect({"wide": 1}), inspect({"wide": 0})
+    assert len(wide["wide_items"]) > 0 and len(narrow["wide_items"]) == 0
+    few = inspect({"items_per_block": 2})
+    per_block = (few["items"].reshape(-1, few["narrow_slots"], 16)[:, :, 1] > 0).sum(axis=1)
+    assert per_block.max() <= 2 and base["n_narrow_blocks"] < few["n_narrow_blocks"]
+    short = inspect({"kc_private": 64})
+    assert len(short["spans"]) > len(base["spans"])
