@@ -215,6 +215,7 @@ struct AttnArgs {
   int32_t narrow_blocks;   // grid blocks of the narrow role (a multiple of 8)
   int32_t narrow_slots;    // item slots per narrow workgroup (one per wave)
   int32_t wide_group;      // consecutive wide items kept on one XCD
+  int32_t wide_span;       // launch rounds (of 8 blocks) the wide rounds are spread over
   int32_t num_kv_heads;
   float scale_log2;   // sm_scale * log2(e)
 };
@@ -939,11 +940,12 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
 // prefix or prefill work) and narrow ones (lists of one-wave items, mostly
 // HBM-bound suffix streaming), so the two kinds of work overlap on the GPU.
 // RB = 0: no wide role.
-// The grid is dealt in rounds of 8 blocks (one per XCD); rounds of the two
-// roles are spread evenly over the launch so every CU mixes MFMA-heavy wide
-// blocks with HBM-heavy narrow ones, and within a role the block index modulo
-// 8 still names the XCD (xcd_remap, and the planner's dealing of narrow
-// items to XCDs, rely on it).
+// The grid is dealt in rounds of 8 blocks (one per XCD); the wide rounds
+// are spread evenly over the first wide_span rounds, so CUs mix MFMA-heavy
+// wide blocks with HBM-heavy narrow ones, and the launch ends on narrow
+// blocks (dealt longest first, so its tail is short ones). Within a role
+// the block index modulo 8 still names the XCD (xcd_remap, and the
+// planner's dealing of narrow items to XCDs, rely on it).
 template <typename T, int D, typename TO, int RB>
 __global__ __launch_bounds__(64 * block_waves<T>())
 __attribute__((amdgpu_waves_per_eu(block_waves<T>() / 4)))
@@ -956,9 +958,9 @@ void attn_kernel(AttnArgs a) {
   const int x = b & 7, r = b >> 3;
   if constexpr (RB > 0) {
     const int wr = a.wide_blocks >> 3;
-    const int tr = wr + (a.narrow_blocks >> 3);
-    const int w_before = (int)((int64_t)r * wr / tr);
-    const int w_upto = (int)((int64_t)(r + 1) * wr / tr);
+    const int sp = a.wide_span;
+    const int w_before = r < sp ? (int)((int64_t)r * wr / sp) : wr;
+    const int w_upto = r < sp ? (int)((int64_t)(r + 1) * wr / sp) : wr;
     if (w_upto > w_before) {
       const int item = xcd_remap(w_before * 8 + x, a.wide_group);
       if (item < a.n_wide) wide_item<D, TO>(a, item, smem);
@@ -1091,10 +1093,18 @@ halo_status_t hip_check(const char* what) {
 
 int pad_to(int n, int m) { return (n + m - 1) / m * m; }
 
+// Share (percent) of the narrow rounds interleaved with the wide ones; the
+// rest run after the last wide round.
+constexpr int kWideSpanNarrowPct = 80;
+
 template <typename T, int D, typename TO>
 void launch_attention(AttnArgs args, const MergeArgs& margs, int wide_rb, hipStream_t stream) {
   const int rb = sizeof(T) == 2 ? wide_rb : 0;
   args.wide_blocks = (rb > 0 && args.n_wide > 0) ? pad_to(args.n_wide, 8 * args.wide_group) : 0;
+  {
+    const int wr = args.wide_blocks / 8, nr = args.narrow_blocks / 8;
+    args.wide_span = wr + (int)((int64_t)nr * kWideSpanNarrowPct / 100);
+  }
   constexpr int W = block_waves<T>();
   const int grid = args.wide_blocks + args.narrow_blocks;
   if (grid > 0) {
@@ -1152,7 +1162,7 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                 reinterpret_cast<const Span*>(m + L.spans),
                 reinterpret_cast<const Row*>(m + L.rows),
                 plan->n_items, plan->n_wide, 0, plan->n_narrow_blocks, plan->narrow_slots,
-                plan->wide_group,
+                plan->wide_group, 0,
                 p.num_kv_heads, p.sm_scale * kLog2e};
   MergeArgs margs{part_o, part_lse,
                   reinterpret_cast<const int32_t*>(m + L.merge_rows),

@@ -575,15 +575,21 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   }
 
   // Narrow items are dealt to workgroups ahead of time: workgroup b has
-  // `slots` item slots (one per wave), and
-  // item b * slots + k, if not empty, runs in slot k. A CU ingests only
-  // ~30 GB/s from HBM (~70 GB/s from L2), so a small batch is spread over
-  // every CU (at least 256 workgroups of 8 waves, one per CU) and items go
-  // longest first to the least loaded workgroup. Beside wide workgroups,
-  // narrow ones fill half their slots. Workgroup b runs on XCD b % 8
-  // (dispatch is round-robin), and the row groups of one shared chunk go to
-  // workgroups of one XCD, in units of up to shared_unit items on one
-  // workgroup, so re-reads of the chunk hit that XCD's L2 or the CU's L1.
+  // `slots` item slots (one per wave), and item b * slots + k, if not empty,
+  // runs in slot k. Workgroup b runs on XCD b % 8 (dispatch is round-robin),
+  // and the row groups of one shared chunk go to workgroups of one XCD, in
+  // units of up to shared_unit items on one workgroup, so re-reads of the
+  // chunk hit that XCD's L2 or the CU's L1.
+  //  * One round (at most one workgroup per CU): a CU ingests only ~30 GB/s
+  //    from HBM (~70 GB/s from L2), so the batch is spread over every CU
+  //    (256 workgroups) and units go longest first to the least loaded
+  //    workgroup of their XCD.
+  //  * Several rounds: a workgroup holds its CU until its longest item ends
+  //    (a new 8-wave workgroup needs all its wave slots free), so each
+  //    workgroup gets units of about the same length: units are taken
+  //    longest first and fill the open workgroup of their XCD (shared) or
+  //    of the XCD with the fewest items (private). Workgroups then launch
+  //    longest first, and the short ones fill the tail.
   std::vector<ItemRec> recs;
   const int64_t n_real_items = (int64_t)items.size();
   if (!items.empty()) {
@@ -591,12 +597,13 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     const int64_t n = (int64_t)items.size();
     const int slots = waves;
     const int cap = opt.items_per_block > 0 ? std::min(opt.items_per_block, slots) : slots;
-    int64_t nb = std::max<int64_t>((n + cap - 1) / cap, std::min<int64_t>(n, kNumCUs));
-    nb = (nb + 7) / 8 * 8;
-    if (nb * slots > (int64_t)std::numeric_limits<int32_t>::max()) {
+    if (n > (int64_t)std::numeric_limits<int32_t>::max() / 2) {
       delete plan;
       return fail(HALO_ERR_INVALID_ARGUMENT, "too many narrow work items");
     }
+    const bool rounds = (int64_t)witems.size() + (n + cap - 1) / cap > kNumCUs;
+    int64_t nb = std::max<int64_t>((n + cap - 1) / cap, std::min<int64_t>(n, kNumCUs));
+    nb = (nb + 7) / 8 * 8;
     const int shared_unit = std::min(cap, opt.shared_unit > 0 ? opt.shared_unit : 4);
     // work units: runs of up to shared_unit items of one chunk, or one item
     struct Unit { int32_t first, count, chunk; int64_t cost; };
@@ -613,11 +620,42 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       }
     }
     std::stable_sort(units.begin(), units.end(), [](const Unit& a, const Unit& b) { return a.cost > b.cost; });
-    // one min-heap of (load, block) per XCD over the blocks with room left
+    std::vector<std::vector<int32_t>> blk;
+    if (rounds) {
+      // per XCD, its workgroups in launch order; the last one is open
+      std::vector<std::vector<std::vector<int32_t>>> xb(8);
+      std::vector<int64_t> xitems(8, 0);
+      for (const Unit& u : units) {
+        int x = 0;
+        if (u.chunk >= 0) {
+          x = u.chunk % 8;
+        } else {
+          for (int y = 1; y < 8; ++y)
+            if (xitems[y] < xitems[x]) x = y;
+        }
+        if (xb[x].empty() || (int)xb[x].back().size() + u.count > cap) xb[x].emplace_back();
+        for (int32_t k = 0; k < u.count; ++k) xb[x].back().push_back(u.first + k);
+        xitems[x] += u.count;
+      }
+      size_t per_xcd = 0;
+      for (int x = 0; x < 8; ++x) per_xcd = std::max(per_xcd, xb[x].size());
+      nb = 8 * (int64_t)per_xcd;
+      blk.assign(nb, {});
+      for (int x = 0; x < 8; ++x)
+        for (size_t j = 0; j < xb[x].size(); ++j) blk[j * 8 + x].swap(xb[x][j]);
+    }
+    if (nb * slots > (int64_t)std::numeric_limits<int32_t>::max()) {
+      delete plan;
+      return fail(HALO_ERR_INVALID_ARGUMENT, "too many narrow work items");
+    }
+    // one round: one min-heap of (load, block) per XCD over the blocks with
+    // room left
     using Slot = std::pair<int64_t, int32_t>;
     std::vector<std::priority_queue<Slot, std::vector<Slot>, std::greater<Slot>>> heap(8);
-    for (int32_t b = 0; b < (int32_t)nb; ++b) heap[b % 8].push(Slot{0, b});
-    std::vector<std::vector<int32_t>> blk(nb);
+    if (!rounds) {
+      blk.assign(nb, {});
+      for (int32_t b = 0; b < (int32_t)nb; ++b) heap[b % 8].push(Slot{0, b});
+    }
     // place `count` items from `first` on the least loaded block of XCD x
     // with room for them; false if there is none
     auto place_on = [&](int x, int32_t first, int32_t count, int64_t cost) {
@@ -645,6 +683,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       return x;
     };
     for (const Unit& u : units) {
+      if (rounds) break;
       if (u.chunk >= 0 && place_on(u.chunk % 8, u.first, u.count, u.cost)) continue;
       const int x = least_loaded_xcd();
       if (x >= 0 && place_on(x, u.first, u.count, u.cost)) continue;
