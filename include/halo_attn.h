@@ -121,15 +121,15 @@ halo_status_t halo_plan_create(const halo_attn_params_t* params,
  *   kc_shared        keys per chunk of a shared segment in narrow items
  *                    (multiple of 32, <= 1024; 0: 512)
  *   kc_private       keys per chunk of a request's private keys (multiple of
- *                    32, <= 1024; 0: 1024, 512 or 256, the longest that
- *                    leaves >= 3 items per CU)
+ *                    32, <= 65536; 0: 2048, 1024, 512 or 256, the longest
+ *                    that leaves >= 3 items per CU)
  *   wide             -1: wide items (256-row MFMA workgroups over one key
  *                    stream) when the shared work is large; 0: never; 1:
  *                    always (bf16 only)
  *   wide_rows        rows per wide item (multiple of 32, <= 256; 0: from the
  *                    sharing groups' sizes; prefill: 256)
  *   kc_wide          keys per chunk of a shared segment in wide items
- *                    (multiple of 32; 0: the longest of 2048, 1024, ... that
+ *                    (multiple of 32; 0: the longest of 4096, 2048, ... that
  *                    gives >= wide_min_items items)
  *   wide_min_items   see kc_wide (0: 128)
  *   shared_unit      narrow items of one shared chunk kept together on one

@@ -177,8 +177,8 @@ halo_status_t check_options(const halo_plan_options_t& o) {
   auto bad = [](const char* what) { return fail(HALO_ERR_INVALID_ARGUMENT, std::string("options: ") + what); };
   if (o.kc_shared < 0 || o.kc_shared % 32 || o.kc_shared > kMaxSpanKeys)
     return bad("kc_shared is 0 or a multiple of 32 up to 1024");
-  if (o.kc_private < 0 || o.kc_private % 32 || o.kc_private > kMaxSpanKeys)
-    return bad("kc_private is 0 or a multiple of 32 up to 1024");
+  if (o.kc_private < 0 || o.kc_private % 32 || o.kc_private > (1 << 16))
+    return bad("kc_private is 0 or a multiple of 32 up to 65536");
   if (o.wide < -1 || o.wide > 1) return bad("wide is -1, 0 or 1");
   if (o.wide_rows < 0 || o.wide_rows % 32 || o.wide_rows > kMaxWideRows)
     return bad("wide_rows is 0 or a multiple of 32 up to 256");
@@ -259,8 +259,8 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
 
   if (!prefill) {
     const int kc_shared = opt.kc_shared > 0 ? opt.kc_shared : 512;
-    // Private chunks: the longest of 1024, 512 and 256 keys that still
-    // leaves >= 3 items per CU (longer chunks write and merge fewer
+    // Private chunks: the longest of 2048, 1024, 512 and 256 keys that
+    // still leaves >= 3 items per CU (longer chunks write and merge fewer
     // partials; with fewer items a CU has too few loads in flight), else 256.
     auto private_items = [&](int64_t kc) {
       int64_t n = 0;
@@ -273,7 +273,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       return n;
     };
     int kc_private_default = 256;
-    for (int kc : {1024, 512})
+    for (int kc : {2048, 1024, 512})
       if (private_items(kc) >= 3 * kNumCUs) {
         kc_private_default = kc;
         break;
@@ -288,7 +288,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     // bf16 inputs and enough shared work the rows go to wide items (an 8-wave
     // workgroup reading each page once for up to 256 rows); the rows per item
     // follow the row-weighted size of the shared groups, and the key chunk
-    // (at most 2048 keys) shrinks until there are >= 128 wide items. Longer
+    // (at most 4096 keys) shrinks until there are >= 128 wide items. Longer
     // chunks mean fewer partials to write and merge, and a wide item's ring
     // start-up and 256-row epilogue are paid fewer times.
     std::vector<std::vector<int32_t>> seg_reqs(S);
@@ -320,7 +320,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       // them on one XCD
       plan->wide_group = (int)std::min<double>(8, std::max(1.0, std::ceil(avg_rows / rows_per)));
       const int min_items = opt.wide_min_items > 0 ? opt.wide_min_items : 128;
-      kc = 2 * kMaxSpanKeys;
+      kc = 4 * kMaxSpanKeys;
       while (kc > 128) {
         int64_t n = 0;
         for (int s = 0; s < S; ++s)

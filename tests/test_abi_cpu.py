@@ -476,7 +476,7 @@ def test_plan_options_are_checked(lib):
     are refused."""
     params = halo.AttnParams(4, 2, 64, 16, 3, halo.HALO_F32, halo.HALO_F32, 0.125)
     csr = _csr(GOOD["seg_len"], GOOD["pages"], GOOD["paths"])
-    for bad in ({"kc_shared": 100}, {"kc_shared": 2048}, {"kc_private": 1056}, {"wide": 2},
+    for bad in ({"kc_shared": 100}, {"kc_shared": 2048}, {"kc_private": 65568}, {"wide": 2},
                 {"wide_rows": 48}, {"kc_wide": -32}, {"wide_min_items": -1}, {"shared_unit": 65},
                 {"items_per_block": 9}):
         with pytest.raises(halo.HaloError) as e:
