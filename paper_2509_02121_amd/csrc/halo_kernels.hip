@@ -712,9 +712,7 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
       for (int b = 0; b < NO; ++b)
         vf[g][b] = __builtin_bit_cast(F, *reinterpret_cast<const u32x4_t*>(rd + (NK + g * NO + b) * 1024));
   };
-  auto pv = [&](const StepPos& p, const uint8_t* img, const F (&pf)[2]) {
-    F vf[2][NO];
-    read_v(img, vf);
+  auto mask_v = [&](const StepPos& p, F (&vf)[2][NO]) {
     if (p.t0 + kKeysPerStep > p.key_end) {
       const int lim = p.key_end - p.t0;
 #pragma unroll
@@ -732,6 +730,8 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
           vf[g][b] = __builtin_bit_cast(F, w);
         }
     }
+  };
+  auto pv = [&](const F (&vf)[2][NO], const F (&pf)[2]) {
 #pragma unroll
     for (int g = 0; g < 2; ++g)
 #pragma unroll
@@ -784,13 +784,16 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
   // One iteration on full, unmasked steps as a single basic block: the 16
   // MFMAs (P V of step t-1, Q K^T of step t+1) are interleaved with the
   // softmax VALU work of step t, so a wave keeps issuing independent VALU
-  // instructions while each MFMA runs. The accumulator rescale, which must
-  // wait for the P V products, is returned (move) and applied afterwards.
-  auto fast_iter = [&](const uint8_t* img_pv, const uint8_t* img_qk, const F (&pf_prev)[2],
+  // instructions while each MFMA runs. V of step t-1 arrives in registers
+  // (read during the previous iteration); the K reads of step t+1 go out
+  // first and arrive behind the P V products, and the V reads of step t,
+  // for the next iteration, go out behind the Q K^T products. The
+  // accumulator rescale, which must wait for the P V products, is returned
+  // (alpha) and applied afterwards.
+  auto fast_iter = [&](F (&vf)[2][NO], const uint8_t* img_qk, const uint8_t* img_v, const F (&pf_prev)[2],
                        const f32x16_t& sacc_cur, f32x16_t& sacc_nxt, F (&pf_cur)[2], float& alpha) {
     const uint8_t* rk = img_qk + lane * 16;
-    F vf[2][NO], kf[NK];
-    read_v(img_pv, vf);
+    F kf[NK];
 #pragma unroll
     for (int s = 0; s < NK; ++s) kf[s] = __builtin_bit_cast(F, *reinterpret_cast<const u32x4_t*>(rk + s * 1024));
 #pragma unroll
@@ -800,6 +803,7 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
     f32x16_t sn = f32x16_t{};
 #pragma unroll
     for (int s = 0; s < NK; ++s) sn = mma32(kf[s], qf[s], sn);
+    read_v(img_v, vf);
     // softmax of step t (no masks: full step); the max as a tree of
     // three-input maxima (v_max3_f32, 8 instructions for 16 scores)
     auto max3 = [](float x, float y, float z) { return fmaxf(fmaxf(x, y), z); };
@@ -838,21 +842,30 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
       asm volatile("" ::"v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]));
     }
     asm volatile("" ::"v"(lsum));
-    // schedule: all LDS reads first, then each MFMA followed by VALU work
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NO + NK, 0);
+    // schedule: the K reads, the P V MFMAs, then the Q K^T MFMAs with the V
+    // reads of step t after the first of them; each MFMA followed by VALU
+    // work
+    __builtin_amdgcn_sched_group_barrier(0x100, NK, 0);
 #pragma unroll
-    for (int k = 0; k < 2 * NO + NK; ++k) {
+    for (int k = 0; k < 2 * NO + 1; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NO, 0);
+#pragma unroll
+    for (int k = 0; k < NK - 1; ++k) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
     }
   };
 
   // ---- pipeline. Step t lives in stage t % S. Iteration t:
-  //   wait for this wave's loads of step t+1 (steps t+2..t+S-3 may still be
+  //   wait for this wave's loads of step t+1 (steps t+2..t+S-2 may still be
   //   in flight) and retire its LDS reads (lgkmcnt 0); barrier: step t+1 is
-  //   visible to every wave, and step t-2's stage is free (its V was read by
-  //   P V in iteration t-1); issue step t+S-2 into it;
-  //   MFMA: P V of step t-1, Q K^T of step t+1; VALU: softmax of step t.
+  //   visible to every wave, and step t-1's stage is free (its K was read in
+  //   iteration t-2, its V in iteration t-1); issue step t+S-1 into it;
+  //   MFMA: P V of step t-1 (V already in registers), Q K^T of step t+1;
+  //   VALU: softmax of step t; LDS: K of step t+1, V of step t.
   // Score and probability tiles alternate by step parity (S is even, so the
   // parity of each unrolled position is fixed). Positions past the end
   // re-load the current step's pages (in bounds, never read) so the count of
@@ -861,12 +874,13 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
   ps[0] = advance();
   if (ps[0].valid) {
 #pragma unroll
-    for (int i = 0; i < S - 2; ++i) {
+    for (int i = 0; i < S - 1; ++i) {
       if (i > 0) ps[i] = advance();
       issue(pick(ps[i].valid, ps[i], ps[0]), lds[i]);
     }
     f32x16_t sacc[2];
     F pf[2][2];
+    F vf[2][NO];
     wait_vmcnt<(S - 3) * kLoadsPerWave>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
@@ -876,27 +890,35 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
 #pragma unroll
       for (int st = 0; st < S; ++st) {
         const int cur_p = st & 1, nxt_p = cur_p ^ 1;
-        const int nx = (st + 1) % S, pv_st = (st + S - 1) % S, fr = (st + S - 2) % S;
-        wait_vmcnt<(S - 4) * kLoadsPerWave>();
+        const int nx = (st + 1) % S, pv_st = (st + S - 1) % S;
+        wait_vmcnt<(S - 3) * kLoadsPerWave>();
         wait_lgkmcnt0();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        ps[fr] = advance();
-        issue(pick(ps[fr].valid, ps[fr], ps[st]), lds[fr]);
+        const StepPos prev = ps[pv_st];   // step t-1, whose V is in vf
+        ps[pv_st] = advance();
+        issue(pick(ps[pv_st].valid, ps[pv_st], ps[st]), lds[pv_st]);
         const bool more = ps[nx].valid;
-        const bool fast = !first && more && ps[st].full && ps[pv_st].full;
+        const bool fast = !first && more && ps[st].full && prev.full;
         if (computes && fast) {
           float alpha;
-          fast_iter(lds[pv_st], lds[nx], pf[nxt_p], sacc[cur_p], sacc[nxt_p], pf[cur_p], alpha);
+          fast_iter(vf, lds[nx], lds[st], pf[nxt_p], sacc[cur_p], sacc[nxt_p], pf[cur_p], alpha);
           if (__any(alpha != 1.f)) {
 #pragma unroll
             for (int b = 0; b < NO; ++b) acc[b] *= alpha;
           }
         } else if (computes) {
-          if (!first) pv(ps[pv_st], lds[pv_st], pf[nxt_p]);
+          if (!first) {
+            mask_v(prev, vf);
+            pv(vf, pf[nxt_p]);
+          }
           if (more) qk(lds[nx], sacc[nxt_p]);
           softmax(ps[st], sacc[cur_p], pf[cur_p]);
-          if (!more) pv(ps[st], lds[st], pf[cur_p]);
+          read_v(lds[st], vf);
+          if (!more) {
+            mask_v(ps[st], vf);
+            pv(vf, pf[cur_p]);
+          }
         }
         first = false;
         if (!more) {
