@@ -523,9 +523,30 @@ def _plan_timing(halo, params, csr, device_meta, stream, repeats=7):
         torch.cuda.synchronize()
         ups.append(e0.elapsed_time(e1) * 1e3)
     ups.sort()
-    return {"plan_ms": round(ts[len(ts) // 2], 4), "plan_ms_min": round(ts[0], 4), "repeats": repeats,
-            "meta_upload_bytes": int(plan.device_meta_bytes), "upload_us": round(ups[1], 1),
-            "workspace_bytes": int(plan.workspace_bytes)}
+    res = {"plan_ms": round(ts[len(ts) // 2], 4), "plan_ms_min": round(ts[0], 4), "repeats": repeats,
+           "meta_upload_bytes": int(plan.device_meta_bytes), "upload_us": round(ups[1], 1),
+           "workspace_bytes": int(plan.workspace_bytes)}
+    if csr.get("q_len") is None:
+        # decode-append update: the next step's forest with one token more
+        # in every private segment whose last page has room (the others
+        # would open a page, which takes a new plan)
+        import numpy as np
+        refs = np.bincount(csr["req_seg_ids"], minlength=len(csr["seg_len"]))
+        room = (refs == 1) & (np.diff(csr["seg_page_indptr"]) * 16 > csr["seg_len"])
+        base = np.asarray(csr["seg_len"], np.int32)
+        us = []
+        for k in range(repeats):
+            # alternately one token more and the plan's own lengths again
+            nxt = dict(csr)
+            nxt["seg_len"] = base + (room * (k % 2 == 0)).astype(np.int32)
+            t0 = time.perf_counter()
+            ok = plan.update_lengths(nxt)
+            us.append((time.perf_counter() - t0) * 1e3)
+            assert ok
+        us.sort()
+        res.update({"update_ms": round(us[len(us) // 2], 4), "update_segments": int(room.sum()),
+                    "private_segments": int((refs == 1).sum())})
+    return res
 
 
 def measure_workload(name, args, dev, pool_fill=0.0, with_cpu=False, percentiles=False):

@@ -39,9 +39,9 @@
  * Python binding). Run calls allocate nothing and enqueue work on the
  * caller's HIP stream (passed as void*, a hipStream_t); HALO_OK means
  * "validated and enqueued". A plan is host memory owned by the library from
- * halo_plan_create until halo_plan_destroy; it is immutable, and its
- * uploaded device_meta is only read by runs, so several streams may run one
- * plan concurrently if each has its own workspace.
+ * halo_plan_create until halo_plan_destroy; only halo_plan_update_lengths
+ * changes it, and its uploaded device_meta is only read by runs, so several
+ * streams may run one plan concurrently if each has its own workspace.
  *
  * Errors. Every call returns a halo_status_t; halo_last_error_message()
  * gives a thread-local description of the last failure. Structural checks
@@ -63,7 +63,9 @@ typedef enum {
   HALO_ERR_INVALID_ARGUMENT = 1,   /* malformed forest, null pointer, bad size */
   HALO_ERR_UNSUPPORTED = 2,        /* valid but not built: head_dim, page size, dtype */
   HALO_ERR_WORKSPACE_TOO_SMALL = 3,
-  HALO_ERR_HIP = 4                 /* a HIP runtime call or kernel launch failed */
+  HALO_ERR_HIP = 4,                /* a HIP runtime call or kernel launch failed */
+  HALO_ERR_REPLAN = 5              /* halo_plan_update_lengths: the forest changed
+                                      beyond tokens appended inside existing pages */
 } halo_status_t;
 
 typedef enum { HALO_F32 = 0, HALO_BF16 = 1 } halo_dtype_t;
@@ -158,6 +160,23 @@ halo_status_t halo_plan_create_with_options(const halo_attn_params_t* params,
                                             halo_plan_t** plan,
                                             size_t* device_meta_bytes,
                                             size_t* workspace_bytes);
+
+/* Decode-append update (§4.1: the plan of a decode batch is rebuilt every
+ * step). Brings a decode plan up to date with `forest`, the plan's own
+ * forest after tokens were appended to (or removed from) private segments
+ * inside pages those segments already hold: same requests and paths, same
+ * page tables, every shared segment (on two or more paths) unchanged, and
+ * every other segment keeping its page count. The plan's decisions depend
+ * on lengths rounded up to whole pages only, so the updated host image is
+ * byte for byte the image halo_plan_create would build for `forest`; only
+ * span ends, the matching inline first-span copies, the segment length
+ * table and the statistics change. Cost: a comparison of the page tables
+ * and work proportional to the spans of the changed segments.
+ * Returns HALO_ERR_REPLAN, leaving the plan unchanged, when `forest` is
+ * outside these bounds (build a new plan then). The caller re-uploads the
+ * plan (halo_plan_upload) before the next run, and must not update a plan
+ * while an upload of it is still in flight. */
+halo_status_t halo_plan_update_lengths(halo_plan_t* plan, const halo_forest_t* forest);
 
 /* Copy the plan's metadata (page ids, work lists) into device_meta, a caller-owned 256-byte aligned device buffer of at least
  * device_meta_bytes, asynchronously on stream. The plan must stay alive

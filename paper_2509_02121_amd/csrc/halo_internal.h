@@ -42,7 +42,8 @@ struct Item {
   int32_t part_base;   // >= 0: the rows write partial results, each to its
                        // row's slot (Row::slot, ItemRec::aux); -1: final rows
                        // written straight to o / lse
-  int32_t keys;        // visible-key estimate (cost, for ordering only)
+  int32_t keys;        // visible keys, each span rounded up to whole pages
+                       // (cost, for ordering only)
   int32_t flags;       // kItemStream: keys read by this item only (stream them)
   int32_t s0_key_begin;   // the first span (when n_spans > 0)
   int32_t s0_key_end;
@@ -107,6 +108,16 @@ struct MetaLayout {
   size_t total = 0;
 };
 
+// A decode plan's copy of its forest, and per segment the spans that end
+// at its last key (CSR over segments: tail_span[tail_indptr[s] ..
+// tail_indptr[s+1])), each with the image byte offset of the item whose
+// first span it is (-1 if none).
+struct AppendIndex {
+  std::vector<int32_t> seg_len, page_indptr, page_ids, req_indptr, req_ids, refs;
+  std::vector<int32_t> tail_indptr, tail_span;
+  std::vector<int64_t> tail_item;
+};
+
 }  // namespace halo
 
 struct halo_plan {
@@ -135,6 +146,7 @@ struct halo_plan {
   size_t workspace_bytes = 0;
   halo::MetaLayout layout;
   std::vector<uint8_t> meta;   // host image of the device metadata
+  halo::AppendIndex append;    // decode plans: for halo_plan_update_lengths
 };
 
 namespace halo {

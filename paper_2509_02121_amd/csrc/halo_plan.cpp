@@ -238,6 +238,11 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
 
   auto path_begin = [&](int r) { return f.req_seg_indptr[r]; };
   auto path_end = [&](int r) { return f.req_seg_indptr[r + 1]; };
+  // Every decision below (chunk lengths, packing, ordering, dealing) looks
+  // at lengths rounded up to whole pages, so tokens appended inside pages a
+  // segment already holds change no decision: halo_plan_update_lengths
+  // relies on it.
+  auto paged = [&](int64_t n) { return ceil_div(n, p.page_size) * p.page_size; };
 
   std::vector<int32_t> refs(S, 0);
   for (int r = 0; r < R; ++r)
@@ -267,7 +272,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       for (int r = 0; r < R; ++r) {
         int64_t priv = 0;
         for (int32_t i = path_begin(r); i < path_end(r); ++i)
-          if (refs[f.req_seg_ids[i]] == 1) priv += f.seg_len[f.req_seg_ids[i]];
+          if (refs[f.req_seg_ids[i]] == 1) priv += paged(f.seg_len[f.req_seg_ids[i]]);
         n += ceil_div(priv, kc) * Hkv;
       }
       return n;
@@ -347,7 +352,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
             pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
             pr.spans = {piece};
             pr.kv_head = g;
-            pr.keys = piece.key_end - piece.key_begin;
+            pr.keys = paged(piece.key_end - piece.key_begin);
             pr.shared = true;
             pr.wide = wide;
             pr.chunk = n_chunks;
@@ -368,7 +373,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       std::vector<std::vector<Span>> chunks;
       int64_t cur = 0;
       for (const Span& piece : sp) {
-        const int64_t n = piece.key_end - piece.key_begin;
+        const int64_t n = paged(piece.key_end - piece.key_begin);
         if (chunks.empty() || cur + n > kc_private) {
           chunks.emplace_back();
           cur = 0;
@@ -379,7 +384,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       for (int g = 0; g < Hkv; ++g)
         for (auto& ch : chunks) {
           int64_t keys = 0;
-          for (auto& x : ch) keys += x.key_end - x.key_begin;
+          for (auto& x : ch) keys += paged(x.key_end - x.key_begin);
           for (int j0 = 0; j0 < G; j0 += kRowsPerItem) {
             Proto pr;
             for (int j = j0; j < std::min(G, j0 + kRowsPerItem); ++j)
@@ -774,6 +779,40 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   if (!merge_parts.empty())
     memcpy(m + L.merge_parts, merge_parts.data(), sizeof(int32_t) * merge_parts.size());
 
+  // What halo_plan_update_lengths needs: the forest the plan was built for,
+  // and for every segment the spans that end at its last key (with the
+  // image offset of the item whose first span it is, whose inline copy of
+  // the span must follow).
+  if (!prefill) {
+    AppendIndex& ax = plan->append;
+    const int64_t n_refs = f.req_seg_indptr[R];
+    ax.seg_len.assign(f.seg_len, f.seg_len + S);
+    ax.page_indptr.assign(f.seg_page_indptr, f.seg_page_indptr + S + 1);
+    ax.page_ids.assign(f.seg_page_ids, f.seg_page_ids + total_pages);
+    ax.req_indptr.assign(f.req_seg_indptr, f.req_seg_indptr + R + 1);
+    ax.req_ids.assign(f.req_seg_ids, f.req_seg_ids + n_refs);
+    ax.refs = refs;
+    std::vector<int64_t> first_of(spans.size(), -1);
+    for (size_t i = 0; i < items.size(); ++i)
+      if (items[i].n_rows > 0 && items[i].n_spans > 0)
+        first_of[items[i].span_begin] = (int64_t)(L.items + i * sizeof(Item));
+    for (size_t i = 0; i < witems.size(); ++i)
+      if (witems[i].n_spans > 0) first_of[witems[i].span_begin] = (int64_t)(L.wide_items + i * sizeof(Item));
+    ax.tail_indptr.assign(S + 1, 0);
+    for (const Span& sp : spans)
+      if (sp.key_end == f.seg_len[sp.seg]) ax.tail_indptr[sp.seg + 1]++;
+    for (int s = 0; s < S; ++s) ax.tail_indptr[s + 1] += ax.tail_indptr[s];
+    ax.tail_span.resize(ax.tail_indptr[S]);
+    ax.tail_item.resize(ax.tail_indptr[S]);
+    std::vector<int32_t> fill(ax.tail_indptr.begin(), ax.tail_indptr.end() - 1);
+    for (size_t i = 0; i < spans.size(); ++i)
+      if (spans[i].key_end == f.seg_len[spans[i].seg]) {
+        const int32_t k = fill[spans[i].seg]++;
+        ax.tail_span[k] = (int32_t)i;
+        ax.tail_item[k] = first_of[i];
+      }
+  }
+
   *plan_out = plan;
   if (device_meta_bytes) *device_meta_bytes = L.total;
   if (workspace_bytes) *workspace_bytes = plan->workspace_bytes;
@@ -835,8 +874,52 @@ extern "C" const char* halo_status_string(halo_status_t s) {
     case HALO_ERR_UNSUPPORTED: return "HALO_ERR_UNSUPPORTED";
     case HALO_ERR_WORKSPACE_TOO_SMALL: return "HALO_ERR_WORKSPACE_TOO_SMALL";
     case HALO_ERR_HIP: return "HALO_ERR_HIP";
+    case HALO_ERR_REPLAN: return "HALO_ERR_REPLAN";
   }
   return "HALO_ERR_UNKNOWN";
 }
 
 extern "C" const char* halo_last_error_message(void) { return halo::last_error(); }
+
+extern "C" halo_status_t halo_plan_update_lengths(halo_plan_t* plan, const halo_forest_t* forest) {
+  clear_error();
+  if (!plan || !forest) return fail(HALO_ERR_INVALID_ARGUMENT, "plan and forest must not be NULL");
+  if (plan->prefill || forest->q_len)
+    return fail(HALO_ERR_REPLAN, "only decode plans and decode forests can be updated");
+  const AppendIndex& ax = plan->append;
+  const int S = plan->num_segments, R = plan->num_requests;
+  const halo_forest_t& f = *forest;
+  auto same = [](const int32_t* a, const std::vector<int32_t>& b) {
+    return b.empty() || (a && memcmp(a, b.data(), sizeof(int32_t) * b.size()) == 0);
+  };
+  if (f.num_segments != S || f.num_requests != R || !f.seg_len || !f.seg_page_indptr || !f.req_seg_indptr ||
+      !same(f.req_seg_indptr, ax.req_indptr) || !same(f.req_seg_ids, ax.req_ids) ||
+      !same(f.seg_page_indptr, ax.page_indptr) || !same(f.seg_page_ids, ax.page_ids))
+    return fail(HALO_ERR_REPLAN, "requests, paths or page tables differ from the plan's forest");
+  const int32_t ps = plan->params.page_size;
+  for (int s = 0; s < S; ++s) {
+    const int32_t len = f.seg_len[s], old = ax.seg_len[s];
+    if (len == old) continue;
+    const int64_t np = ax.page_indptr[s + 1] - ax.page_indptr[s];
+    if (len < 0 || ceil_div(len, ps) != np)
+      return fail(HALO_ERR_REPLAN, "segment " + std::to_string(s) + " changed its page count");
+    if (ax.refs[s] >= 2) return fail(HALO_ERR_REPLAN, "shared segment " + std::to_string(s) + " changed length");
+  }
+  uint8_t* m = plan->meta.data();
+  const MetaLayout& L = plan->layout;
+  AppendIndex& mx = plan->append;
+  for (int s = 0; s < S; ++s) {
+    const int32_t len = f.seg_len[s], old = mx.seg_len[s];
+    if (len == old) continue;
+    for (int32_t k = mx.tail_indptr[s]; k < mx.tail_indptr[s + 1]; ++k) {
+      Span* sp = reinterpret_cast<Span*>(m + L.spans) + mx.tail_span[k];
+      sp->key_end = len;
+      if (mx.tail_item[k] >= 0) reinterpret_cast<Item*>(m + mx.tail_item[k])->s0_key_end = len;
+    }
+    reinterpret_cast<int32_t*>(m + L.seg_len)[s] = len;
+    plan->distinct_kv_tokens += len - old;
+    plan->visible_pairs += (int64_t)(len - old) * mx.refs[s] * plan->params.num_q_heads;
+    mx.seg_len[s] = len;
+  }
+  return HALO_OK;
+}

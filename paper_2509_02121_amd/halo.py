@@ -18,6 +18,7 @@ HALO_ERR_INVALID_ARGUMENT = 1
 HALO_ERR_UNSUPPORTED = 2
 HALO_ERR_WORKSPACE_TOO_SMALL = 3
 HALO_ERR_HIP = 4
+HALO_ERR_REPLAN = 5
 
 HALO_F32 = 0
 HALO_BF16 = 1
@@ -67,7 +68,7 @@ class PlanOptions(ctypes.Structure):
 
 EXPORTED_SYMBOLS = (
     "halo_plan_create", "halo_plan_create_with_options", "halo_plan_options_default", "halo_plan_upload",
-    "halo_plan_destroy", "halo_plan_get_stats",
+    "halo_plan_destroy", "halo_plan_get_stats", "halo_plan_update_lengths",
     "halo_plan_inspect",
     "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_prefix_attn_decode_noalloc",
     "halo_kv_page_gather",
@@ -94,7 +95,7 @@ _LIB = None
 
 def _status_name(status):
     names = {0: "HALO_OK", 1: "HALO_ERR_INVALID_ARGUMENT", 2: "HALO_ERR_UNSUPPORTED",
-             3: "HALO_ERR_WORKSPACE_TOO_SMALL", 4: "HALO_ERR_HIP"}
+             3: "HALO_ERR_WORKSPACE_TOO_SMALL", 4: "HALO_ERR_HIP", 5: "HALO_ERR_REPLAN"}
     return names.get(status, f"status {status}")
 
 
@@ -132,6 +133,8 @@ def load_library(require_gpu=False):
     lib.halo_plan_create_with_options.restype = ctypes.c_int
     lib.halo_plan_options_default.argtypes = [ctypes.POINTER(PlanOptions)]
     lib.halo_plan_options_default.restype = None
+    lib.halo_plan_update_lengths.argtypes = [vp, ctypes.POINTER(Forest)]
+    lib.halo_plan_update_lengths.restype = ctypes.c_int
     lib.halo_plan_upload.argtypes = [vp, vp, sz, vp]
     lib.halo_plan_upload.restype = ctypes.c_int
     lib.halo_plan_destroy.argtypes = [vp]
@@ -278,6 +281,30 @@ class Plan:
     def from_csr(cls, params, csr, options=None):
         return cls(params, csr["seg_len"], csr["seg_page_indptr"], csr["seg_page_ids"],
                    csr["req_seg_indptr"], csr["req_seg_ids"], csr.get("q_len"), options)
+
+    def update_lengths(self, csr):
+        """halo_plan_update_lengths with the forest `csr`: True if the plan
+        now describes it (re-upload before the next run), False if it
+        changed beyond tokens appended inside existing pages (the plan is
+        unchanged; build a new one)."""
+        keep = [_i32(csr[k]) if csr.get(k) is not None else None
+                for k in ("seg_len", "seg_page_indptr", "seg_page_ids", "req_seg_indptr", "req_seg_ids", "q_len")]
+        seg_len_a, indptr_a, ids_a, rindptr_a, rids_a, qlen_a = keep
+        forest = Forest(len(seg_len_a), _ptr(seg_len_a), _ptr(indptr_a), _ptr(ids_a),
+                        len(rindptr_a) - 1, _ptr(rindptr_a), _ptr(rids_a), _ptr(qlen_a))
+        st = _LIB.halo_plan_update_lengths(self._handle, ctypes.byref(forest))
+        if st == HALO_ERR_REPLAN:
+            return False
+        _check(st)
+        self._keep = keep
+        return True
+
+    def image(self):
+        """The host metadata image as bytes (a copy)."""
+        img = ctypes.c_void_p()
+        lay = PlanLayout()
+        _check(_LIB.halo_plan_inspect(self._handle, ctypes.byref(img), ctypes.byref(lay)))
+        return ctypes.string_at(img.value, lay.total_bytes)
 
     def stats(self):
         st = PlanStats()
@@ -658,6 +685,31 @@ class PrefixAttention:
         self._uploaded.record(upload_stream)
         self._upload_stream = upload_stream
         self.out_dtype = {HALO_F32: torch.float32, HALO_BF16: torch.bfloat16}[params.out_dtype]
+
+    def update(self, csr, stream=None):
+        """Bring the plan up to date with `csr` (the next decode step's
+        forest): the length update when it applies, else a new plan (with
+        larger metadata and workspace buffers if needed). Uploads the new
+        metadata on `stream` (None: the current stream); later runs on that
+        stream are ordered after the runs already enqueued there. Returns
+        True if the update applied."""
+        import torch
+        # the previous upload read the host image asynchronously
+        self._uploaded.synchronize()
+        applied = self.plan.update_lengths(csr)
+        if not applied:
+            self.plan = Plan.from_csr(self.plan.params, csr)
+            if self.plan.device_meta_bytes > self.meta.numel():
+                self.meta = torch.empty(self.plan.device_meta_bytes, dtype=torch.uint8, device=self.device)
+            ws_have = self.workspace.numel() if self.workspace is not None else 0
+            if self.plan.workspace_bytes > ws_have:
+                self.workspace = torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=self.device)
+        upload_stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.plan.upload(self.meta, upload_stream)
+        self._uploaded = torch.cuda.Event()
+        self._uploaded.record(upload_stream)
+        self._upload_stream = upload_stream
+        return applied
 
     def _after_upload(self, stream):
         """Make `stream` (None: the current stream) wait for the metadata upload."""

@@ -508,3 +508,102 @@ def test_plan_options_change_the_decomposition(lib):
     assert per_block.max() <= 2 and base["n_narrow_blocks"] < few["n_narrow_blocks"]
     short = inspect({"kc_private": 64})
     assert len(short["spans"]) > len(base["spans"])
+
+
+def _grow_inside_pages(csr, rng, frac=0.7):
+    """A copy of `csr` with tokens appended to random private segments, each
+    staying inside the pages the segment already holds."""
+    out = {k: (None if v is None else np.array(v)) for k, v in csr.items()}
+    refs = np.bincount(csr["req_seg_ids"], minlength=len(csr["seg_len"]))
+    pages = np.diff(csr["seg_page_indptr"])
+    grown = 0
+    for s in range(len(csr["seg_len"])):
+        room = int(pages[s]) * 16 - int(csr["seg_len"][s])
+        if refs[s] == 1 and room > 0 and rng.random() < frac:
+            out["seg_len"][s] += int(rng.integers(1, room + 1))
+            grown += 1
+    return out, grown
+
+
+def _random_decode_csr(rng, n_req, max_len=300):
+    seg_len, paths, _ = random_forest(rng, n_req, max_len=max_len)
+    pages, nxt = [], 0
+    for n in seg_len:
+        pages.append(list(range(nxt, nxt + (n + 15) // 16)))
+        nxt += (n + 15) // 16
+    return _csr(seg_len, pages, paths), nxt
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_update_lengths_matches_a_fresh_plan(lib, seed):
+    """Tokens appended inside existing pages: the updated plan's host image
+    is byte for byte a fresh plan's, and so are its statistics; two updates
+    in a row too."""
+    rng = np.random.default_rng(500 + seed)
+    hkv, g, dtype = [(2, 4, halo.HALO_BF16), (1, 8, halo.HALO_BF16), (2, 2, halo.HALO_F32)][seed % 3]
+    csr, n_pages = _random_decode_csr(rng, int(rng.integers(2, 40)))
+    params = halo.AttnParams(hkv * g, hkv, 128, 16, max(n_pages, 1), dtype, dtype, 0.1)
+    plan = halo.Plan.from_csr(params, csr)
+    for _ in range(2):
+        csr, grown = _grow_inside_pages(csr, rng)
+        assert plan.update_lengths(csr)
+        fresh = halo.Plan.from_csr(params, csr)
+        assert plan.image() == fresh.image()
+        assert plan.stats() == fresh.stats()
+
+
+@pytest.mark.parametrize("index", [1, 2, 4])
+def test_update_lengths_on_the_seeded_decode_batches(lib, index):
+    """The Llama-8B-shaped, two-level tree and 70B-shaped batches (their
+    forests only, pages in order): every request whose last page has room
+    gains a token."""
+    from workloads import synth
+    rng = np.random.Generator(np.random.PCG64(1000 + index))
+    seg_len, paths, _ = synth._forest(index, rng)
+    pages, nxt = [], 0
+    for n in seg_len:
+        pages.append(list(range(nxt, nxt + (int(n) + 15) // 16)))
+        nxt += (int(n) + 15) // 16
+    csr = _csr([int(n) for n in seg_len], pages, paths)
+    hq = 64 if index == 4 else 32
+    params = halo.AttnParams(hq, 8, 128, 16, nxt, halo.HALO_BF16, halo.HALO_BF16, 128 ** -0.5)
+    plan = halo.Plan.from_csr(params, csr)
+    new = {k: (None if v is None else np.array(v)) for k, v in csr.items()}
+    refs = np.bincount(csr["req_seg_ids"], minlength=len(csr["seg_len"]))
+    room = (refs == 1) & (np.diff(csr["seg_page_indptr"]) * 16 > csr["seg_len"])
+    new["seg_len"][room] += 1
+    assert room.sum() > 0
+    assert plan.update_lengths(new)
+    fresh = halo.Plan.from_csr(params, new)
+    assert plan.image() == fresh.image() and plan.stats() == fresh.stats()
+
+
+def test_update_lengths_refuses_other_changes(lib):
+    """A new page, a grown shared segment, another path, a prefill forest:
+    HALO_ERR_REPLAN and the plan left as it was."""
+    seg_len = [40, 10, 5, 30]            # segment 0 shared by requests 0 and 1
+    pages = [[0, 1, 2], [3], [4], [5, 6]]
+    paths = [[0, 1], [0, 2], [3]]
+    csr = _csr(seg_len, pages, paths)
+    params = halo.AttnParams(4, 2, 64, 16, 8, halo.HALO_F32, halo.HALO_F32, 0.125)
+    plan = halo.Plan.from_csr(params, csr)
+    before = plan.image()
+    bad = [
+        _csr([40, 17, 5, 30], [[0, 1, 2], [3, 7], [4], [5, 6]], paths),   # a new page
+        _csr([41, 10, 5, 30], pages, paths),                              # shared segment grew
+        _csr(seg_len, pages, [[0, 1], [0, 2], [0, 3]]),                    # another path
+        _csr(seg_len, [[0, 1, 2], [3], [4], [6, 5]], paths),               # pages moved
+        _csr([40, 17, 5, 30], pages, paths),                               # past the page end
+    ]
+    for c in bad:
+        try:
+            ok = plan.update_lengths(c)
+        except halo.HaloError:
+            ok = None
+        assert ok is False, c
+        assert plan.image() == before
+    pf = halo.Plan.from_csr(params, _csr([40, 10, 5, 30], pages, paths, q_len=[10, 5, 30]))
+    assert pf.update_lengths(_csr([40, 10, 5, 30], pages, paths, q_len=[10, 5, 30])) is False
+    # and a valid in-page append still applies afterwards
+    assert plan.update_lengths(_csr([40, 12, 5, 31], pages, paths))
+    assert plan.image() == halo.Plan.from_csr(params, _csr([40, 12, 5, 31], pages, paths)).image()

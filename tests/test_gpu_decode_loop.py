@@ -1,7 +1,8 @@
 """A decode loop end to end (GPU): prompts as token ids -> prefix forest ->
 each segment's K/V written once -> for several steps, every request appends
 its new token to its private segment (a fresh page at page boundaries), the
-plan is rebuilt, and decode attention is compared with the oracle's
+plan is brought up to date (updated in place when no request opened a page,
+else rebuilt), and decode attention is compared with the oracle's
 unshared attention over the request's whole token sequence (§3)."""
 
 import types
@@ -78,6 +79,7 @@ def test_decode_loop_over_token_id_forest(gpu_lib):
           torch.cat(ks), torch.cat(vs))
 
     tokens = [list(p) for p in prompts]
+    pa, applied = None, 0
     for step in range(12):
         new = rng.integers(0, 1000, size=R).tolist()
         starts = []
@@ -97,7 +99,12 @@ def test_decode_loop_over_token_id_forest(gpu_lib):
                    seg_page_ids=np.concatenate(seg_pages).astype(np.int32),
                    req_seg_indptr=tree.req_seg_indptr.copy(), req_seg_ids=tree.req_seg_ids.copy(), q_len=None)
         q = (torch.randn((R, HQ, D), generator=gen) * 0.5).to(dtype)
-        pa = halo.PrefixAttention(params, csr, dev)
+        if pa is None:
+            pa = halo.PrefixAttention(params, csr, dev)
+        elif pa.update(csr):
+            # the in-place length update: byte for byte a fresh plan
+            applied += 1
+            assert pa.plan.image() == halo.Plan.from_csr(params, csr).image()
         o, lse = pa.run(q.to(dev), kp, vp)
         torch.cuda.synchronize()
         seg_k, seg_v = {}, {}
@@ -107,3 +114,6 @@ def test_decode_loop_over_token_id_forest(gpu_lib):
         o_ref, lse_ref = oracle.decode(q.double().numpy(), seg_k, seg_v, [[r] for r in range(R)], scale)
         assert_parity(types.SimpleNamespace(dtype=dtype), o.double().cpu().numpy(), lse.double().cpu().numpy(),
                       o_ref, lse_ref, np.arange(R), f"decode step {step}")
+    # steps where no request opened a page reuse the plan
+    print(f"plan updated in place on {applied} of 11 steps", flush=True)
+    assert applied > 0
