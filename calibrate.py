@@ -19,14 +19,20 @@ pool of 1.25x the need), timed over single calls with HIP events on the
 call's stream, the median of the calls taken, inputs rotated over copies
 larger than the Infinity Cache so keys stream from HBM.
 
-A linear model is fitted by non-negative least squares (weighted for
-relative error):
+A model is fitted by least squares on relative error:
 
-    T = c0 + c_kv * (distinct K/V bytes) + c_pair * (visible (query, key)
-        pairs x query heads) + c_row * (query rows x query heads)
+    T = c0 + c_row * (query rows x query heads)
         + c_split * (1 if decode rows are split over several work items,
-          which adds the merge launch) + c_shared * (K/V bytes of prefixes
-          shared by more than one request)
+          which adds the merge launch)
+        + (A^k + B^k)^(1/k),
+    A = c_kv * (distinct K/V bytes) + c_pair_private * (visible (query,
+        key) pairs outside shared prefixes x query heads)
+    B = c_pair_shared * (visible pairs on shared prefixes x query heads)
+        + c_shared * (K/V bytes of prefixes shared by more than one request)
+
+A is the streaming of keys read by one request, B the matrix work of the
+grouped prefix pass; the two run side by side in one launch, so they add
+when k = 1 and overlap fully as k grows (k is fitted).
 
 in which the prefix-caching discount is explicit: a prefix shared by G
 requests contributes its K/V bytes once, not G times. Checks: T grows with S
@@ -56,31 +62,44 @@ DECODE_GRID = dict(requests=[64], group=[1, 4, 16, 64], prefix=[0, 512, 2048, 81
 # large batches in few sharing groups (the regime of serving many replicas of
 # one workflow); kept small so the sweep stays within seconds per point
 DECODE_GRID_WIDE = dict(requests=[512], group=[8, 64, 512], prefix=[2048, 8192], suffix=[64, 256])
+# the largest batches: 1024 requests in 8 groups or one, long suffixes
+DECODE_GRID_LARGE = dict(requests=[1024], group=[128, 1024], prefix=[2048, 8192], suffix=[256, 1024, 2048])
 PREFILL_GRID = dict(requests=[8, 32], group=["1", "all"], prefix=[0, 1024, 4096], suffix=[128, 512])
 QUICK_DECODE = dict(requests=[32], group=[1, 32], prefix=[0, 1024], suffix=[64, 1024])
 QUICK_PREFILL = dict(requests=[8], group=["all"], prefix=[0, 1024], suffix=[128, 256])
 
 
+COEF_NAMES = ("c0_us", "c_kv_us_per_byte", "c_pair_shared_us", "c_pair_private_us", "c_row_us", "c_split_us",
+              "c_shared_us_per_byte", "k")
+# private keys a decode row reads in one work item before it is split
+SPLIT_KEYS = 2048
+
+
 def features(kind, requests, group, prefix, suffix):
-    """Model features of one point: 1, distinct K/V bytes, visible pairs x
-    query heads, query rows x query heads (a decode step has one query row
-    per request, a prefill chunk `suffix` rows, causal inside the chunk),
-    the split indicator (decode rows whose keys span a shared prefix and a
-    suffix, or more than 1024 private keys, go through the merge) and the
-    K/V bytes of shared prefixes."""
+    """Model features of one point: 1, distinct K/V bytes, visible pairs on
+    shared prefixes x query heads, the other visible pairs x query heads,
+    query rows x query heads (a decode step has one query row per request, a
+    prefill chunk `suffix` rows, causal inside the chunk), the split
+    indicator (decode rows whose keys span a shared prefix and a suffix, or
+    more than SPLIT_KEYS private keys, go through the merge) and the K/V
+    bytes of shared prefixes."""
     n_prefixes = requests // group if prefix > 0 else 0
     kv_tokens = n_prefixes * prefix + requests * suffix
     tok_bytes = 2 * HKV * D * ELT
-    shared_bytes = n_prefixes * prefix * tok_bytes if group > 1 else 0
+    shared = group > 1 and prefix > 0
+    shared_bytes = n_prefixes * prefix * tok_bytes if shared else 0
     if kind == "decode":
         rows = requests
-        pairs = requests * (prefix + suffix)
-        split = 1.0 if (group > 1 and prefix > 0) or prefix + suffix > 1024 else 0.0
+        prefix_pairs, other_pairs = requests * prefix, requests * suffix
+        split = 1.0 if shared or prefix + suffix > SPLIT_KEYS else 0.0
     else:
         rows = requests * suffix
-        pairs = requests * (suffix * prefix + suffix * (suffix + 1) // 2)
+        prefix_pairs, other_pairs = requests * suffix * prefix, requests * suffix * (suffix + 1) // 2
         split = 0.0
-    return [1.0, float(kv_tokens * tok_bytes), float(pairs * HQ), float(rows * HQ), split, float(shared_bytes)]
+    pairs_shared = prefix_pairs if shared else 0
+    pairs_private = other_pairs + (0 if shared else prefix_pairs)
+    return [1.0, float(kv_tokens * tok_bytes), float(pairs_shared * HQ), float(pairs_private * HQ),
+            float(rows * HQ), split, float(shared_bytes)]
 
 
 def forest_features(seg_len, req_paths, q_len=None, num_q_heads=None, num_kv_heads=None, head_dim=None, elt=ELT):
@@ -100,48 +119,87 @@ def forest_features(seg_len, req_paths, q_len=None, num_q_heads=None, num_kv_hea
             refs[s] += 1
     kv_bytes = sum(seg_len) * tok_bytes
     shared_bytes = sum(n for n, r in zip(seg_len, refs) if r > 1) * tok_bytes
-    rows = pairs = 0
+    rows = pairs_shared = pairs_private = 0
     split = 0.0
     for r, path in enumerate(req_paths):
         keys = sum(seg_len[s] for s in path)
+        shared_keys = sum(seg_len[s] for s in path if refs[s] > 1)
         if q_len is None:
             rows += 1
-            pairs += keys
-            private = sum(seg_len[s] for s in path if refs[s] == 1)
-            if keys > private or private > 1024:
+            pairs_shared += shared_keys
+            pairs_private += keys - shared_keys
+            if shared_keys > 0 or keys - shared_keys > SPLIT_KEYS:
                 split = 1.0
         else:
             n = int(q_len[r])
             rows += n
-            pairs += n * (keys - n) + n * (n + 1) // 2
-    return [1.0, float(kv_bytes), float(pairs * num_q_heads), float(rows * num_q_heads), split,
-            float(shared_bytes)]
+            pairs_shared += n * shared_keys
+            pairs_private += n * (keys - n - shared_keys) + n * (n + 1) // 2
+    return [1.0, float(kv_bytes), float(pairs_shared * num_q_heads), float(pairs_private * num_q_heads),
+            float(rows * num_q_heads), split, float(shared_bytes)]
+
+
+def latency(coef, f):
+    """The model's latency (us) for coefficients `coef` (COEF_NAMES order)
+    and a feature vector (or an array of them, one per row)."""
+    import numpy as np
+    F = np.atleast_2d(np.asarray(f, dtype=np.float64))
+    c0, ckv, cps, cpp, crow, csplit, cshared, k = coef
+    a = ckv * F[:, 1] + cpp * F[:, 3]
+    b = cps * F[:, 2] + cshared * F[:, 6]
+    t = c0 + crow * F[:, 4] + csplit * F[:, 5] + (a ** k + b ** k) ** (1.0 / k)
+    return t if np.ndim(f) > 1 else float(t[0])
 
 
 def predict_forest(coef, seg_len, req_paths, q_len=None, **shape):
     """Predicted latency (us) of one call on a batch given as a forest."""
-    import numpy as np
-    return float(np.dot(coef, forest_features(seg_len, req_paths, q_len, **shape)))
+    return latency(coef, forest_features(seg_len, req_paths, q_len, **shape))
+
+
+# starting point of the fit (us, us/byte, us/pair, ...): a few-us launch,
+# ~7 TB/s streaming, ~2 PFLOP/s matrix work
+_FIT_START = (3.0, 1.4e-7, 5e-7, 1e-9, 1e-3, 5.0, 1e-9)
 
 
 def fit(points):
-    """Non-negative least squares of the latency model on a list of
-    (features, latency_us); returns coefficients and relative errors."""
+    """Least squares of the latency model on relative error over a list of
+    (features, latency_us); coefficients are kept positive (fitted in log
+    space) and k >= 1. Returns coefficients and relative errors."""
     import numpy as np
-    from scipy.optimize import nnls
-    X = np.array([p[0] for p in points], dtype=np.float64)
+    from scipy.optimize import least_squares
+    F = np.array([p[0] for p in points], dtype=np.float64)
     y = np.array([p[1] for p in points], dtype=np.float64)
-    # weight by 1/y so that the fit minimises relative, not absolute, error
-    w = 1.0 / y
-    coef, _ = nnls(X * w[:, None], y * w)
-    pred = X @ coef
-    rel = np.abs(pred - y) / y
-    return coef.tolist(), rel.tolist()
+
+    def coef_of(theta):
+        return list(np.exp(theta[:7])) + [1.0 + float(np.exp(theta[7]))]
+
+    x0 = np.append(np.log(_FIT_START), 0.0)
+    lo = np.append(np.full(7, -80.0), -10.0)
+    hi = np.append(np.full(7, 30.0), 3.0)      # k <= 1 + e^3
+    r = least_squares(lambda th: (latency(coef_of(th), F) - y) / y, x0, bounds=(lo, hi), max_nfev=20000)
+    coef = [float(c) for c in coef_of(r.x)]
+    # a feature that is zero at every point leaves its coefficient undefined
+    for j in range(1, 7):
+        if not F[:, j].any():
+            coef[j] = 0.0
+    rel = np.abs(latency(coef, F) - y) / y
+    return coef, rel.tolist()
+
+
+def cross_validate(points):
+    """Leave-one-out relative errors of the model on a list of (features,
+    latency_us): each point predicted by the fit on all the others."""
+    import numpy as np
+    errs = []
+    for i in range(len(points)):
+        coef, _ = fit(points[:i] + points[i + 1:])
+        f, y = points[i]
+        errs.append(abs(latency(coef, f) - y) / y)
+    return errs
 
 
 def predict(coef, kind, requests, group, prefix, suffix):
-    import numpy as np
-    return float(np.dot(coef, features(kind, requests, group, prefix, suffix)))
+    return latency(coef, features(kind, requests, group, prefix, suffix))
 
 
 def check_monotone(points, tol=MONOTONE_TOL):
@@ -252,8 +310,9 @@ def held_out(summary, calls=50, log=print):
 
 
 def summarize(points):
-    out = {"model": "T_us = c0 + c_kv*kv_bytes + c_pair*pairs_x_hq + c_row*rows_x_hq + c_split*split "
-                    "+ c_shared*shared_kv_bytes",
+    out = {"model": "T_us = c0 + c_row*rows_x_hq + c_split*split + (A^k + B^k)^(1/k); "
+                    "A = c_kv*kv_bytes + c_pair_private*private_pairs_x_hq, "
+                    "B = c_pair_shared*shared_pairs_x_hq + c_shared*shared_kv_bytes",
            "shape": {"num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": D, "dtype": "bf16"},
            "points": [dict(kind=k[0], requests=k[1], group=k[2], prefix=k[3], suffix=k[4], us=round(v, 2))
                       for k, v in points.items()]}
@@ -262,10 +321,11 @@ def summarize(points):
         if len(pts) < 4:
             continue
         coef, rel = fit(pts)
-        out[kind] = {"coef": dict(zip(("c0_us", "c_kv_us_per_byte", "c_pair_us", "c_row_us", "c_split_us",
-                                       "c_shared_us_per_byte"), coef)),
+        loo = sorted(cross_validate(pts))
+        out[kind] = {"coef": dict(zip(COEF_NAMES, coef)),
                      "effective_kv_tbps": round(1.0 / coef[1] / 1e6, 3) if coef[1] > 0 else None,
-                     "max_rel_err": round(max(rel), 4), "median_rel_err": round(sorted(rel)[len(rel) // 2], 4)}
+                     "max_rel_err": round(max(rel), 4), "median_rel_err": round(sorted(rel)[len(rel) // 2], 4),
+                     "loo_median_rel_err": round(loo[len(loo) // 2], 4), "loo_max_rel_err": round(loo[-1], 4)}
     out["monotonicity_violations"] = check_monotone(points)
     return out
 
@@ -278,13 +338,15 @@ def to_markdown(summary, command):
              "| kind | R | G | P | S | us |", "|---|---|---|---|---|---|"]
     for p in summary["points"]:
         lines.append(f"| {p['kind']} | {p['requests']} | {p['group']} | {p['prefix']} | {p['suffix']} | {p['us']} |")
-    lines += ["", f"Model: `{summary['model']}` (non-negative least squares, relative error weighting).", ""]
+    lines += ["", f"Model: `{summary['model']}` (least squares on relative error, positive coefficients, "
+              "k >= 1).", ""]
     for kind in ("decode", "prefill"):
         if kind in summary:
             s = summary[kind]
             lines.append(f"- {kind}: {json.dumps(s['coef'])}; effective K/V streaming rate "
                          f"{s['effective_kv_tbps']} TB/s; relative error max {s['max_rel_err']}, "
-                         f"median {s['median_rel_err']}.")
+                         f"median {s['median_rel_err']}; leave-one-out median {s['loo_median_rel_err']}, "
+                         f"max {s['loo_max_rel_err']}.")
     if summary.get("held_out"):
         lines += ["", "Held-out workloads (forests outside the grid), measured and predicted from their forests "
                   "(`forest_features`):", "", "| workload | measured (us) | predicted (us) | error |",
@@ -313,7 +375,8 @@ def main():
     halo.load_library(require_gpu=True)
     torch.cuda.set_device(0)
     grids = [("decode", QUICK_DECODE), ("prefill", QUICK_PREFILL)] if args.quick else \
-        [("decode", DECODE_GRID), ("decode", DECODE_GRID_WIDE), ("prefill", PREFILL_GRID)]
+        [("decode", DECODE_GRID), ("decode", DECODE_GRID_WIDE), ("decode", DECODE_GRID_LARGE),
+         ("prefill", PREFILL_GRID)]
     points = run(grids, args.calls, log=lambda m: print(m, flush=True))
     summary = summarize(points)
     if not args.quick:
