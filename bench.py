@@ -289,6 +289,35 @@ def gather_bench(args):
     print(json.dumps(line), flush=True)
 
 
+def probe_read_bench(args):
+    """One tile-read microbenchmark configuration over a pool of
+    args.probe_read_bytes bytes (two register stages, two waves per SIMD,
+    32 steps of 4 tiles per item, random tile order): the known number of
+    bytes every launch reads, for dividing the HBM read counter of a profiled
+    run by (one JSON line)."""
+    import numpy as np
+    import torch
+    from paper_2509_02121_amd import probe
+    probe.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    n_tiles = args.probe_read_bytes // 4096 // 128 * 128
+    pool_bytes = n_tiles * 4096
+    pool = torch.empty(pool_bytes, dtype=torch.uint8, device=dev)
+    pool.view(torch.int32).fill_(0x3c003c00)
+    perm = torch.as_tensor(np.random.Generator(np.random.PCG64(11)).permutation(n_tiles).astype(np.int32),
+                           device=dev)
+    out = torch.empty(1 << 16, dtype=torch.int32, device=dev)
+    nt = 0 if args.probe_plain_loads else 1
+    call = probe.bind_stream_read(pool, perm, 32, 2, 2, nt, 256, out, stream)
+    steps, warmup = max(1, min(args.steps, 20)), max(1, min(args.warmup, 3))
+    us = _time_launches(call, steps, warmup, stream)
+    print(json.dumps({"metric": "tile read", "bytes_per_launch": int(pool_bytes), "nontemporal": nt,
+                      "launches": steps + warmup, "us": round(us, 1),
+                      "gbps": round(pool_bytes / us / 1e3, 1)}), flush=True)
+
+
 def probe_bench(args):
     """Context microbenchmarks (one JSON line): the HBM read rate of random
     4 KB tiles with the suffix pass's loads, the dense bf16 MFMA rate, and
@@ -404,6 +433,11 @@ def main():
                     help="only time the paged-KV write path on the workload's page lists: each "
                          "request's newest token appended (decode) or its chunk written (prefill), "
                          "K and V pools, and a copy-on-write page copy per request")
+    ap.add_argument("--probe-read-bytes", type=int, default=0,
+                    help="only run the tile-read microbenchmark over a pool of this many bytes (every 4 KB tile "
+                         "read once per launch, random order), with the suffix pass's non-temporal loads "
+                         "(--probe-plain-loads: ordinary loads): a known-size read for scaling HBM counters")
+    ap.add_argument("--probe-plain-loads", action="store_true")
     ap.add_argument("--probe", action="store_true",
                     help="only run the context microbenchmarks: random 4 KB tile reads with the suffix "
                          "pass's loads, the bf16 MFMA rate and the v_exp_f32 rate")
@@ -411,6 +445,12 @@ def main():
                     help="only time the page gather of the workload's whole working set (every "
                          "segment, K and V pools) into dense token-major buffers")
     args = ap.parse_args()
+    if args.probe_read_bytes:
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        probe_read_bench(args)
+        return
     if args.probe:
         if args.gpus != 1:
             print("bench.py measures one GPU only", file=sys.stderr)
