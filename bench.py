@@ -407,6 +407,25 @@ def probe_bench(args):
                        "us": round(us, 1), "cycles_per_exp": round(cycles / n_exp, 2),
                        "cycles_per_mfma": round(cycles / n_mfma, 2) if m else None})
     res["exp"] = ex
+
+    # --- MFMA beside VALU work on one SIMD: interleaved in each wave, or one
+    # wave of each kind per SIMD
+    fo = torch.empty(512 * 512, dtype=torch.float32, device=dev)
+    ov = []
+    for use_exp, ratios in ((0, (2, 4, 8)), (1, (2, 4))):
+        for v in ratios:
+            for split in (0, 1):
+                iters = 2000
+                call = probe.bind_overlap(split, v, use_exp, iters, 512, fo, stream)
+                us = _time_launches(call, steps, warmup, stream)
+                # 512 blocks of 8 waves on 256 CUs: two wave pairs per SIMD, each
+                # issuing 16 MFMAs per iteration
+                cycles = us * 1e-6 * 2.4e9
+                n_mfma = 2 * iters * 16
+                ov.append({"valu": "exp" if use_exp else "fma", "valu_per_mfma": v,
+                           "split_waves": bool(split), "us": round(us, 1),
+                           "cycles_per_mfma_2.4GHz": round(cycles / n_mfma, 2)})
+    res["overlap"] = ov
     print(json.dumps(res), flush=True)
 
 

@@ -57,6 +57,16 @@ int halo_probe_mfma(int32_t shape, int32_t iters, int32_t blocks, float* out, vo
  * out: blocks * 256 floats. */
 int halo_probe_exp(int32_t valu_per_mfma, int32_t iters, int32_t blocks, float* out, void* stream);
 
+/* blocks x 8 waves (two per SIMD), iters rounds; per round and wave pair
+ * 16 v_mfma_f32_32x32x16_bf16 (4 accumulator chains) and 16 * valu_per_mfma
+ * VALU instructions on 16 independent chains (v_fma_f32, or v_exp_f32 if
+ * use_exp). split = 0: every wave issues half of both, interleaved in its
+ * own instruction stream; split = 1: waves 0-3 issue only the MFMAs and
+ * waves 4-7 only the VALU work. valu_per_mfma: 2, 4 or 8 (2 or 4 with
+ * use_exp). out: blocks * 512 floats. */
+int halo_probe_overlap(int32_t split, int32_t valu_per_mfma, int32_t use_exp, int32_t iters, int32_t blocks,
+                       float* out, void* stream);
+
 const char* halo_probe_last_error(void);
 
 #ifdef __cplusplus

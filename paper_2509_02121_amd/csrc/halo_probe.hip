@@ -10,6 +10,8 @@
 //  * exp_kernel: independent v_exp_f32 chains, optionally one MFMA per
 //    `valu_per_mfma` of them on the same wave, to measure the transcendental
 //    rate and how much VALU work hides behind the matrix cores.
+//  * overlap_kernel: MFMA and VALU work on one SIMD, either interleaved in
+//    each wave or split between the two waves of the SIMD.
 
 #include <hip/hip_runtime.h>
 
@@ -280,7 +282,93 @@ __global__ __launch_bounds__(256) void exp_kernel(ExpArgs a) {
   a.out[blockIdx.x * blockDim.x + threadIdx.x] = sum;
 }
 
+// ---------------------------------------------------------------- overlap
+
+// MFMA and VALU work on one SIMD: 8-wave workgroups (two waves per SIMD),
+// per iteration and wave pair 16 32x32x16 MFMAs (4 accumulator chains) and
+// 16 V VALU instructions (16 independent chains of v_fma_f32, or of
+// v_exp_f32 when EXP). SPLIT = false: every wave issues half of both,
+// interleaved in its own stream; SPLIT = true: waves 0-3 issue only the
+// MFMAs and waves 4-7 only the VALU work (one of each kind per SIMD).
+template <bool SPLIT, int V, bool EXP>
+__global__ __launch_bounds__(512) void overlap_kernel(ExpArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  float v[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) v[j] = -0.001f * (lane + j);
+  bf16x8_t x, y;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    x[j] = (__bf16)(0.001f * (lane + j));
+    y[j] = (__bf16)(0.002f * (lane - j));
+  }
+  f32x16_t c[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) c[i] = f32x16_t{};
+  auto valu = [&](int j) {
+    if constexpr (EXP) v[j] = __builtin_amdgcn_exp2f(v[j]);
+    else v[j] = __builtin_fmaf(v[j], 0.999f, 0.001f);
+  };
+  const bool do_mfma = !SPLIT || wave < 4;
+  const bool do_valu = !SPLIT || wave >= 4;
+  constexpr int NM = SPLIT ? 16 : 8;          // MFMAs per iteration of this wave
+  for (int it = 0; it < a.iters; ++it) {
+    if (do_mfma && do_valu) {
+#pragma unroll
+      for (int k = 0; k < NM; ++k) {
+        c[k % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c[k % 4], 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < V; ++q) valu((k * V + q) % 16);
+      }
+    } else if (do_mfma) {
+#pragma unroll
+      for (int k = 0; k < NM; ++k) c[k % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, c[k % 4], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int k = 0; k < NM * V; ++k) valu(k % 16);
+    }
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) sum += v[j];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sum += c[i][j];
+  a.out[blockIdx.x * blockDim.x + threadIdx.x] = sum;
+}
+
 }  // namespace
+
+extern "C" int halo_probe_overlap(int32_t split, int32_t valu_per_mfma, int32_t use_exp, int32_t iters,
+                                  int32_t blocks, float* out, void* stream) {
+  g_err.clear();
+  if (!out || iters < 1 || blocks < 1) return fail(HALO_PROBE_ERR_ARG, "out, iters >= 1, blocks >= 1");
+  (void)hipGetLastError();
+  ExpArgs a{out, iters};
+  hipStream_t st = static_cast<hipStream_t>(stream);
+#define HALO_PROBE_OVERLAP(S, V, E) \
+  hipLaunchKernelGGL((overlap_kernel<S, V, E>), dim3(blocks), dim3(512), 0, st, a)
+  const int key = (split ? 100 : 0) + (use_exp ? 10 : 0) + valu_per_mfma;
+  switch (key) {
+    case 2: HALO_PROBE_OVERLAP(false, 2, false); break;
+    case 4: HALO_PROBE_OVERLAP(false, 4, false); break;
+    case 8: HALO_PROBE_OVERLAP(false, 8, false); break;
+    case 12: HALO_PROBE_OVERLAP(false, 2, true); break;
+    case 14: HALO_PROBE_OVERLAP(false, 4, true); break;
+    case 102: HALO_PROBE_OVERLAP(true, 2, false); break;
+    case 104: HALO_PROBE_OVERLAP(true, 4, false); break;
+    case 108: HALO_PROBE_OVERLAP(true, 8, false); break;
+    case 112: HALO_PROBE_OVERLAP(true, 2, true); break;
+    case 114: HALO_PROBE_OVERLAP(true, 4, true); break;
+    default: return fail(HALO_PROBE_ERR_ARG, "valu_per_mfma is 2, 4 or 8 (2 or 4 with exp)");
+  }
+#undef HALO_PROBE_OVERLAP
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(HALO_PROBE_ERR_HIP, hipGetErrorString(e));
+  return 0;
+}
 
 extern "C" int halo_probe_stream_read(const void* pool, int64_t pool_bytes, const int32_t* tiles, int64_t n_tiles,
                                       int32_t steps_per_item, int32_t stages, int32_t waves_per_simd,

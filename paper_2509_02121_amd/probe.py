@@ -6,7 +6,8 @@ import os
 
 from .build import PROBE_LIB_PATH
 
-EXPORTED_SYMBOLS = ("halo_probe_stream_read", "halo_probe_mfma", "halo_probe_exp", "halo_probe_last_error")
+EXPORTED_SYMBOLS = ("halo_probe_stream_read", "halo_probe_mfma", "halo_probe_exp", "halo_probe_overlap",
+                    "halo_probe_last_error")
 
 _LIB = None
 
@@ -24,6 +25,8 @@ def load():
         lib.halo_probe_mfma.restype = ctypes.c_int
         lib.halo_probe_exp.argtypes = [i32, i32, i32, vp, vp]
         lib.halo_probe_exp.restype = ctypes.c_int
+        lib.halo_probe_overlap.argtypes = [i32, i32, i32, i32, i32, vp, vp]
+        lib.halo_probe_overlap.restype = ctypes.c_int
         lib.halo_probe_last_error.argtypes = []
         lib.halo_probe_last_error.restype = ctypes.c_char_p
         _LIB = lib
@@ -74,4 +77,14 @@ def bind_exp(valu_per_mfma, iters, blocks, out, stream=None):
 
     def call():
         _check(lib.halo_probe_exp(*args))
+    return call
+
+
+def bind_overlap(split, valu_per_mfma, use_exp, iters, blocks, out, stream=None):
+    lib = load()
+    assert out.is_cuda and out.numel() >= blocks * 512
+    args = (int(split), int(valu_per_mfma), int(use_exp), int(iters), int(blocks), out.data_ptr(), _stream(stream))
+
+    def call():
+        _check(lib.halo_probe_overlap(*args))
     return call
