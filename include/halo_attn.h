@@ -188,9 +188,9 @@ void halo_plan_destroy(halo_plan_t* plan);
 
 /* Decode attention over the forest (one query per request).
  * q, k_pool, v_pool, o, device_meta, workspace: device pointers, layouts
- * above; lse may be NULL. workspace holds per-chunk partial results and must
- * be at least the plan's workspace_bytes (its contents on entry do not
- * matter). The plan must be a decode plan whose metadata was uploaded to
+ * above; lse may be NULL. workspace holds per-chunk partial results (O in
+ * the output element type, LSE in fp32) and must be at least the plan's
+ * workspace_bytes (its contents on entry do not matter). The plan must be a decode plan whose metadata was uploaded to
  * device_meta. Shared segments are read once per group of stacked query
  * rows (the grouped prefix pass, §2 intra-batch prefix sharing); partial
  * results over disjoint key ranges are combined with the exact log-sum-exp

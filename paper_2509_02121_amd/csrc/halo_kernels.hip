@@ -30,6 +30,7 @@
 #include <cmath>
 #include <mutex>
 #include <string>
+#include <type_traits>
 
 #include "halo_internal.h"
 
@@ -148,9 +149,14 @@ __device__ __forceinline__ f32x8_t to_frag(const float (&p)[8], f32x8_t*) {
 __device__ __forceinline__ void store4(float* dst, f32x4_t v) {
   *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
 }
-// Partial results are read once, by the merge launch that follows on
-// another XCD: write them past the caches.
-__device__ __forceinline__ void store4_nt(float* dst, f32x4_t v) {
+// Partial results (read once, by the merge launch): four elements of a row
+// per lane, so a row's line is written in 16-byte (fp32) or 8-byte (bf16)
+// pieces by several instructions. fp32 pieces go past the caches; bf16
+// pieces are half as large, and written past the caches they cost more than
+// they save (measured on the 70B-shaped decode: 966 against 934 us of
+// attention for fp32 partials), so they go through L2, which assembles the
+// lines before they reach HBM.
+__device__ __forceinline__ void store4_part(float* dst, f32x4_t v) {
   __builtin_nontemporal_store(v, reinterpret_cast<f32x4_t*>(dst));
 }
 __device__ __forceinline__ void store4(__bf16* dst, f32x4_t v) {
@@ -162,6 +168,7 @@ __device__ __forceinline__ void store4(__bf16* dst, f32x4_t v) {
   r[3] = (__bf16)v[3];
   *reinterpret_cast<uint2*>(dst) = __builtin_bit_cast(uint2, r);
 }
+__device__ __forceinline__ void store4_part(__bf16* dst, f32x4_t v) { store4(dst, v); }
 
 // Reductions over the four 16-lane rows of a wave (lanes l, l^16, l^32,
 // l^48) with the gfx950 row-swap instructions, which stay on the VALU
@@ -199,7 +206,7 @@ struct AttnArgs {
   const void* v_pool;
   void* o;
   float* lse;
-  float* part_o;
+  void* part_o;      // partial O rows, in the output element type
   float* part_lse;
   const int32_t* seg_page_off;
   const int32_t* seg_len;
@@ -493,10 +500,10 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
   if (it.part_base >= 0) {
     if (has_row) {
       const int64_t prow = row.slot;
-      float* dst = a.part_o + prow * D + 4 * grp;
+      TO* dst = static_cast<TO*>(a.part_o) + prow * D + 4 * grp;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) store4_nt(dst + 16 * b, acc[b] * inv);
-      if (grp == 0) __builtin_nontemporal_store(lse2, a.part_lse + prow);
+      for (int b = 0; b < NB; ++b) store4_part(dst + 16 * b, acc[b] * inv);
+      if (grp == 0) a.part_lse[prow] = lse2;
     }
   } else if (has_row) {
     TO* dst = static_cast<TO*>(a.o) + (int64_t)row.q_row * D + 4 * grp;
@@ -938,13 +945,13 @@ __device__ __forceinline__ void wide_item(const AttnArgs& a, int item_id, uint8_
     const float lse2 = l > 0.f ? m + __log2f(l) : kNegInf;
     if (it.part_base >= 0) {
       const int64_t prow = row.slot;
-      float* dst = a.part_o + prow * D + 4 * h;
+      TO* dst = static_cast<TO*>(a.part_o) + prow * D + 4 * h;
 #pragma unroll
       for (int b = 0; b < NO; ++b)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          store4_nt(dst + 32 * b + 8 * q, f32x4_t{acc[b][4 * q], acc[b][4 * q + 1], acc[b][4 * q + 2], acc[b][4 * q + 3]} * inv);
-      if (h == 0) __builtin_nontemporal_store(lse2, a.part_lse + prow);
+          store4_part(dst + 32 * b + 8 * q, f32x4_t{acc[b][4 * q], acc[b][4 * q + 1], acc[b][4 * q + 2], acc[b][4 * q + 3]} * inv);
+      if (h == 0) a.part_lse[prow] = lse2;
     } else {
       TO* dst = static_cast<TO*>(a.o) + (int64_t)row.q_row * D + 4 * h;
 #pragma unroll
@@ -997,8 +1004,19 @@ void attn_kernel(AttnArgs a) {
 
 // ---------------------------------------------------------------- merge
 
+// Four partial elements from their raw bits: fp32, or bf16 (the upper half
+// of an fp32). (Vector elements go through __uint_as_float: hipcc's
+// __builtin_bit_cast of a vector element reads element 0 whatever the index.)
+__device__ __forceinline__ f32x4_t partial4(u32x4_t x) {
+  return f32x4_t{__uint_as_float(x[0]), __uint_as_float(x[1]), __uint_as_float(x[2]), __uint_as_float(x[3])};
+}
+__device__ __forceinline__ f32x4_t partial4(u32x2_t x) {
+  return f32x4_t{__uint_as_float(x[0] << 16), __uint_as_float(x[0] & 0xffff0000u), __uint_as_float(x[1] << 16),
+                 __uint_as_float(x[1] & 0xffff0000u)};
+}
+
 struct MergeArgs {
-  const float* part_o;
+  const void* part_o;     // in the output element type
   const float* part_lse;
   const int32_t* merge_rows;
   const int32_t* merge_indptr;
@@ -1031,17 +1049,20 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
   if (r >= a.n_merge) return;
   const int q_row = a.merge_rows[r];
   const int p0 = a.merge_indptr[r], p1 = a.merge_indptr[r + 1];
+  // 4 partial elements per thread as raw bits (16 bytes fp32, 8 bytes bf16)
+  using Bits = typename std::conditional<sizeof(TO) == 4, u32x4_t, u32x2_t>::type;
+  const TO* part_o = static_cast<const TO*>(a.part_o);
   uint32_t lb[kBatch];
-  uint4 vb[kBatch];
+  Bits vb[kBatch];
 #pragma unroll
   for (int k = 0; k < kBatch; ++k) {
     if (k < a.k0) {
       const int64_t slot = (int64_t)k * a.n_merge + r;
       lb[k] = __builtin_bit_cast(uint32_t, a.part_lse[slot]);
-      vb[k] = *reinterpret_cast<const uint4*>(a.part_o + slot * D + 4 * t);
+      vb[k] = *reinterpret_cast<const Bits*>(part_o + slot * D + 4 * t);
     } else {
       lb[k] = 0;
-      vb[k] = make_uint4(0u, 0u, 0u, 0u);
+      vb[k] = Bits{};
     }
   }
   float mx = kNegInf;
@@ -1074,9 +1095,10 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     for (int k = 0; k < kBatch; ++k) {
       const bool keep = k < n && k < a.k0;
       l[k] = __builtin_bit_cast(float, keep ? lb[k] : neg_inf_bits);
-      const uint4 x = keep ? vb[k] : make_uint4(0u, 0u, 0u, 0u);
-      v[k] = f32x4_t{__builtin_bit_cast(float, x.x), __builtin_bit_cast(float, x.y),
-                     __builtin_bit_cast(float, x.z), __builtin_bit_cast(float, x.w)};
+      Bits x = vb[k];
+#pragma unroll
+      for (int j = 0; j < (int)(sizeof(Bits) / 4); ++j) x[j] = keep ? x[j] : 0u;
+      v[k] = partial4(x);
     }
     fold(l, v);
   }
@@ -1089,11 +1111,9 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) l[k] = pid[k] >= 0 ? a.part_lse[pid[k]] : kNegInf;
 #pragma unroll
-    for (int k = 0; k < kBatch; ++k) {
-      const float4 x = pid[k] >= 0 ? *reinterpret_cast<const float4*>(a.part_o + (int64_t)pid[k] * D + 4 * t)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
-      v[k] = f32x4_t{x.x, x.y, x.z, x.w};
-    }
+    for (int k = 0; k < kBatch; ++k)
+      v[k] = pid[k] >= 0 ? partial4(*reinterpret_cast<const Bits*>(part_o + (int64_t)pid[k] * D + 4 * t))
+                         : f32x4_t{0.f, 0.f, 0.f, 0.f};
     fold(l, v);
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
@@ -1169,10 +1189,12 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
   const MetaLayout& L = plan->layout;
   const uint8_t* m = static_cast<const uint8_t*>(device_meta);
   const int D = p.head_dim;
-  float* part_o = static_cast<float*>(workspace);
+  // partial O rows in the output element type, then their LSEs
+  void* part_o = workspace;
+  const size_t part_elem = p.out_dtype == HALO_F32 ? 4 : 2;
   float* part_lse = plan->n_part_slots
                         ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
-                                                   align256((size_t)plan->n_part_slots * D * sizeof(float)))
+                                                   align256((size_t)plan->n_part_slots * D * part_elem))
                         : nullptr;
   AttnArgs args{q, k_pool, v_pool, o, lse, part_o, part_lse,
                 reinterpret_cast<const int32_t*>(m + L.seg_page_off),

@@ -736,8 +736,10 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   plan->n_part_slots = n_slots;
   plan->merge_k0 = merge_k0;
   const size_t D = (size_t)p.head_dim;
+  // partial O rows in the output element type, then one fp32 LSE per row
+  const int64_t part_elem = p.out_dtype == HALO_F32 ? 4 : 2;
   plan->workspace_bytes =
-      n_slots ? align_up(n_slots * D * sizeof(float), 256) + align_up(n_slots * sizeof(float), 256) : 0;
+      n_slots ? align_up(n_slots * D * part_elem, 256) + align_up(n_slots * sizeof(float), 256) : 0;
 
   // Pack the device metadata image.
   MetaLayout L;

@@ -61,8 +61,9 @@ def test_noalloc_matches_workspace_decode_twice(gpu_lib):
 
 def test_noalloc_rejects_a_plan_beyond_its_scratch(gpu_lib):
     """A plan needing more workspace than the scratch holds is refused by the
-    C ABI before any launch (the 70B-shaped batch's forest, host arrays only;
-    the pointers are never dereferenced)."""
+    C ABI before any launch (the 70B-shaped batch's forest with fp32 output,
+    whose partials are fp32; host arrays only, the pointers are never
+    dereferenced)."""
     print("case: no-alloc size limit", flush=True)
     rng = np.random.Generator(np.random.PCG64(1004))
     suffix = rng.integers(256, 2048, size=1024, endpoint=True)
@@ -73,7 +74,8 @@ def test_noalloc_rejects_a_plan_beyond_its_scratch(gpu_lib):
     csr = dict(seg_len=seg_len, seg_page_indptr=indptr, seg_page_ids=np.arange(indptr[-1], dtype=np.int32),
                req_seg_indptr=np.arange(0, 2049, 2, dtype=np.int32),
                req_seg_ids=np.array([x for r in range(1024) for x in (r // 128, 8 + r)], np.int32), q_len=None)
-    plan = halo.Plan.from_csr(halo.make_params(64, 8, 128, torch.bfloat16, int(indptr[-1]), 0.0883883), csr)
+    plan = halo.Plan.from_csr(halo.make_params(64, 8, 128, torch.bfloat16, int(indptr[-1]), 0.0883883,
+                                                torch.float32), csr)
     assert plan.workspace_bytes > halo.NOALLOC_SCRATCH_BYTES
     fake = 1 << 20
     st = halo._LIB.halo_prefix_attn_decode_noalloc(plan._handle, fake, fake, fake, fake, fake, None, None)
