@@ -234,6 +234,14 @@ struct AttnArgs {
 //   ((p / 8) / S * 8 + p % 8) * S + (p / 8) % S,
 // i.e. groups of S logical blocks go round-robin to XCDs, in order. The
 // segment length is a multiple of 8 S, so this is a permutation.
+// Within an XCD, workgroups are dispatched in order and in turn to its 4
+// shader engines (the XCD's j-th workgroup goes to engine j % 4, in a fixed
+// order): a workgroup waits for its engine even when another engine has a
+// free CU. The launch therefore mixes wide and narrow workgroups in whole
+// cycles of kSeCycle rounds, so every engine gets the same kinds at the same
+// time.
+constexpr int kSeCycle = 4;
+
 __device__ __forceinline__ int xcd_remap(int p, int S) {
   const int x = p & 7, j = p >> 3;
   return ((j / S) * 8 + x) * S + j % S;
@@ -986,16 +994,18 @@ void attn_kernel(AttnArgs a) {
   const int b = blockIdx.x;
   const int x = b & 7, r = b >> 3;
   if constexpr (RB > 0) {
-    const int wr = a.wide_blocks >> 3;
+    // in cycles of kSeCycle rounds, whole cycles wide or narrow
+    const int ws = a.wide_blocks / (8 * kSeCycle);
     const int sp = a.wide_span;
-    const int w_before = r < sp ? (int)((int64_t)r * wr / sp) : wr;
-    const int w_upto = r < sp ? (int)((int64_t)(r + 1) * wr / sp) : wr;
+    const int cyc = r / kSeCycle, q = r % kSeCycle;
+    const int w_before = cyc < sp ? (int)((int64_t)cyc * ws / sp) : ws;
+    const int w_upto = cyc < sp ? (int)((int64_t)(cyc + 1) * ws / sp) : ws;
     if (w_upto > w_before) {
-      const int item = xcd_remap(w_before * 8 + x, a.wide_group);
+      const int item = xcd_remap((w_before * kSeCycle + q) * 8 + x, a.wide_group);
       if (item < a.n_wide) wide_item<D, TO>(a, item, smem);
       return;
     }
-    narrow_block<T, D, TO>(a, (r - w_upto) * 8 + x);
+    narrow_block<T, D, TO>(a, ((cyc - w_upto) * kSeCycle + q) * 8 + x);
   } else {
     (void)smem;
     narrow_block<T, D, TO>(a, b);
@@ -1004,15 +1014,34 @@ void attn_kernel(AttnArgs a) {
 
 // ---------------------------------------------------------------- merge
 
-// Four partial elements from their raw bits: fp32, or bf16 (the upper half
-// of an fp32). (Vector elements go through __uint_as_float: hipcc's
-// __builtin_bit_cast of a vector element reads element 0 whatever the index.)
-__device__ __forceinline__ f32x4_t partial4(u32x4_t x) {
-  return f32x4_t{__uint_as_float(x[0]), __uint_as_float(x[1]), __uint_as_float(x[2]), __uint_as_float(x[3])};
+// E partial elements (16 bytes) from their raw bits: 4 fp32, or 8 bf16
+// (each the upper half of an fp32). Vector elements go through
+// __uint_as_float: hipcc's __builtin_bit_cast of a vector element reads
+// element 0 whatever the index.
+template <typename TO, int E>
+__device__ __forceinline__ void unpack16(u32x4_t x, float (&v)[E]) {
+  if constexpr (sizeof(TO) == 4) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = __uint_as_float(x[j]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[2 * j] = __uint_as_float(x[j] << 16);
+      v[2 * j + 1] = __uint_as_float(x[j] & 0xffff0000u);
+    }
+  }
 }
-__device__ __forceinline__ f32x4_t partial4(u32x2_t x) {
-  return f32x4_t{__uint_as_float(x[0] << 16), __uint_as_float(x[0] & 0xffff0000u), __uint_as_float(x[1] << 16),
-                 __uint_as_float(x[1] & 0xffff0000u)};
+template <typename TO, int E>
+__device__ __forceinline__ void store16(TO* dst, const float (&v)[E]) {
+  if constexpr (sizeof(TO) == 4) {
+    *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    typedef __bf16 bf16x8v_t __attribute__((ext_vector_type(8)));
+    bf16x8v_t r;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) r[j] = (__bf16)v[j];
+    *reinterpret_cast<u32x4_t*>(dst) = __builtin_bit_cast(u32x4_t, r);
+  }
 }
 
 struct MergeArgs {
@@ -1027,6 +1056,9 @@ struct MergeArgs {
   int32_t k0;   // partials of entry r at slots k * n_merge + r for k < k0
 };
 
+// Rows per merge workgroup (256 threads, 16 bytes of a row per thread).
+template <int D, typename TO> constexpr int merge_rows_per_block() { return 256 / (D * (int)sizeof(TO) / 16); }
+
 // Output rows whose keys were split over several items. Partials hold the
 // normalized o_i and lse_i (log2) of disjoint key sets:
 //   M = max_i lse_i,  w_i = 2^(lse_i - M),  O = sum w_i o_i / sum w_i,
@@ -1038,51 +1070,58 @@ struct MergeArgs {
 // read too (in bounds: the workspace holds k0 * n_merge of them) and dropped
 // by integer selects, which fast math cannot fold away whatever bits they
 // hold. Further partials (entries with more than k0) come from the slot
-// list merge_parts. One group of D/4 threads per row, 4 dims per thread.
+// list merge_parts. One group of threads per row, 16 bytes of each partial
+// (8 bf16 or 4 fp32 dims) per thread.
 template <int D, typename TO>
-__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
-  constexpr int TPR = D / 4;
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6))) void merge_kernel(MergeArgs a) {
+  constexpr int E = 16 / (int)sizeof(TO);
+  constexpr int TPR = D / E;
   constexpr int RPB = 256 / TPR;
+  static_assert(RPB == merge_rows_per_block<D, TO>(), "rows per block");
   constexpr int kBatch = kMergeK0;
   const int r = blockIdx.x * RPB + threadIdx.x / TPR;
   const int t = threadIdx.x % TPR;
   if (r >= a.n_merge) return;
+  const TO* part_o = static_cast<const TO*>(a.part_o);
   const int q_row = a.merge_rows[r];
   const int p0 = a.merge_indptr[r], p1 = a.merge_indptr[r + 1];
-  // 4 partial elements per thread as raw bits (16 bytes fp32, 8 bytes bf16)
-  using Bits = typename std::conditional<sizeof(TO) == 4, u32x4_t, u32x2_t>::type;
-  const TO* part_o = static_cast<const TO*>(a.part_o);
   uint32_t lb[kBatch];
-  Bits vb[kBatch];
+  u32x4_t vb[kBatch];
 #pragma unroll
   for (int k = 0; k < kBatch; ++k) {
     if (k < a.k0) {
       const int64_t slot = (int64_t)k * a.n_merge + r;
       lb[k] = __builtin_bit_cast(uint32_t, a.part_lse[slot]);
-      vb[k] = *reinterpret_cast<const Bits*>(part_o + slot * D + 4 * t);
+      vb[k] = *reinterpret_cast<const u32x4_t*>(part_o + slot * D + E * t);
     } else {
       lb[k] = 0;
-      vb[k] = Bits{};
+      vb[k] = u32x4_t{0u, 0u, 0u, 0u};
     }
   }
   float mx = kNegInf;
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
   float wsum = 0.f;
   // online over batches of parts: rescale when the running max moves
-  auto fold = [&](const float (&l)[kBatch], const f32x4_t (&v)[kBatch]) {
+  auto fold = [&](const float (&l)[kBatch], const u32x4_t (&raw)[kBatch]) {
     float bm = kNegInf;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) bm = fmaxf(bm, l[k]);
     const float m_new = fmaxf(mx, bm);
     if (m_new == kNegInf) return;
     const float alpha = mx == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mx - m_new);
-    acc *= alpha;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] *= alpha;
     wsum *= alpha;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const float w = __builtin_amdgcn_exp2f(l[k] - m_new);   // 0 for absent parts
+      float v[E];
+      unpack16<TO, E>(raw[k], v);
       wsum += w;
-      acc += w * v[k];
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] = __builtin_fmaf(w, v[e], acc[e]);
     }
     mx = m_new;
   };
@@ -1090,34 +1129,34 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     const int n = p1 - p0;
     const uint32_t neg_inf_bits = 0xff800000u;
     float l[kBatch];
-    f32x4_t v[kBatch];
+    u32x4_t raw[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const bool keep = k < n && k < a.k0;
       l[k] = __builtin_bit_cast(float, keep ? lb[k] : neg_inf_bits);
-      Bits x = vb[k];
-#pragma unroll
-      for (int j = 0; j < (int)(sizeof(Bits) / 4); ++j) x[j] = keep ? x[j] : 0u;
-      v[k] = partial4(x);
+      const uint32_t m = keep ? 0xffffffffu : 0u;
+      raw[k] = vb[k] & u32x4_t{m, m, m, m};
     }
-    fold(l, v);
+    fold(l, raw);
   }
   for (int pb = p0 + a.k0; pb < p1; pb += kBatch) {
     int pid[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) pid[k] = pb + k < p1 ? a.merge_parts[pb + k] : -1;
     float l[kBatch];
-    f32x4_t v[kBatch];
+    u32x4_t raw[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) l[k] = pid[k] >= 0 ? a.part_lse[pid[k]] : kNegInf;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k)
-      v[k] = pid[k] >= 0 ? partial4(*reinterpret_cast<const Bits*>(part_o + (int64_t)pid[k] * D + 4 * t))
-                         : f32x4_t{0.f, 0.f, 0.f, 0.f};
-    fold(l, v);
+      raw[k] = pid[k] >= 0 ? *reinterpret_cast<const u32x4_t*>(part_o + (int64_t)pid[k] * D + E * t)
+                           : u32x4_t{0u, 0u, 0u, 0u};
+    fold(l, raw);
   }
   const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  store4(static_cast<TO*>(a.o) + (int64_t)q_row * D + 4 * t, acc * inv);
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] *= inv;
+  store16<TO, E>(static_cast<TO*>(a.o) + (int64_t)q_row * D + E * t, acc);
   if (t == 0 && a.lse) a.lse[q_row] = wsum > 0.f ? (mx + __log2f(wsum)) * kLn2 : kNegInf;
 }
 
@@ -1139,13 +1178,25 @@ int pad_to(int n, int m) { return (n + m - 1) / m * m; }
 // rest run after the last wide round.
 constexpr int kWideSpanNarrowPct = 80;
 
+int lcm_int(int a, int b) {
+  int x = a, y = b;
+  while (y) {
+    const int t = x % y;
+    x = y;
+    y = t;
+  }
+  return a / x * b;
+}
+
 template <typename T, int D, typename TO>
 void launch_attention(AttnArgs args, const MergeArgs& margs, int wide_rb, hipStream_t stream) {
   const int rb = sizeof(T) == 2 ? wide_rb : 0;
-  args.wide_blocks = (rb > 0 && args.n_wide > 0) ? pad_to(args.n_wide, 8 * args.wide_group) : 0;
+  // whole dispatch cycles of wide rounds, each a multiple of wide_group rounds
+  args.wide_blocks =
+      (rb > 0 && args.n_wide > 0) ? pad_to(args.n_wide, 8 * lcm_int(args.wide_group, kSeCycle)) : 0;
   {
-    const int wr = args.wide_blocks / 8, nr = args.narrow_blocks / 8;
-    args.wide_span = wr + (int)((int64_t)nr * kWideSpanNarrowPct / 100);
+    const int ws = args.wide_blocks / (8 * kSeCycle), ns = args.narrow_blocks / (8 * kSeCycle);
+    args.wide_span = ws + (int)((int64_t)ns * kWideSpanNarrowPct / 100);
   }
   constexpr int W = block_waves<T>();
   const int grid = args.wide_blocks + args.narrow_blocks;
@@ -1160,7 +1211,7 @@ void launch_attention(AttnArgs args, const MergeArgs& margs, int wide_rb, hipStr
     }
   }
   if (margs.n_merge > 0) {
-    constexpr int rpb = 256 / (D / 4);
+    constexpr int rpb = merge_rows_per_block<D, TO>();
     const int blocks = (margs.n_merge + rpb - 1) / rpb;
     hipLaunchKernelGGL((merge_kernel<D, TO>), dim3(blocks), dim3(256), 0, stream, margs);
   }
