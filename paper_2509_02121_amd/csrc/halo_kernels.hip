@@ -366,18 +366,40 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
     p.pid1 = p.has1 ? __builtin_amdgcn_readlane(st.vpid, j + 1) : p.pid0;
     return p;
   };
+  // bf16: a position past the item's end loads, in every lane, the same one
+  // of 16 distinct 16-byte words at the start of the item table (at least
+  // 8 workgroups x 8 slots x 64 bytes; cached after its first use) instead
+  // of K/V pages: the count of loads in flight stays fixed (the loop's
+  // waits are static) without reading pages again and waiting for them
+  // when the item ends (measured: 70B-shaped decode 918.6 -> 912 us,
+  // two-level tree -1.6%, Llama-8B-shaped -2.5%).
+  const uint8_t* idle_words = reinterpret_cast<const uint8_t*>(a.items);
   auto fetch = [&](const StepPos& p, Regs& r) {
     // A rows 0-7 come from page 0, rows 8-15 from page 1; a V lane reads
     // page grp / 2.
     const T* kq = kbase + (int64_t)(col < 8 ? p.pid0 : p.pid1) * page_stride;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      r.k[0][s] = load_k8<NT>(kq, col & 7, 32 * s + 8 * grp);
-      r.k[1][s] = load_k8<NT>(kq, 8 + (col & 7), 32 * s + 8 * grp);
-    }
     const T* vq = vbase + (int64_t)(grp < 2 ? p.pid0 : p.pid1) * page_stride;
+    if constexpr (sizeof(T) == 2) {
+      const bool live = p.valid;
+      auto word = [&](const T* real, int k) {
+        return live ? reinterpret_cast<const uint8_t*>(real) : idle_words + 16 * k;
+      };
 #pragma unroll
-    for (int b = 0; b < NB; ++b) r.v[b] = load_v8<NT>(vq, v_off + b * 256);
+      for (int s = 0; s < NS; ++s) {
+        r.k[0][s] = __builtin_bit_cast(F, ld16<NT>(word(kq + ((4 * s + grp) * 16 + (col & 7)) * 8, 2 * s)));
+        r.k[1][s] = __builtin_bit_cast(F, ld16<NT>(word(kq + ((4 * s + grp) * 16 + 8 + (col & 7)) * 8, 2 * s + 1)));
+      }
+#pragma unroll
+      for (int b = 0; b < NB; ++b) r.v[b] = __builtin_bit_cast(F, ld16<NT>(word(vq + v_off + b * 256, 2 * NS + b)));
+    } else {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        r.k[0][s] = load_k8<NT>(kq, col & 7, 32 * s + 8 * grp);
+        r.k[1][s] = load_k8<NT>(kq, 8 + (col & 7), 32 * s + 8 * grp);
+      }
+#pragma unroll
+      for (int b = 0; b < NB; ++b) r.v[b] = load_v8<NT>(vq, v_off + b * 256);
+    }
   };
 
   // Span cursor. The first span comes with the item and its record; a later
@@ -473,8 +495,8 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
   };
 
   // P register stages rotate: while step s is computed, the next P - 1
-  // steps are in flight. A position past the end re-fetches the current
-  // step's pages (in bounds, never used).
+  // steps are in flight. A position past the end loads idle words (bf16) or
+  // re-fetches the current step's pages (fp32); in bounds, never used.
   Regs r[P];
   StepPos ps[P];
   ps[0] = advance();
@@ -483,7 +505,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
 #pragma unroll
     for (int i = 1; i < P - 1; ++i) {
       ps[i] = advance();
-      fetch(pick(ps[i].valid, ps[i], ps[0]), r[i]);
+      fetch(sizeof(T) == 2 ? ps[i] : pick(ps[i].valid, ps[i], ps[0]), r[i]);
     }
     bool done = false;
     while (!done) {
@@ -491,7 +513,7 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
       for (int s = 0; s < P; ++s) {
         const int w = (s + P - 1) % P;
         ps[w] = advance();
-        fetch(pick(ps[w].valid, ps[w], ps[s]), r[w]);
+        fetch(sizeof(T) == 2 ? ps[w] : pick(ps[w].valid, ps[w], ps[s]), r[w]);
         compute(ps[s], r[s]);
         if (!ps[(s + 1) % P].valid) {
           done = true;
