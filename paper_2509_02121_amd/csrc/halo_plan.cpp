@@ -425,10 +425,18 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
         for (size_t rb = 0; rb < rows.size(); rb += rows_per) {
           Proto pr;
           pr.rows.assign(rows.begin() + rb, rows.begin() + std::min(rows.size(), rb + (size_t)rows_per));
-          int32_t qmax = 0;
-          for (auto& x : pr.rows) qmax = std::max(qmax, x.qpos);
+          int32_t qmin = n, qmax = 0;
+          for (auto& x : pr.rows) {
+            qmin = std::min(qmin, x.qpos);
+            qmax = std::max(qmax, x.qpos);
+          }
           pr.spans = prefix_spans;
-          pr.spans.push_back(Span{chunk_seg, 0, std::min(n, qmax + 1), 1, 0, {0, 0, 0}});
+          // keys up to the group's first position are visible to every row:
+          // that part of the chunk (whole 32-key steps) needs no mask
+          const int32_t open = std::min(std::min(n, qmax + 1), (qmin + 1) / 32 * 32);
+          if (open > 0) pr.spans.push_back(Span{chunk_seg, 0, open, 0, 0, {0, 0, 0}});
+          if (std::min(n, qmax + 1) > open)
+            pr.spans.push_back(Span{chunk_seg, open, std::min(n, qmax + 1), 1, 0, {0, 0, 0}});
           pr.kv_head = g;
           pr.keys = prefix_keys + qmax + 1;
           pr.shared = false;
