@@ -48,3 +48,19 @@ def test_option_settings_match_the_oracle(gpu_lib, opts):
         o, lse = _run(w, opts)
         ro, rl, rows = oracle_for(w)
         assert_parity(w, o, lse, ro, rl, rows, f"forest {seed} {opts}")
+
+
+@pytest.mark.parametrize("n_req,wide_rows", [(1, 32), (3, 96), (9, 256), (17, 64), (40, 32)])
+def test_mixed_wide_and_narrow_launch_cycles(gpu_lib, n_req, wide_rows):
+    """Wide and narrow workgroups are launched in whole 4-round cycles; wide
+    counts padded to whole cycles and narrow counts that end inside a cycle
+    must still cover every item once (oracle parity on decode forests with
+    wide items forced)."""
+    print(f"case: launch cycles n_req={n_req} wide_rows={wide_rows}", flush=True)
+    rng = np.random.default_rng(1000 + n_req)
+    seg_len, paths, q_len = random_forest(rng, n_req, max_len=300, share_prob=0.9)
+    w = build_workload("cycles", 400 + n_req, 8, 2, 128, torch.bfloat16, seg_len, paths, q_len,
+                       value_scale=0.5)
+    o, lse = _run(w, {"wide": 1, "wide_rows": wide_rows, "kc_wide": 64})
+    ro, rl, rows = oracle_for(w)
+    assert_parity(w, o, lse, ro, rl, rows, f"cycles {n_req} {wide_rows}")
