@@ -310,8 +310,14 @@ struct StepRegs {
 //  * Loads are software-pipelined: the operands of step i+1 are in flight
 //    while step i is computed, and the next span's page ids are loaded when
 //    its predecessor starts.
+// This lane's words of a narrow item's record: its row's q_row and second
+// word (lane % 16), and page lane % 32 of the first span.
+struct RecLane {
+  int32_t q_row, aux, page;
+};
+
 template <typename T, int D, typename TO, bool NT, int P>
-__device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, const ItemRec* rec, int lane) {
+__device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, const RecLane& rl, int lane) {
   using F = typename FragOf<T>::type;
   constexpr int NS = D / 32;   // QK steps over d
   constexpr int NB = D / 16;   // PV output blocks over d
@@ -320,11 +326,11 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
   const int col = lane & 15;
   const int grp = lane >> 4;
 
-  // The item's lane record (one load per field, all in flight together):
-  // this lane's row, and page j of the first span in lane j.
-  // (aux: chunk position for a prefill item, partial slot for a decode one)
-  Row row{rec->q_row[col], rec->aux[col], -1, rec->aux[col]};
-  const int32_t vpid0 = rec->page[lane & 31];
+  // The item's lane record: this lane's row, and page j of the first span
+  // in lane j. (aux: chunk position for a prefill item, partial slot for a
+  // decode one)
+  Row row{rl.q_row, rl.aux, -1, rl.aux};
+  const int32_t vpid0 = rl.page;
 
   F qf[NS];
   {
@@ -549,19 +555,23 @@ __device__ __forceinline__ void run_item(const AttnArgs& a, const Item& it, cons
 template <typename T> constexpr int block_waves() { return sizeof(T) == 2 ? 8 : 4; }
 
 // Narrow workgroup `block` runs the items in its narrow_slots slots (dealt
-// by the planner; n_rows = 0 marks an empty slot), one per wave; waves of
-// empty slots exit.
+// by the planner; n_rows = 0 marks an empty slot), one per wave; a wave of
+// an empty slot runs through without loading a page or writing a row.
 template <typename T, int D, typename TO>
 __device__ __forceinline__ void narrow_block(const AttnArgs& a, int block) {
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
-  const int64_t item_id = (int64_t)block * a.narrow_slots + wave;
-  if (wave >= a.narrow_slots) return;
+  // one slot per wave (the host checks narrow_slots == block_waves<T>())
+  const int64_t item_id = (int64_t)block * block_waves<T>() + wave;
+  // The slot's item and lane record go out together (one round trip): no
+  // branch waits for the item first. An empty slot (n_rows = 0, no spans)
+  // runs through without loading a page or writing a row.
   const Item it = a.items[item_id];
-  if (it.n_rows <= 0) return;
   const ItemRec* rec = a.item_recs + item_id;
-  if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, rec, lane);
-  else run_item<T, D, TO, false, 2>(a, it, rec, lane);
+  const int col = lane & 15;
+  const RecLane rl{rec->q_row[col], rec->aux[col], rec->page[lane & 31]};
+  if (it.flags & kItemStream) run_item<T, D, TO, true, 2>(a, it, rl, lane);
+  else run_item<T, D, TO, false, 2>(a, it, rl, lane);
 }
 
 // ---------------------------------------------------------------- wide items
@@ -1286,6 +1296,9 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
                   reinterpret_cast<const int32_t*>(m + L.merge_indptr),
                   reinterpret_cast<const int32_t*>(m + L.merge_parts),
                   o, lse, plan->n_merge, plan->merge_k0};
+  if (plan->n_narrow_blocks > 0 &&
+      plan->narrow_slots != (p.kv_dtype == HALO_BF16 ? block_waves<__bf16>() : block_waves<float>()))
+    return fail(HALO_ERR_INVALID_ARGUMENT, "internal: narrow slots per workgroup differ from its waves");
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();   // clear any stale error of the caller
   const bool out_f32 = p.out_dtype == HALO_F32;
