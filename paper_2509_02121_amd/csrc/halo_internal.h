@@ -3,7 +3,9 @@
 
 #include <stdint.h>
 
+#include <memory>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "halo_attn.h"
@@ -112,6 +114,27 @@ struct MetaLayout {
 // at its last key (CSR over segments: tail_span[tail_indptr[s] ..
 // tail_indptr[s+1])), each with the image byte offset of the item whose
 // first span it is (-1 if none).
+// Allocator whose value-less construct() leaves the bytes as they are, so a
+// vector resized to hold the metadata image is not zero-filled first.
+template <typename T>
+struct DefaultInitAlloc : std::allocator<T> {
+  template <typename U>
+  struct rebind {
+    using other = DefaultInitAlloc<U>;
+  };
+  DefaultInitAlloc() = default;
+  template <typename U>
+  DefaultInitAlloc(const DefaultInitAlloc<U>&) noexcept {}
+  template <typename U>
+  void construct(U* p) noexcept {
+    ::new (static_cast<void*>(p)) U;
+  }
+  template <typename U, typename... A>
+  void construct(U* p, A&&... a) {
+    ::new (static_cast<void*>(p)) U(std::forward<A>(a)...);
+  }
+};
+
 struct AppendIndex {
   std::vector<int32_t> seg_len, page_indptr, page_ids, req_indptr, req_ids, refs;
   std::vector<int32_t> tail_indptr, tail_span;
@@ -145,7 +168,7 @@ struct halo_plan {
   int64_t visible_pairs = 0;
   size_t workspace_bytes = 0;
   halo::MetaLayout layout;
-  std::vector<uint8_t> meta;   // host image of the device metadata
+  std::vector<uint8_t, halo::DefaultInitAlloc<uint8_t>> meta;   // host image of the device metadata
   halo::AppendIndex append;    // decode plans: for halo_plan_update_lengths
 };
 

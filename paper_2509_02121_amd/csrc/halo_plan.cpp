@@ -25,6 +25,7 @@
 #include <cmath>
 #include <cstring>
 #include <limits>
+#include <mutex>
 #include <new>
 #include <queue>
 #include <string>
@@ -158,6 +159,22 @@ void pieces(int32_t seg, int32_t len, int32_t chunk, std::vector<Span>& out) {
     out.push_back(Span{seg, kb, std::min(len, kb + chunk), 0, 0, {0, 0, 0}});
 }
 
+// The planner's large arrays are thread-local and keep their capacity from
+// one call to the next (returned empty): a decode loop plans every step, and
+// first touches of fresh multi-megabyte allocations (page faults) cost about
+// as much as the planning itself. Tag tells the arrays of one type apart.
+template <typename V, int Tag>
+V& scratch() {
+  static thread_local V v;
+  v.clear();
+  return v;
+}
+
+// The metadata image of the last plan destroyed, kept for the next plan
+// (one buffer, the largest seen): same reason.
+std::mutex g_spare_mu;
+std::vector<uint8_t, DefaultInitAlloc<uint8_t>> g_spare_meta;
+
 }  // namespace
 
 extern "C" void halo_plan_options_default(halo_plan_options_t* o) {
@@ -259,7 +276,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     bool wide;
     int32_t chunk = -1;   // shared items: id of the (piece, kv head) whose pages they read
   };
-  std::vector<Proto> protos;
+  auto& protos = scratch<std::vector<Proto>, 0>();
   int32_t n_chunks = 0;
 
   if (!prefill) {
@@ -449,7 +466,8 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
 
   // Parts per output row; items whose rows all have a single part write
   // their final result directly.
-  std::vector<int32_t> n_parts(n_q_rows * Hq, 0);
+  auto& n_parts = scratch<std::vector<int32_t>, 1>();
+  n_parts.assign(n_q_rows * Hq, 0);
   for (auto& pr : protos)
     for (auto& row : pr.rows) n_parts[row.q_row]++;
   // Rows that see no key at all get an item with no spans, which writes
@@ -470,7 +488,8 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       protos.push_back(std::move(pr));
     }
   }
-  std::vector<char> is_final(protos.size(), 0);
+  auto& is_final = scratch<std::vector<char>, 0>();
+  is_final.assign(protos.size(), 0);
   for (size_t i = 0; i < protos.size(); ++i) {
     bool all_one = true;
     for (auto& row : protos[i].rows) all_one &= (n_parts[row.q_row] == 1);
@@ -479,18 +498,46 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
 
   // Shared items first, then private ones; longest first within each class
   // (stable: items reading the same pages stay neighbours).
-  std::vector<size_t> order(protos.size());
+  auto& order = scratch<std::vector<size_t>, 0>();
+  order.resize(protos.size());
   for (size_t i = 0; i < order.size(); ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(), [&](size_t a, size_t b) {
     if (protos[a].shared != protos[b].shared) return protos[a].shared;
     return protos[a].keys > protos[b].keys;
   });
 
-  std::vector<Item> items, witems;
-  std::vector<int32_t> item_chunk;   // per narrow item: its proto's chunk id
-  std::vector<Span> spans;
-  std::vector<Row> rows;
-  std::vector<std::vector<int32_t>> row_parts(prefill ? 0 : n_q_rows * Hq);
+  auto& items = scratch<std::vector<Item>, 0>();
+  auto& witems = scratch<std::vector<Item>, 1>();
+  auto& item_chunk = scratch<std::vector<int32_t>, 2>();   // per narrow item: its proto's chunk id
+  auto& spans = scratch<std::vector<Span>, 0>();
+  auto& rows = scratch<std::vector<Row>, 0>();
+  // Partial rows of each output row, in item order (CSR over q rows).
+  auto& parts_indptr = scratch<std::vector<int32_t>, 3>();
+  auto& parts_of = scratch<std::vector<int32_t>, 4>();
+  {
+    size_t n_rows_all = 0, n_spans_all = 0, n_wide = 0;
+    if (!prefill) parts_indptr.assign(n_q_rows * Hq + 1, 0);
+    for (size_t i = 0; i < protos.size(); ++i) {
+      const Proto& pr = protos[i];
+      n_rows_all += pr.rows.size();
+      n_wide += pr.wide ? 1 : 0;
+      const int32_t max_keys = pr.wide ? kMaxSpanKeys : kNarrowSpanKeys;
+      for (const Span& sp : pr.spans) n_spans_all += (size_t)((sp.key_end - sp.key_begin + max_keys - 1) / max_keys);
+      if (!prefill && !is_final[i])
+        for (const Row& row : pr.rows) parts_indptr[row.q_row + 1]++;
+    }
+    rows.reserve(n_rows_all);
+    spans.reserve(n_spans_all);
+    witems.reserve(n_wide);
+    items.reserve(protos.size() - n_wide);
+    item_chunk.reserve(protos.size() - n_wide);
+    if (!prefill) {
+      for (size_t q = 0; q + 1 < parts_indptr.size(); ++q) parts_indptr[q + 1] += parts_indptr[q];
+      parts_of.resize(parts_indptr.back());
+    }
+  }
+  auto& parts_fill = scratch<std::vector<int32_t>, 5>();
+  parts_fill.assign(prefill ? 0 : n_q_rows * Hq, 0);
   int64_t part_rows = 0;
   for (size_t oi : order) {
     Proto& pr = protos[oi];
@@ -511,7 +558,10 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
         return fail(HALO_ERR_INVALID_ARGUMENT, "too many partial rows");
       }
       it.part_base = (int32_t)part_rows;
-      for (int i = 0; i < it.n_rows; ++i) row_parts[pr.rows[i].q_row].push_back((int32_t)(part_rows + i));
+      for (int i = 0; i < it.n_rows; ++i) {
+        const int32_t q = pr.rows[i].q_row;
+        parts_of[parts_indptr[q] + parts_fill[q]++] = (int32_t)(part_rows + i);
+      }
       part_rows += it.n_rows;
     }
     if (pr.shared) plan->n_shared_items++;
@@ -547,27 +597,36 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   // kernel finds them from m alone and loads them in the same round trip as
   // the entry's metadata; partials past k0 take consecutive slots after
   // k0 * n_merge. merge_parts lists every entry's slots in order.
-  std::vector<int32_t> merge_rows, merge_indptr{0}, merge_parts;
+  auto& merge_rows = scratch<std::vector<int32_t>, 6>();
+  auto& merge_indptr = scratch<std::vector<int32_t>, 7>();
+  auto& merge_parts = scratch<std::vector<int32_t>, 8>();
+  merge_indptr.push_back(0);
   int64_t n_slots = 0;
   int32_t merge_k0 = 0;
   if (!prefill) {
-    std::vector<int32_t> merge_of(n_q_rows * Hq, -1);
-    std::vector<int32_t> slot_of_part(part_rows, -1);
+    auto& merge_of = scratch<std::vector<int32_t>, 9>();
+    merge_of.assign(n_q_rows * Hq, -1);
+    auto& slot_of_part = scratch<std::vector<int32_t>, 10>();
+    slot_of_part.assign(part_rows, -1);
     size_t most = 0;
     for (int64_t qr = 0; qr < n_q_rows * Hq; ++qr) {
-      if (row_parts[qr].empty()) continue;   // written by a final item
+      const size_t np = (size_t)(parts_indptr[qr + 1] - parts_indptr[qr]);
+      if (np == 0) continue;   // written by a final item
       merge_of[qr] = (int32_t)merge_rows.size();
       merge_rows.push_back((int32_t)qr);
-      most = std::max(most, row_parts[qr].size());
+      most = std::max(most, np);
     }
+    merge_parts.reserve(parts_of.size());
+    merge_indptr.reserve(merge_rows.size() + 1);
     const int64_t nm = (int64_t)merge_rows.size();
     merge_k0 = (int32_t)std::min<size_t>(kMergeK0, most);
     int64_t next = merge_k0 * nm;
     for (int64_t m = 0; m < nm; ++m) {
-      const std::vector<int32_t>& parts = row_parts[merge_rows[m]];
-      for (size_t k = 0; k < parts.size(); ++k) {
+      const int32_t qr = merge_rows[m];
+      const int32_t b0 = parts_indptr[qr], b1 = parts_indptr[qr + 1];
+      for (int32_t k = 0; k < b1 - b0; ++k) {
         const int64_t slot = (int64_t)k < merge_k0 ? (int64_t)k * nm + m : next++;
-        slot_of_part[parts[k]] = (int32_t)slot;
+        slot_of_part[parts_of[b0 + k]] = (int32_t)slot;
         merge_parts.push_back((int32_t)slot);
       }
       merge_indptr.push_back((int32_t)merge_parts.size());
@@ -603,7 +662,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   //    longest first and fill the open workgroup of their XCD (shared) or
   //    of the XCD with the fewest items (private). Workgroups then launch
   //    longest first, and the short ones fill the tail.
-  std::vector<ItemRec> recs;
+  auto& recs = scratch<std::vector<ItemRec>, 0>();
   const int64_t n_real_items = (int64_t)items.size();
   if (!items.empty()) {
     const int waves = narrow_items_per_block(p.kv_dtype);
@@ -710,7 +769,8 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       }
     }
     // slot layout, empty slots n_rows = 0; and each slot's lane record
-    std::vector<Item> dealt((size_t)(nb * slots), Item{});
+    auto& dealt = scratch<std::vector<Item>, 2>();
+    dealt.assign((size_t)(nb * slots), Item{});
     recs.assign((size_t)(nb * slots), ItemRec{});
     for (int64_t b = 0; b < nb; ++b)
       for (size_t k = 0; k < blk[b].size(); ++k) {
@@ -772,22 +832,36 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   L.merge_parts = place(sizeof(int32_t) * std::max<size_t>(merge_parts.size(), 1));
   L.total = off;
   plan->layout = L;
-  plan->meta.assign(L.total, 0);
-  uint8_t* m = plan->meta.data();
-  if (S) {
-    memcpy(m + L.seg_page_off, f.seg_page_indptr, sizeof(int32_t) * S);
-    memcpy(m + L.seg_len, f.seg_len, sizeof(int32_t) * S);
+  // (the image is not zero-filled first: each array is copied in and the
+  // rest of its 256-byte-aligned place is zeroed)
+  {
+    std::lock_guard<std::mutex> lock(g_spare_mu);
+    plan->meta.swap(g_spare_meta);
   }
-  if (total_pages) memcpy(m + L.page_ids, f.seg_page_ids, sizeof(int32_t) * total_pages);
-  if (!items.empty()) memcpy(m + L.items, items.data(), sizeof(Item) * items.size());
-  if (!recs.empty()) memcpy(m + L.item_recs, recs.data(), sizeof(ItemRec) * recs.size());
-  if (!witems.empty()) memcpy(m + L.wide_items, witems.data(), sizeof(Item) * witems.size());
-  if (!spans.empty()) memcpy(m + L.spans, spans.data(), sizeof(Span) * spans.size());
-  if (!rows.empty()) memcpy(m + L.rows, rows.data(), sizeof(Row) * rows.size());
-  if (!merge_rows.empty()) memcpy(m + L.merge_rows, merge_rows.data(), sizeof(int32_t) * merge_rows.size());
-  memcpy(m + L.merge_indptr, merge_indptr.data(), sizeof(int32_t) * merge_indptr.size());
-  if (!merge_parts.empty())
-    memcpy(m + L.merge_parts, merge_parts.data(), sizeof(int32_t) * merge_parts.size());
+  plan->meta.clear();
+  plan->meta.resize(L.total);
+  uint8_t* m = plan->meta.data();
+  {
+    const struct { size_t at; const void* src; size_t bytes; } parts[] = {
+        {L.seg_page_off, f.seg_page_indptr, S ? sizeof(int32_t) * S : 0},
+        {L.seg_len, f.seg_len, S ? sizeof(int32_t) * S : 0},
+        {L.page_ids, f.seg_page_ids, sizeof(int32_t) * (size_t)total_pages},
+        {L.items, items.data(), sizeof(Item) * items.size()},
+        {L.item_recs, recs.data(), sizeof(ItemRec) * recs.size()},
+        {L.wide_items, witems.data(), sizeof(Item) * witems.size()},
+        {L.spans, spans.data(), sizeof(Span) * spans.size()},
+        {L.rows, rows.data(), sizeof(Row) * rows.size()},
+        {L.merge_rows, merge_rows.data(), sizeof(int32_t) * merge_rows.size()},
+        {L.merge_indptr, merge_indptr.data(), sizeof(int32_t) * merge_indptr.size()},
+        {L.merge_parts, merge_parts.data(), sizeof(int32_t) * merge_parts.size()},
+    };
+    const size_t n = sizeof(parts) / sizeof(parts[0]);
+    for (size_t i = 0; i < n; ++i) {
+      const size_t end = i + 1 < n ? parts[i + 1].at : L.total;
+      if (parts[i].bytes) memcpy(m + parts[i].at, parts[i].src, parts[i].bytes);
+      memset(m + parts[i].at + parts[i].bytes, 0, end - parts[i].at - parts[i].bytes);
+    }
+  }
 
   // What halo_plan_update_lengths needs: the forest the plan was built for,
   // and for every segment the spans that end at its last key (with the
@@ -829,7 +903,13 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   return HALO_OK;
 }
 
-extern "C" void halo_plan_destroy(halo_plan_t* plan) { delete plan; }
+extern "C" void halo_plan_destroy(halo_plan_t* plan) {
+  if (plan) {
+    std::lock_guard<std::mutex> lock(g_spare_mu);
+    if (plan->meta.capacity() > g_spare_meta.capacity()) g_spare_meta.swap(plan->meta);
+  }
+  delete plan;
+}
 
 extern "C" halo_status_t halo_plan_get_stats(const halo_plan_t* plan, halo_plan_stats_t* st) {
   clear_error();
