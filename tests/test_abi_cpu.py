@@ -608,3 +608,39 @@ def test_update_lengths_refuses_other_changes(lib):
     # and a valid in-page append still applies afterwards
     assert plan.update_lengths(_csr([40, 12, 5, 31], pages, paths))
     assert plan.image() == halo.Plan.from_csr(params, _csr([40, 12, 5, 31], pages, paths)).image()
+
+
+def test_plans_from_concurrent_threads_match_sequential_plans(lib):
+    """The planner keeps its large arrays per thread between calls and
+    recycles the metadata image of destroyed plans: plans built by several
+    threads at once, each destroying the previous one, are byte for byte the
+    plans built one after another."""
+    import threading
+    rng = np.random.default_rng(2024)
+    cases = []
+    for k in range(12):
+        csr, n_pages = _random_decode_csr(rng, int(rng.integers(1, 120)))
+        cases.append((halo.make_params(16, 4, 128, torch.bfloat16, n_pages + 8, 0.1), csr))
+    want = [halo.Plan.from_csr(p, c).image() for p, c in cases]
+    got = [[None] * len(cases) for _ in range(4)]
+    errors = []
+
+    def worker(t):
+        try:
+            for rep in range(3):
+                for i in ([*range(len(cases))] if t % 2 == 0 else [*reversed(range(len(cases)))]):
+                    plan = halo.Plan.from_csr(*cases[i])
+                    got[t][i] = plan.image()
+                    del plan
+        except Exception as e:   # surfaced below
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(4)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
+    for t in range(4):
+        for i in range(len(cases)):
+            assert got[t][i] == want[i], f"thread {t} case {i}"
