@@ -587,24 +587,28 @@ def _plan_timing(halo, params, csr, device_meta, stream, repeats=7):
            "workspace_bytes": int(plan.workspace_bytes)}
     if csr.get("q_len") is None:
         # decode-append update: the next step's forest with one token more
-        # in every private segment whose last page has room (the others
-        # would open a page, which takes a new plan)
+        # in every private segment, a fresh page (id 0 stands in) for each
+        # segment whose last page is full
         import numpy as np
         refs = np.bincount(csr["req_seg_ids"], minlength=len(csr["seg_len"]))
-        room = (refs == 1) & (np.diff(csr["seg_page_indptr"]) * 16 > csr["seg_len"])
+        grow = (refs == 1).astype(np.int32)
         base = np.asarray(csr["seg_len"], np.int32)
+        indptr = np.asarray(csr["seg_page_indptr"], np.int32)
+        opens = (base + grow + 15) // 16 > np.diff(indptr)
+        nxt = dict(csr)
+        nxt["seg_len"] = base + grow
+        nxt["seg_page_ids"] = np.insert(np.asarray(csr["seg_page_ids"], np.int32), indptr[1:][opens], 0)
+        nxt["seg_page_indptr"] = np.concatenate([[0], np.cumsum(np.diff(indptr) + opens)]).astype(np.int32)
         us = []
         for k in range(repeats):
-            # alternately one token more and the plan's own lengths again
-            nxt = dict(csr)
-            nxt["seg_len"] = base + (room * (k % 2 == 0)).astype(np.int32)
+            # alternately one token more and the plan's own forest again
             t0 = time.perf_counter()
-            ok = plan.update_lengths(nxt)
+            ok = plan.update_lengths(nxt if k % 2 == 0 else csr)
             us.append((time.perf_counter() - t0) * 1e3)
             assert ok
         us.sort()
-        res.update({"update_ms": round(us[len(us) // 2], 4), "update_segments": int(room.sum()),
-                    "private_segments": int((refs == 1).sum())})
+        res.update({"update_ms": round(us[len(us) // 2], 4), "update_segments": int(grow.sum()),
+                    "update_pages_opened": int(opens.sum()), "private_segments": int((refs == 1).sum())})
     return res
 
 

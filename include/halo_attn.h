@@ -65,7 +65,7 @@ typedef enum {
   HALO_ERR_WORKSPACE_TOO_SMALL = 3,
   HALO_ERR_HIP = 4,                /* a HIP runtime call or kernel launch failed */
   HALO_ERR_REPLAN = 5              /* halo_plan_update_lengths: the forest changed
-                                      beyond tokens appended inside existing pages */
+                                      beyond what the plan can absorb in place */
 } halo_status_t;
 
 typedef enum { HALO_F32 = 0, HALO_BF16 = 1 } halo_dtype_t;
@@ -137,7 +137,11 @@ halo_status_t halo_plan_create(const halo_attn_params_t* params,
  *   shared_unit      narrow items of one shared chunk kept together on one
  *                    workgroup (0: 4)
  *   items_per_block  narrow items per workgroup, at most one per wave
- *                    (0: one per wave, 8 for bf16 and 4 for fp32) */
+ *                    (0: one per wave, 8 for bf16 and 4 for fp32)
+ *   append_reserve   decode plans: tokens every private segment (on one
+ *                    path) may gain through halo_plan_update_lengths before
+ *                    a new plan is needed; page-table room and span cuts
+ *                    are laid out for it (1..256; 0: 256) */
 typedef struct {
   int32_t kc_shared;
   int32_t kc_private;
@@ -147,6 +151,7 @@ typedef struct {
   int32_t wide_min_items;
   int32_t shared_unit;
   int32_t items_per_block;
+  int32_t append_reserve;
 } halo_plan_options_t;
 
 /* Fill *options with the defaults (every field "chosen by the planner"). */
@@ -164,17 +169,26 @@ halo_status_t halo_plan_create_with_options(const halo_attn_params_t* params,
 /* Decode-append update (§4.1: the plan of a decode batch is rebuilt every
  * step). Brings a decode plan up to date with `forest`, the plan's own
  * forest after tokens were appended to (or removed from) private segments
- * inside pages those segments already hold: same requests and paths, same
- * page tables, every shared segment (on two or more paths) unchanged, and
- * every other segment keeping its page count. The plan's decisions depend
- * on lengths rounded up to whole pages only, so the updated host image is
- * byte for byte the image halo_plan_create would build for `forest`; only
- * span ends, the matching inline first-span copies, the segment length
- * table and the statistics change. Cost: a comparison of the page tables
- * and work proportional to the spans of the changed segments.
+ * (segments on one path): same requests and paths, every other segment
+ * unchanged (length and pages), and each changed segment's page list its
+ * old list with pages appended at the end (or dropped from it). A private
+ * segment of length n at planning time can take any length in
+ * (b, n + append_reserve], b < n being the first key of its last span
+ * (for the caller: any length >= its planning-time length up to the
+ * reserve); its page table and last span were laid out with that room.
+ * Only span ends, the matching inline first-span copies and record page
+ * ids, the new page ids, the segment length table and the statistics
+ * change; the work decomposition stays the planning-time one. While no
+ * segment has changed its page count since planning, the updated host
+ * image is byte for byte the image halo_plan_create would build for
+ * `forest` (every decision looks at lengths in whole pages).
+ * Cost: a comparison of the page tables and work proportional to the spans
+ * of the changed segments.
  * Returns HALO_ERR_REPLAN, leaving the plan unchanged, when `forest` is
- * outside these bounds (build a new plan then). The caller re-uploads the
- * plan (halo_plan_upload) before the next run, and must not update a plan
+ * outside these bounds (build a new plan then), and
+ * HALO_ERR_INVALID_ARGUMENT, also leaving it unchanged, for a new page id
+ * outside [0, num_pool_pages). The caller re-uploads the plan
+ * (halo_plan_upload) before the next run, and must not update a plan
  * while an upload of it is still in flight. */
 halo_status_t halo_plan_update_lengths(halo_plan_t* plan, const halo_forest_t* forest);
 

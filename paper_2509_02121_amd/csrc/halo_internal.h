@@ -65,9 +65,14 @@ struct ItemRec {
   int32_t aux[16];
   int32_t page[32];
 };
-// Narrow items' spans are cut at this many keys, so that the first span's
-// page ids fit the record.
+// A narrow item's first span is cut at this many keys, so that its page
+// ids fit the record; later spans, like wide items' spans, at kMaxSpanKeys.
 constexpr int kNarrowSpanKeys = 512;
+// Growth room (tokens) a decode plan leaves every private segment for
+// halo_plan_update_lengths: the default, and the largest allowed (the span
+// cut that leaves the room assumes it is at most half of kNarrowSpanKeys).
+constexpr int kDefaultAppendReserve = 256;
+constexpr int kMaxAppendReserve = 256;
 
 // A contiguous range of keys of one segment, [key_begin, key_end).
 // key_begin is a multiple of kKeysPerStep and a span covers at most
@@ -110,10 +115,6 @@ struct MetaLayout {
   size_t total = 0;
 };
 
-// A decode plan's copy of its forest, and per segment the spans that end
-// at its last key (CSR over segments: tail_span[tail_indptr[s] ..
-// tail_indptr[s+1])), each with the image byte offset of the item whose
-// first span it is (-1 if none).
 // Allocator whose value-less construct() leaves the bytes as they are, so a
 // vector resized to hold the metadata image is not zero-filled first.
 template <typename T>
@@ -135,10 +136,18 @@ struct DefaultInitAlloc : std::allocator<T> {
   }
 };
 
+// A decode plan's copy of its forest; per segment its page slots in the
+// image (page_slot_off, S + 1 entries: a private segment has room for the
+// pages its growth reserve needs) and the lengths it may take in place,
+// (len_lo, len_hi]; and per segment the spans that end at its last key (CSR
+// over segments: tail_span[tail_indptr[s] .. tail_indptr[s+1])), each with
+// the image byte offsets of the item whose first span it is and of that
+// item's lane record (-1 if none).
 struct AppendIndex {
   std::vector<int32_t> seg_len, page_indptr, page_ids, req_indptr, req_ids, refs;
+  std::vector<int32_t> page_slot_off, len_lo, len_hi;
   std::vector<int32_t> tail_indptr, tail_span;
-  std::vector<int64_t> tail_item;
+  std::vector<int64_t> tail_item, tail_rec;
 };
 
 }  // namespace halo

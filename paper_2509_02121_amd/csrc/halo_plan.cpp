@@ -187,6 +187,7 @@ extern "C" void halo_plan_options_default(halo_plan_options_t* o) {
   o->wide_min_items = 0;
   o->shared_unit = 0;
   o->items_per_block = 0;
+  o->append_reserve = 0;
 }
 
 namespace {
@@ -203,6 +204,7 @@ halo_status_t check_options(const halo_plan_options_t& o) {
   if (o.wide_min_items < 0) return bad("wide_min_items must be >= 0");
   if (o.shared_unit < 0 || o.shared_unit > 64) return bad("shared_unit is 0..64");
   if (o.items_per_block < 0 || o.items_per_block > 8) return bad("items_per_block is 0..8");
+  if (o.append_reserve < 0 || o.append_reserve > kMaxAppendReserve) return bad("append_reserve is 0..256");
   return HALO_OK;
 }
 }  // namespace
@@ -506,6 +508,29 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     return protos[a].keys > protos[b].keys;
   });
 
+  // Page slots of the image: each segment's pages, and after those of a
+  // private segment of a decode plan (on at most one path) room for the
+  // pages its growth reserve can open, so that halo_plan_update_lengths
+  // never has to move another segment's page ids.
+  const int32_t reserve =
+      prefill ? 0 : (opt.append_reserve > 0 ? opt.append_reserve : kDefaultAppendReserve);
+  auto& slot_off = scratch<std::vector<int32_t>, 20>();
+  slot_off.assign(S + 1, 0);
+  for (int s = 0; s < S; ++s) {
+    const int64_t n = (int64_t)slot_off[s] + (f.seg_page_indptr[s + 1] - f.seg_page_indptr[s]) +
+                      (!prefill && refs[s] < 2 ? ceil_div(reserve, p.page_size) : 0);
+    if (n > (int64_t)std::numeric_limits<int32_t>::max()) {
+      delete plan;
+      return fail(HALO_ERR_INVALID_ARGUMENT, "too many pages");
+    }
+    slot_off[s + 1] = (int32_t)n;
+  }
+  auto& page_slots = scratch<std::vector<int32_t>, 21>();
+  page_slots.assign(slot_off[S], 0);
+  for (int s = 0; s < S; ++s)
+    std::copy(f.seg_page_ids + f.seg_page_indptr[s], f.seg_page_ids + f.seg_page_indptr[s + 1],
+              page_slots.begin() + slot_off[s]);
+
   auto& items = scratch<std::vector<Item>, 0>();
   auto& witems = scratch<std::vector<Item>, 1>();
   auto& item_chunk = scratch<std::vector<int32_t>, 2>();   // per narrow item: its proto's chunk id
@@ -521,8 +546,8 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       const Proto& pr = protos[i];
       n_rows_all += pr.rows.size();
       n_wide += pr.wide ? 1 : 0;
-      const int32_t max_keys = pr.wide ? kMaxSpanKeys : kNarrowSpanKeys;
-      for (const Span& sp : pr.spans) n_spans_all += (size_t)((sp.key_end - sp.key_begin + max_keys - 1) / max_keys);
+      for (const Span& sp : pr.spans)
+        n_spans_all += (size_t)((sp.key_end - sp.key_begin + kNarrowSpanKeys - 1) / kNarrowSpanKeys) + 1;
       if (!prefill && !is_final[i])
         for (const Row& row : pr.rows) parts_indptr[row.q_row + 1]++;
     }
@@ -566,17 +591,32 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     }
     if (pr.shared) plan->n_shared_items++;
     rows.insert(rows.end(), pr.rows.begin(), pr.rows.end());
-    // Split spans at kMaxSpanKeys (kNarrowSpanKeys for narrow items) and
-    // resolve their page-table offsets.
-    const int32_t max_keys = pr.wide ? kMaxSpanKeys : kNarrowSpanKeys;
-    for (const Span& sp : pr.spans)
-      for (int32_t kb = sp.key_begin; kb < sp.key_end; kb += max_keys) {
+    // Split spans: a narrow item's first span at kNarrowSpanKeys (its page
+    // ids travel in the item's record), every other span at kMaxSpanKeys
+    // (its page ids fill one 64-lane register); resolve their page slots.
+    // The last span of a private segment of a decode plan keeps `reserve`
+    // keys of room below its cap (when it would not, its keys are cut in
+    // two, the second part being a later span), so that
+    // halo_plan_update_lengths can grow it in place. The cut looks at whole
+    // pages only.
+    for (const Span& sp : pr.spans) {
+      const bool tail = !prefill && refs[sp.seg] == 1 && sp.key_end == f.seg_len[sp.seg];
+      const int32_t room = tail ? reserve : 0;
+      for (int32_t kb = sp.key_begin; kb < sp.key_end;) {
+        const bool first = !pr.wide && (int32_t)spans.size() == it.span_begin;
+        const int32_t cap = first ? kNarrowSpanKeys : kMaxSpanKeys;
+        const int32_t rest = (int32_t)paged(sp.key_end - kb);
+        const int32_t take = rest > cap            ? cap
+                             : rest + room <= cap ? rest
+                                                  : std::max(kKeysPerStep, rest / 2 / kKeysPerStep * kKeysPerStep);
         Span piece = sp;
         piece.key_begin = kb;
-        piece.key_end = std::min(sp.key_end, kb + max_keys);
-        piece.page_off = f.seg_page_indptr[sp.seg] + kb / p.page_size;
+        piece.key_end = std::min(sp.key_end, kb + take);
+        piece.page_off = slot_off[sp.seg] + kb / p.page_size;
         spans.push_back(piece);
+        kb += take;
       }
+    }
     it.n_spans = (int32_t)spans.size() - it.span_begin;
     if (it.n_spans > 0) {
       const Span& s0 = spans[it.span_begin];
@@ -786,7 +826,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
         if (it.n_spans > 0) {
           const Span& s0 = spans[it.span_begin];
           const int32_t np = (s0.key_end - s0.key_begin + p.page_size - 1) / p.page_size;
-          for (int32_t j = 0; j < np && j < 32; ++j) rc.page[j] = f.seg_page_ids[s0.page_off + j];
+          for (int32_t j = 0; j < np && j < 32; ++j) rc.page[j] = page_slots[s0.page_off + j];
         }
       }
     items.swap(dealt);
@@ -817,7 +857,7 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     off = align_up(off + bytes, 256);
     return o;
   };
-  const int64_t total_pages = S ? f.seg_page_indptr[S] : 0;
+  const int64_t total_pages = slot_off[S];
   plan->n_pages = (int32_t)total_pages;
   L.seg_page_off = place(sizeof(int32_t) * std::max(S, 1));
   L.seg_len = place(sizeof(int32_t) * std::max(S, 1));
@@ -843,9 +883,9 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   uint8_t* m = plan->meta.data();
   {
     const struct { size_t at; const void* src; size_t bytes; } parts[] = {
-        {L.seg_page_off, f.seg_page_indptr, S ? sizeof(int32_t) * S : 0},
+        {L.seg_page_off, slot_off.data(), S ? sizeof(int32_t) * S : 0},
         {L.seg_len, f.seg_len, S ? sizeof(int32_t) * S : 0},
-        {L.page_ids, f.seg_page_ids, sizeof(int32_t) * (size_t)total_pages},
+        {L.page_ids, page_slots.data(), sizeof(int32_t) * (size_t)total_pages},
         {L.items, items.data(), sizeof(Item) * items.size()},
         {L.item_recs, recs.data(), sizeof(ItemRec) * recs.size()},
         {L.wide_items, witems.data(), sizeof(Item) * witems.size()},
@@ -864,22 +904,27 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
   }
 
   // What halo_plan_update_lengths needs: the forest the plan was built for,
-  // and for every segment the spans that end at its last key (with the
-  // image offset of the item whose first span it is, whose inline copy of
-  // the span must follow).
+  // the page slots, and for every segment the spans that end at its last
+  // key (with the image offsets of the item whose first span it is, whose
+  // inline copy of the span must follow, and of that item's lane record),
+  // and the lengths it may take in place: above the first key of each of
+  // those spans, and within their caps and the segment's page slots.
   if (!prefill) {
     AppendIndex& ax = plan->append;
     const int64_t n_refs = f.req_seg_indptr[R];
     ax.seg_len.assign(f.seg_len, f.seg_len + S);
     ax.page_indptr.assign(f.seg_page_indptr, f.seg_page_indptr + S + 1);
-    ax.page_ids.assign(f.seg_page_ids, f.seg_page_ids + total_pages);
+    ax.page_ids.assign(f.seg_page_ids, f.seg_page_ids + (S ? f.seg_page_indptr[S] : 0));
     ax.req_indptr.assign(f.req_seg_indptr, f.req_seg_indptr + R + 1);
     ax.req_ids.assign(f.req_seg_ids, f.req_seg_ids + n_refs);
     ax.refs = refs;
-    std::vector<int64_t> first_of(spans.size(), -1);
+    ax.page_slot_off = slot_off;
+    std::vector<int64_t> first_of(spans.size(), -1), rec_of(spans.size(), -1);
     for (size_t i = 0; i < items.size(); ++i)
-      if (items[i].n_rows > 0 && items[i].n_spans > 0)
+      if (items[i].n_rows > 0 && items[i].n_spans > 0) {
         first_of[items[i].span_begin] = (int64_t)(L.items + i * sizeof(Item));
+        rec_of[items[i].span_begin] = (int64_t)(L.item_recs + i * sizeof(ItemRec));
+      }
     for (size_t i = 0; i < witems.size(); ++i)
       if (witems[i].n_spans > 0) first_of[witems[i].span_begin] = (int64_t)(L.wide_items + i * sizeof(Item));
     ax.tail_indptr.assign(S + 1, 0);
@@ -888,13 +933,28 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     for (int s = 0; s < S; ++s) ax.tail_indptr[s + 1] += ax.tail_indptr[s];
     ax.tail_span.resize(ax.tail_indptr[S]);
     ax.tail_item.resize(ax.tail_indptr[S]);
+    ax.tail_rec.resize(ax.tail_indptr[S]);
+    ax.len_lo.assign(S, -1);
+    ax.len_hi.resize(S);
+    for (int s = 0; s < S; ++s)
+      ax.len_hi[s] = refs[s] == 0 ? (slot_off[s + 1] - slot_off[s]) * p.page_size : f.seg_len[s];
     std::vector<int32_t> fill(ax.tail_indptr.begin(), ax.tail_indptr.end() - 1);
-    for (size_t i = 0; i < spans.size(); ++i)
-      if (spans[i].key_end == f.seg_len[spans[i].seg]) {
-        const int32_t k = fill[spans[i].seg]++;
-        ax.tail_span[k] = (int32_t)i;
-        ax.tail_item[k] = first_of[i];
+    for (size_t i = 0; i < spans.size(); ++i) {
+      const Span& sp = spans[i];
+      if (sp.key_end != f.seg_len[sp.seg]) continue;
+      const int32_t k = fill[sp.seg]++;
+      ax.tail_span[k] = (int32_t)i;
+      ax.tail_item[k] = first_of[i];
+      ax.tail_rec[k] = rec_of[i];
+      if (refs[sp.seg] == 1) {
+        const int32_t s = sp.seg;
+        const int32_t cap = rec_of[i] >= 0 ? kNarrowSpanKeys : kMaxSpanKeys;
+        const int32_t slots_end = (slot_off[s + 1] - slot_off[s]) * p.page_size;
+        const bool first_tail = k == ax.tail_indptr[s];
+        ax.len_lo[s] = std::max(ax.len_lo[s], sp.key_begin);
+        ax.len_hi[s] = std::min(first_tail ? slots_end : ax.len_hi[s], sp.key_begin + cap);
       }
+    }
   }
 
   *plan_out = plan;
@@ -983,33 +1043,66 @@ extern "C" halo_status_t halo_plan_update_lengths(halo_plan_t* plan, const halo_
     return b.empty() || (a && memcmp(a, b.data(), sizeof(int32_t) * b.size()) == 0);
   };
   if (f.num_segments != S || f.num_requests != R || !f.seg_len || !f.seg_page_indptr || !f.req_seg_indptr ||
-      !same(f.req_seg_indptr, ax.req_indptr) || !same(f.req_seg_ids, ax.req_ids) ||
-      !same(f.seg_page_indptr, ax.page_indptr) || !same(f.seg_page_ids, ax.page_ids))
-    return fail(HALO_ERR_REPLAN, "requests, paths or page tables differ from the plan's forest");
+      !same(f.req_seg_indptr, ax.req_indptr) || !same(f.req_seg_ids, ax.req_ids))
+    return fail(HALO_ERR_REPLAN, "requests or paths differ from the plan's forest");
+  if (f.seg_page_indptr[0] != 0 || (f.seg_page_indptr[S] > 0 && !f.seg_page_ids))
+    return fail(HALO_ERR_REPLAN, "malformed page table");
+  // Check everything before changing anything.
   const int32_t ps = plan->params.page_size;
+  bool pages_moved = false;
   for (int s = 0; s < S; ++s) {
     const int32_t len = f.seg_len[s], old = ax.seg_len[s];
-    if (len == old) continue;
-    const int64_t np = ax.page_indptr[s + 1] - ax.page_indptr[s];
-    if (len < 0 || ceil_div(len, ps) != np)
-      return fail(HALO_ERR_REPLAN, "segment " + std::to_string(s) + " changed its page count");
+    const int32_t* now = f.seg_page_ids + f.seg_page_indptr[s];
+    const int32_t* was = ax.page_ids.data() + ax.page_indptr[s];
+    const int64_t np = (int64_t)f.seg_page_indptr[s + 1] - f.seg_page_indptr[s];
+    const int64_t np_old = ax.page_indptr[s + 1] - ax.page_indptr[s];
+    if (len == old) {
+      if (np != np_old || (np && memcmp(now, was, sizeof(int32_t) * np) != 0))
+        return fail(HALO_ERR_REPLAN, "the pages of segment " + std::to_string(s) + " changed");
+      continue;
+    }
     if (ax.refs[s] >= 2) return fail(HALO_ERR_REPLAN, "shared segment " + std::to_string(s) + " changed length");
+    if (len <= ax.len_lo[s] || len > ax.len_hi[s])
+      return fail(HALO_ERR_REPLAN, "segment " + std::to_string(s) + " left the length range its plan can absorb");
+    if (np != ceil_div(len, ps))
+      return fail(HALO_ERR_REPLAN, "segment " + std::to_string(s) + " lists the wrong number of pages");
+    if (memcmp(now, was, sizeof(int32_t) * std::min(np, np_old)) != 0)
+      return fail(HALO_ERR_REPLAN, "the pages segment " + std::to_string(s) + " kept changed");
+    for (int64_t j = np_old; j < np; ++j)
+      if (now[j] < 0 || now[j] >= plan->params.num_pool_pages)
+        return fail(HALO_ERR_INVALID_ARGUMENT, "page id out of range in segment " + std::to_string(s));
+    pages_moved |= np != np_old;
   }
   uint8_t* m = plan->meta.data();
   const MetaLayout& L = plan->layout;
   AppendIndex& mx = plan->append;
+  int32_t* slots = reinterpret_cast<int32_t*>(m + L.page_ids);
   for (int s = 0; s < S; ++s) {
     const int32_t len = f.seg_len[s], old = mx.seg_len[s];
     if (len == old) continue;
+    const int64_t np = ceil_div(len, ps), np_old = ceil_div(old, ps);
+    if (np > np_old)
+      memcpy(slots + mx.page_slot_off[s] + np_old, f.seg_page_ids + f.seg_page_indptr[s] + np_old,
+             sizeof(int32_t) * (np - np_old));
     for (int32_t k = mx.tail_indptr[s]; k < mx.tail_indptr[s + 1]; ++k) {
       Span* sp = reinterpret_cast<Span*>(m + L.spans) + mx.tail_span[k];
       sp->key_end = len;
       if (mx.tail_item[k] >= 0) reinterpret_cast<Item*>(m + mx.tail_item[k])->s0_key_end = len;
+      if (mx.tail_rec[k] >= 0 && np != np_old) {
+        // the record holds the span's first 32 page ids
+        ItemRec* rc = reinterpret_cast<ItemRec*>(m + mx.tail_rec[k]);
+        const int64_t n = std::min<int64_t>(32, ceil_div(len - sp->key_begin, ps));
+        for (int64_t j = 0; j < n; ++j) rc->page[j] = slots[sp->page_off + j];
+      }
     }
     reinterpret_cast<int32_t*>(m + L.seg_len)[s] = len;
     plan->distinct_kv_tokens += len - old;
     plan->visible_pairs += (int64_t)(len - old) * mx.refs[s] * plan->params.num_q_heads;
     mx.seg_len[s] = len;
+  }
+  if (pages_moved) {
+    mx.page_indptr.assign(f.seg_page_indptr, f.seg_page_indptr + S + 1);
+    mx.page_ids.assign(f.seg_page_ids, f.seg_page_ids + f.seg_page_indptr[S]);
   }
   return HALO_OK;
 }

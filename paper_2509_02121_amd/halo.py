@@ -63,7 +63,7 @@ class PlanOptions(ctypes.Structure):
     by the planner); see include/halo_attn.h."""
     _fields_ = [(n, ctypes.c_int32) for n in (
         "kc_shared", "kc_private", "wide", "wide_rows", "kc_wide", "wide_min_items", "shared_unit",
-        "items_per_block")]
+        "items_per_block", "append_reserve")]
 
 
 EXPORTED_SYMBOLS = (

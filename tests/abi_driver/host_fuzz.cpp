@@ -132,6 +132,7 @@ halo_plan_options_t random_options() {
   o.wide_min_items = uniform(0, 300);
   o.shared_unit = uniform(0, 8);
   o.items_per_block = uniform(0, 8);
+  o.append_reserve = uniform(0, 256);
   return o;
 }
 
@@ -164,6 +165,7 @@ void one_case(bool prefill) {
   CHECK(image_of(plan).size() == meta);
   if (!prefill) {
     // tokens appended inside existing pages of private segments
+    const std::vector<int32_t> base_len = fo.seg_len;
     std::vector<int32_t> refs(fo.seg_len.size(), 0);
     for (int32_t s : fo.req_ids) refs[s]++;
     for (int round = 0; round < 2; ++round) {
@@ -180,17 +182,35 @@ void one_case(bool prefill) {
         halo_plan_destroy(fresh);
       }
     }
-    // a new page for some segment: refused, plan unchanged
+    // a page opened within the reserve: applied; a private segment grown
+    // far past it, or a shared segment that opens a page: refused, plan
+    // unchanged
     if (fo.seg_len.empty()) {
       halo_plan_destroy(plan);
       return;
     }
+    const int reserve = opt.append_reserve > 0 ? opt.append_reserve : 256;
+    auto open_pages = [&](const Forest& from, int s, int32_t len) {
+      Forest g = from;
+      const int32_t add = (len + 15) / 16 - (g.page_indptr[s + 1] - g.page_indptr[s]);
+      g.seg_len[s] = len;
+      for (int32_t k = 0; k < add; ++k) {
+        g.page_ids.insert(g.page_ids.begin() + g.page_indptr[s + 1], g.pool_pages - 1);
+        for (size_t j = s + 1; j < g.page_indptr.size(); ++j) g.page_indptr[j]++;
+      }
+      return g;
+    };
+    const int s = uniform(0, (int)fo.seg_len.size() - 1);
+    const int32_t len0 = base_len[s];
+    if (refs[s] == 1 && len0 > 0 && fo.seg_len[s] >= len0) {
+      const int32_t to = std::max(fo.seg_len[s], len0 + uniform(0, reserve));
+      Forest g = open_pages(fo, s, to);
+      f = g.view();
+      CHECK(halo_plan_update_lengths(plan, &f) == HALO_OK);
+      fo = g;
+    }
     const std::vector<uint8_t> before = image_of(plan);
-    Forest grown = fo;
-    const int s = uniform(0, (int)grown.seg_len.size() - 1);
-    grown.seg_len[s] = (grown.page_indptr[s + 1] - grown.page_indptr[s]) * 16 + 1;
-    for (size_t k = s + 1; k < grown.page_indptr.size(); ++k) grown.page_indptr[k]++;
-    grown.page_ids.insert(grown.page_ids.begin() + grown.page_indptr[s + 1] - 1, grown.pool_pages - 1);
+    Forest grown = open_pages(fo, s, (refs[s] >= 2 ? fo.seg_len[s] : len0) + 1100);
     f = grown.view();
     CHECK(halo_plan_update_lengths(plan, &f) == HALO_ERR_REPLAN);
     CHECK(image_of(plan) == before);

@@ -7,6 +7,8 @@ import os
 import re
 import subprocess
 
+import types
+
 import numpy as np
 import pytest
 import torch
@@ -580,21 +582,26 @@ def test_update_lengths_on_the_seeded_decode_batches(lib, index):
 
 
 def test_update_lengths_refuses_other_changes(lib):
-    """A new page, a grown shared segment, another path, a prefill forest:
-    HALO_ERR_REPLAN and the plan left as it was."""
+    """A grown shared segment, another path, moved pages, a page list that
+    does not match the length, growth past the reserve, a prefill forest:
+    HALO_ERR_REPLAN and the plan left as it was; a new page id outside the
+    pool: an argument error, the plan left as it was too."""
     seg_len = [40, 10, 5, 30]            # segment 0 shared by requests 0 and 1
     pages = [[0, 1, 2], [3], [4], [5, 6]]
     paths = [[0, 1], [0, 2], [3]]
     csr = _csr(seg_len, pages, paths)
-    params = halo.AttnParams(4, 2, 64, 16, 8, halo.HALO_F32, halo.HALO_F32, 0.125)
-    plan = halo.Plan.from_csr(params, csr)
+    params = halo.AttnParams(4, 2, 64, 16, 64, halo.HALO_F32, halo.HALO_F32, 0.125)
+    plan = halo.Plan.from_csr(params, csr, {"append_reserve": 32})
     before = plan.image()
+    grown = [[0, 1, 2], [3, 7, 8, 9], [4], [5, 6]]
     bad = [
-        _csr([40, 17, 5, 30], [[0, 1, 2], [3, 7], [4], [5, 6]], paths),   # a new page
         _csr([41, 10, 5, 30], pages, paths),                              # shared segment grew
         _csr(seg_len, pages, [[0, 1], [0, 2], [0, 3]]),                    # another path
         _csr(seg_len, [[0, 1, 2], [3], [4], [6, 5]], paths),               # pages moved
         _csr([40, 17, 5, 30], pages, paths),                               # past the page end
+        _csr([40, 17, 5, 30], [[0, 1, 2], [9, 7], [4], [5, 6]], paths),   # a kept page replaced
+        _csr([40, 60, 5, 30], grown, paths),                               # past the reserve
+        _csr([40, 10, 5, 0], [[0, 1, 2], [3], [4], []], paths),            # emptied
     ]
     for c in bad:
         try:
@@ -603,11 +610,126 @@ def test_update_lengths_refuses_other_changes(lib):
             ok = None
         assert ok is False, c
         assert plan.image() == before
+    with pytest.raises(halo.HaloError, match="page id out of range"):
+        plan.update_lengths(_csr([40, 17, 5, 30], [[0, 1, 2], [3, 64], [4], [5, 6]], paths))
+    assert plan.image() == before
     pf = halo.Plan.from_csr(params, _csr([40, 10, 5, 30], pages, paths, q_len=[10, 5, 30]))
     assert pf.update_lengths(_csr([40, 10, 5, 30], pages, paths, q_len=[10, 5, 30])) is False
     # and a valid in-page append still applies afterwards
     assert plan.update_lengths(_csr([40, 12, 5, 31], pages, paths))
-    assert plan.image() == halo.Plan.from_csr(params, _csr([40, 12, 5, 31], pages, paths)).image()
+    fresh = halo.Plan.from_csr(params, _csr([40, 12, 5, 31], pages, paths), {"append_reserve": 32})
+    assert plan.image() == fresh.image()
+    # as do new pages within the reserve (10 + 32 tokens)
+    assert plan.update_lengths(_csr([40, 42, 5, 31], [[0, 1, 2], [3, 7, 8], [4], [5, 6]], paths))
+
+
+def _decode_view(csr, hq, hkv, d, dtype):
+    """The fields the plan checker reads, for a decode forest in CSR form."""
+    ip, ids = csr["seg_page_indptr"], csr["seg_page_ids"]
+    rp, rs = csr["req_seg_indptr"], csr["req_seg_ids"]
+    n_req = len(rp) - 1
+    return types.SimpleNamespace(
+        num_q_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype, is_prefill=False,
+        seg_len=np.asarray(csr["seg_len"]), req_paths=[list(rs[rp[r]:rp[r + 1]]) for r in range(n_req)],
+        seg_pages=[np.asarray(ids[ip[s]:ip[s + 1]]) for s in range(len(ip) - 1)],
+        q=np.zeros((n_req, 1)))
+
+
+def _append(csr, add, next_page):
+    """`csr` with add[s] tokens appended to segment s (negative: removed),
+    fresh page ids from next_page on for the pages that opens (pages no
+    longer needed are dropped). Returns the new forest and the next free id."""
+    lens = np.asarray(csr["seg_len"], np.int64)
+    new_len = lens + np.asarray(add, np.int64)
+    ip, ids = csr["seg_page_indptr"], csr["seg_page_ids"]
+    out_pages = []
+    for s in range(len(lens)):
+        have = list(ids[ip[s]:ip[s + 1]])
+        need = (int(new_len[s]) + 15) // 16
+        while len(have) < need:
+            have.append(next_page)
+            next_page += 1
+        out_pages.append(have[:need])
+    paths = [list(csr["req_seg_ids"][csr["req_seg_indptr"][r]:csr["req_seg_indptr"][r + 1]])
+             for r in range(len(csr["req_seg_indptr"]) - 1)]
+    return _csr(new_len.tolist(), out_pages, paths), next_page
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_update_lengths_opens_pages_within_the_reserve(lib, seed):
+    """Private segments grow (and shrink back) by random amounts within the
+    reserve, opening pages with fresh ids: every update applies in place,
+    and the updated plan's work lists cover exactly the new forest's keys
+    (each once), with each span's page ids and each record's pages those of
+    the new page table; the statistics are a fresh plan's."""
+    rng = np.random.default_rng(900 + seed)
+    hkv, g, dtype, tdt = [(2, 4, halo.HALO_BF16, torch.bfloat16), (1, 8, halo.HALO_BF16, torch.bfloat16),
+                          (2, 2, halo.HALO_F32, torch.float32)][seed % 3]
+    reserve = [0, 64, 1, 200, 256][seed % 5]
+    csr, next_page = _random_decode_csr(rng, int(rng.integers(2, 40)), max_len=int(rng.choice([300, 1500])))
+    params = halo.AttnParams(hkv * g, hkv, 128, 16, 1 << 20, dtype, dtype, 0.1)
+    opts = {"append_reserve": reserve}
+    plan = halo.Plan.from_csr(params, csr, opts)
+    len0 = np.asarray(csr["seg_len"], np.int64)
+    refs = np.bincount(csr["req_seg_ids"], minlength=len(len0))
+    room = reserve if reserve > 0 else 256
+    opened = 0
+    for _ in range(5):
+        cur = np.asarray(csr["seg_len"], np.int64)
+        target = len0 + rng.integers(0, room + 1, size=len(len0))
+        pick = (refs == 1) & (len0 > 0) & (rng.random(len(len0)) < 0.7)
+        add = np.where(pick, target - cur, 0)
+        before_pages = np.diff(csr["seg_page_indptr"])
+        csr, next_page = _append(csr, add, next_page)
+        opened += int((np.diff(csr["seg_page_indptr"]) != before_pages).sum())
+        assert plan.update_lengths(csr)
+        _check_plan(_decode_view(csr, hkv * g, hkv, 128, tdt), plan)
+        fresh = halo.Plan.from_csr(params, csr, opts).stats()
+        st = plan.stats()
+        assert (st["visible_pairs"], st["distinct_kv_tokens"]) == (fresh["visible_pairs"],
+                                                                   fresh["distinct_kv_tokens"])
+    assert opened > 0 or room < 16
+    # one token past what a span or the page slots can hold asks for a new plan
+    s = int(np.nonzero((refs == 1) & (len0 > 0))[0][0])
+    add = np.zeros(len(len0), np.int64)
+    add[s] = int(len0[s]) + 1100 - int(np.asarray(csr["seg_len"])[s])
+    far, _ = _append(csr, add, next_page)
+    before = plan.image()
+    assert plan.update_lengths(far) is False and plan.image() == before
+
+
+def test_update_lengths_follows_a_decode_loop_of_the_70b_shaped_batch(lib):
+    """The 70B-shaped batch (forest only, pages in order): every request
+    appends one token per step, opening a page every 16 steps; with the
+    default reserve (256 tokens) all 256 steps update the plan in place."""
+    from workloads import synth
+    rng = np.random.Generator(np.random.PCG64(1004))
+    seg_len, paths, _ = synth._forest(4, rng)
+    pages, nxt = [], 0
+    for n in seg_len:
+        pages.append(list(range(nxt, nxt + (int(n) + 15) // 16)))
+        nxt += (int(n) + 15) // 16
+    csr = _csr([int(n) for n in seg_len], pages, paths)
+    params = halo.AttnParams(64, 8, 128, 16, 1 << 22, halo.HALO_BF16, halo.HALO_BF16, 128 ** -0.5)
+    plan = halo.Plan.from_csr(params, csr)
+    refs = np.bincount(csr["req_seg_ids"], minlength=len(csr["seg_len"]))
+    one = (refs == 1).astype(np.int64)
+    lens = np.asarray(csr["seg_len"], np.int64)
+    ip = np.asarray(csr["seg_page_indptr"], np.int64)
+    ids = np.asarray(csr["seg_page_ids"], np.int32)
+    for step in range(256):
+        # one token more per request; a fresh id for each page that opens
+        opens = (lens + one + 15) // 16 > np.diff(ip)
+        fresh_ids = np.arange(nxt, nxt + int(opens.sum()), dtype=np.int32)
+        nxt += int(opens.sum())
+        ids = np.insert(ids, ip[1:][opens], fresh_ids)
+        ip = np.concatenate([[0], np.cumsum(np.diff(ip) + opens)])
+        lens = lens + one
+        c = dict(csr, seg_len=lens.astype(np.int32), seg_page_indptr=ip.astype(np.int32), seg_page_ids=ids)
+        assert plan.update_lengths(c), step
+    st = plan.stats()
+    assert st["distinct_kv_tokens"] == int(lens.sum())
+    _check_plan(_decode_view(c, 64, 8, 128, torch.bfloat16), plan)
 
 
 def test_plans_from_concurrent_threads_match_sequential_plans(lib):

@@ -1,8 +1,8 @@
 """A decode loop end to end (GPU): prompts as token ids -> prefix forest ->
 each segment's K/V written once -> for several steps, every request appends
 its new token to its private segment (a fresh page at page boundaries), the
-plan is brought up to date (updated in place when no request opened a page,
-else rebuilt), and decode attention is compared with the oracle's
+plan is brought up to date in place (new pages included: the plan keeps
+room for them), and decode attention is compared with the oracle's
 unshared attention over the request's whole token sequence (§3)."""
 
 import types
@@ -79,7 +79,7 @@ def test_decode_loop_over_token_id_forest(gpu_lib):
           torch.cat(ks), torch.cat(vs))
 
     tokens = [list(p) for p in prompts]
-    pa, applied = None, 0
+    pa, applied, opened = None, 0, 0
     for step in range(12):
         new = rng.integers(0, 1000, size=R).tolist()
         starts = []
@@ -87,6 +87,7 @@ def test_decode_loop_over_token_id_forest(gpu_lib):
             s = leaf[r]
             if seg_len[s] == len(seg_pages[s]) * PAGE:
                 seg_pages[s].append(free.pop())               # a fresh page for the new token
+                opened += pa is not None
             starts.append(int(seg_len[s]))
         k, v = kv(new, [len(tokens[r]) for r in range(R)])
         write(leaf, starts, [1] * R, k, v)
@@ -102,9 +103,10 @@ def test_decode_loop_over_token_id_forest(gpu_lib):
         if pa is None:
             pa = halo.PrefixAttention(params, csr, dev)
         elif pa.update(csr):
-            # the in-place length update: byte for byte a fresh plan
             applied += 1
-            assert pa.plan.image() == halo.Plan.from_csr(params, csr).image()
+            if opened == 0:
+                # no page opened since planning: byte for byte a fresh plan
+                assert pa.plan.image() == halo.Plan.from_csr(params, csr).image()
         o, lse = pa.run(q.to(dev), kp, vp)
         torch.cuda.synchronize()
         seg_k, seg_v = {}, {}
@@ -114,6 +116,6 @@ def test_decode_loop_over_token_id_forest(gpu_lib):
         o_ref, lse_ref = oracle.decode(q.double().numpy(), seg_k, seg_v, [[r] for r in range(R)], scale)
         assert_parity(types.SimpleNamespace(dtype=dtype), o.double().cpu().numpy(), lse.double().cpu().numpy(),
                       o_ref, lse_ref, np.arange(R), f"decode step {step}")
-    # steps where no request opened a page reuse the plan
-    print(f"plan updated in place on {applied} of 11 steps", flush=True)
-    assert applied > 0
+    # every step after the first updates the plan in place, pages opened too
+    print(f"plan updated in place on {applied} of 11 steps, {opened} pages opened", flush=True)
+    assert applied == 11 and opened > 0
