@@ -64,3 +64,42 @@ def test_mixed_wide_and_narrow_launch_cycles(gpu_lib, n_req, wide_rows):
     o, lse = _run(w, {"wide": 1, "wide_rows": wide_rows, "kc_wide": 64})
     ro, rl, rows = oracle_for(w)
     assert_parity(w, o, lse, ro, rl, rows, f"cycles {n_req} {wide_rows}")
+
+
+@pytest.mark.parametrize("dtype,d,opts", [
+    (torch.float32, 64, None), (torch.float32, 128, {"kc_private": 4096}),
+    (torch.bfloat16, 128, {"kc_private": 4096, "append_reserve": 100}), (torch.bfloat16, 128, None)],
+    ids=["f32-d64", "f32-d128-kc4096", "bf16-kc4096-r100", "bf16"])
+def test_long_private_spans_and_grown_plans(gpu_lib, dtype, d, opts):
+    """Private suffixes of 600-3000 keys: items whose later spans run to
+    1024 keys and last spans cut to leave the growth reserve. Oracle parity
+    for a fresh plan, and for a plan made for shorter suffixes (up to the
+    reserve less, fewer pages) and then brought up to the full forest in
+    place, its new page ids included."""
+    print(f"case: long private spans {dtype} d={d} {opts}", flush=True)
+    rng = np.random.default_rng(4242 + d)
+    n_req = 12
+    seg_len = [int(rng.integers(100, 700))] + [int(x) for x in rng.integers(600, 3000, size=n_req)]
+    paths = [[0, 1 + r] if r % 3 else [1 + r] for r in range(n_req)]
+    w = build_workload("long", 500 + d, 8, 2, d, dtype, seg_len, paths, None,
+                       value_scale=0.5 if dtype == torch.bfloat16 else 1.0)
+    o, lse = _run(w, opts)
+    ro, rl, rows = oracle_for(w)
+    assert_parity(w, o, lse, ro, rl, rows, f"long fresh {dtype} {d}")
+    reserve = (opts or {}).get("append_reserve", 256)
+    full = w.forest_csr()
+    short = {k: (None if v is None else np.array(v)) for k, v in full.items()}
+    cut = np.zeros(len(seg_len), np.int64)
+    cut[1:] = rng.integers(1, reserve + 1, size=n_req)
+    short_len = np.asarray(full["seg_len"], np.int64) - cut
+    pages = [list(p[:(int(n) + 15) // 16]) for p, n in zip(w.seg_pages, short_len)]
+    short["seg_len"] = short_len.astype(np.int32)
+    short["seg_page_indptr"] = np.concatenate([[0], np.cumsum([len(p) for p in pages])]).astype(np.int32)
+    short["seg_page_ids"] = np.concatenate(pages).astype(np.int32)
+    assert (np.diff(short["seg_page_indptr"]) < np.diff(full["seg_page_indptr"])).any()
+    pa = halo.PrefixAttention(params_of(w), short, "cuda", opts)
+    assert pa.update(full), "growth within the reserve updates in place"
+    o, lse = pa.run(w.q, w.k_pool, w.v_pool)
+    torch.cuda.synchronize()
+    assert_parity(w, o.double().cpu().numpy(), lse.double().cpu().numpy(), ro, rl, rows,
+                  f"long grown {dtype} {d}")
