@@ -602,17 +602,17 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     for (const Span& sp : pr.spans) {
       const bool tail = !prefill && refs[sp.seg] == 1 && sp.key_end == f.seg_len[sp.seg];
       const int32_t room = tail ? reserve : 0;
-      for (int32_t kb = sp.key_begin; kb < sp.key_end;) {
+      for (int64_t kb = sp.key_begin; kb < sp.key_end;) {
         const bool first = !pr.wide && (int32_t)spans.size() == it.span_begin;
         const int32_t cap = first ? kNarrowSpanKeys : kMaxSpanKeys;
-        const int32_t rest = (int32_t)paged(sp.key_end - kb);
-        const int32_t take = rest > cap            ? cap
+        const int64_t rest = paged(sp.key_end - kb);
+        const int64_t take = rest > cap            ? cap
                              : rest + room <= cap ? rest
-                                                  : std::max(kKeysPerStep, rest / 2 / kKeysPerStep * kKeysPerStep);
+                                                  : std::max<int64_t>(kKeysPerStep, rest / 2 / kKeysPerStep * kKeysPerStep);
         Span piece = sp;
-        piece.key_begin = kb;
-        piece.key_end = std::min(sp.key_end, kb + take);
-        piece.page_off = slot_off[sp.seg] + kb / p.page_size;
+        piece.key_begin = (int32_t)kb;
+        piece.key_end = (int32_t)std::min<int64_t>(sp.key_end, kb + take);
+        piece.page_off = slot_off[sp.seg] + (int32_t)(kb / p.page_size);
         spans.push_back(piece);
         kb += take;
       }
@@ -936,8 +936,10 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
     ax.tail_rec.resize(ax.tail_indptr[S]);
     ax.len_lo.assign(S, -1);
     ax.len_hi.resize(S);
+    // (lengths past the int32 range are never reached: clamp)
+    auto clamp32 = [](int64_t v) { return (int32_t)std::min<int64_t>(v, std::numeric_limits<int32_t>::max()); };
     for (int s = 0; s < S; ++s)
-      ax.len_hi[s] = refs[s] == 0 ? (slot_off[s + 1] - slot_off[s]) * p.page_size : f.seg_len[s];
+      ax.len_hi[s] = refs[s] == 0 ? clamp32((int64_t)(slot_off[s + 1] - slot_off[s]) * p.page_size) : f.seg_len[s];
     std::vector<int32_t> fill(ax.tail_indptr.begin(), ax.tail_indptr.end() - 1);
     for (size_t i = 0; i < spans.size(); ++i) {
       const Span& sp = spans[i];
@@ -949,10 +951,10 @@ extern "C" halo_status_t halo_plan_create_with_options(const halo_attn_params_t*
       if (refs[sp.seg] == 1) {
         const int32_t s = sp.seg;
         const int32_t cap = rec_of[i] >= 0 ? kNarrowSpanKeys : kMaxSpanKeys;
-        const int32_t slots_end = (slot_off[s + 1] - slot_off[s]) * p.page_size;
+        const int32_t slots_end = clamp32((int64_t)(slot_off[s + 1] - slot_off[s]) * p.page_size);
         const bool first_tail = k == ax.tail_indptr[s];
         ax.len_lo[s] = std::max(ax.len_lo[s], sp.key_begin);
-        ax.len_hi[s] = std::min(first_tail ? slots_end : ax.len_hi[s], sp.key_begin + cap);
+        ax.len_hi[s] = std::min(first_tail ? slots_end : ax.len_hi[s], clamp32((int64_t)sp.key_begin + cap));
       }
     }
   }
