@@ -463,6 +463,9 @@ def main():
     ap.add_argument("--gather", action="store_true",
                     help="only time the page gather of the workload's whole working set (every "
                          "segment, K and V pools) into dense token-major buffers")
+    ap.add_argument("--decode-loop", action="store_true",
+                    help="only time a decode loop: per step one token more per request, the plan "
+                         "update and upload, and the attention call (wall clock and GPU time)")
     args = ap.parse_args()
     if args.probe_read_bytes:
         if args.gpus != 1:
@@ -481,6 +484,12 @@ def main():
             print("bench.py measures one GPU only", file=sys.stderr)
             sys.exit(2)
         gather_bench(args)
+        return
+    if args.decode_loop:
+        if args.gpus != 1:
+            print("bench.py measures one GPU only", file=sys.stderr)
+            sys.exit(2)
+        decode_loop_bench(args)
         return
     if args.write_path:
         if args.gpus != 1:
@@ -610,6 +619,111 @@ def _plan_timing(halo, params, csr, device_meta, stream, repeats=7):
         res.update({"update_ms": round(us[len(us) // 2], 4), "update_segments": int(grow.sum()),
                     "update_pages_opened": int(opens.sum()), "private_segments": int((refs == 1).sum())})
     return res
+
+
+def _decode_loop_pages(name, n_steps):
+    """Spare pages a decode loop of n_steps steps needs: every private
+    segment opens a page every 16 steps."""
+    import numpy as np
+    from workloads import synth
+    index = synth.CONFIG_NAMES.index(name)
+    seg_len, paths, _ = synth._forest(index, np.random.Generator(np.random.PCG64(1000 + index)))
+    refs = np.bincount(np.concatenate([np.asarray(p) for p in paths]), minlength=len(seg_len))
+    return int((refs == 1).sum()) * (n_steps // 16 + 2)
+
+
+def decode_loop_bench(args):
+    """A decode loop (one JSON line): each step every request appends one
+    token to its private suffix (a spare page of the pool when its last page
+    is full), the plan follows (halo_plan_update_lengths, a new plan when
+    that refuses), its metadata is uploaded into the buffer the running step
+    does not read (a copy stream of its own), and the attention call runs.
+    The step forests are built before the timed region: they are the
+    serving system's state, not the library's work. Timed: `steps` steps,
+    wall clock on the host (update + upload + call, so host work that does
+    not overlap the GPU shows) and HIP events on the compute stream. The new
+    tokens' K/V are not written (the pool's seeded values stand in; the
+    work does not depend on them)."""
+    import numpy as np
+    import torch
+    from paper_2509_02121_amd import halo
+    from workloads import make_config
+
+    halo.load_library(require_gpu=True)
+    dev = torch.device("cuda", 0)
+    n_steps = args.warmup + args.steps
+    w = make_config(args.workload, device=dev, poison=False,
+                    extra_pages=_decode_loop_pages(args.workload, n_steps))
+    if w.is_prefill:
+        print("--decode-loop needs a decode workload", file=sys.stderr)
+        sys.exit(2)
+    params = halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages,
+                              w.scale, w.dtype)
+    csr0 = w.forest_csr()
+    refs = np.bincount(csr0["req_seg_ids"], minlength=len(csr0["seg_len"]))
+    grow = (refs == 1).astype(np.int64)
+    used = np.zeros(w.num_pool_pages, bool)
+    used[csr0["seg_page_ids"]] = True
+    free = np.nonzero(~used)[0].astype(np.int32)
+    lens = np.asarray(csr0["seg_len"], np.int64)
+    ip = np.asarray(csr0["seg_page_indptr"], np.int64)
+    ids = np.asarray(csr0["seg_page_ids"], np.int32)
+    nf, forests = 0, []
+    for _ in range(n_steps):
+        opens = (lens + grow + 15) // 16 > np.diff(ip)
+        k = int(opens.sum())
+        if nf + k > len(free):
+            print("--decode-loop: the pool has too few spare pages for that many steps", file=sys.stderr)
+            sys.exit(2)
+        ids = np.insert(ids, ip[1:][opens], free[nf:nf + k])
+        nf += k
+        ip = np.concatenate([[0], np.cumsum(np.diff(ip) + opens)])
+        lens = lens + grow
+        forests.append(dict(csr0, seg_len=lens.astype(np.int32), seg_page_indptr=ip.astype(np.int32),
+                            seg_page_ids=ids))
+    runner = halo.PrefixAttention(params, csr0, dev)
+    o, lse = runner.alloc_outputs(w.q)
+    stream = torch.cuda.current_stream()
+    host_ms, applied = [], 0
+
+    def step(i):
+        t0 = time.perf_counter()
+        ok = runner.update(forests[i])
+        host_ms.append((time.perf_counter() - t0) * 1e3)
+        runner.run(w.q, w.k_pool, w.v_pool, o, lse)
+        return ok
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    host_ms.clear()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for i in range(args.warmup, n_steps):
+        applied += int(step(i))
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / args.steps
+    gpu = e0.elapsed_time(e1) / args.steps
+    host_ms.sort()
+    # the batch grows by a token per request and step: the attention call
+    # alone on the timed region's first and last forest, for reference
+    ref = []
+    for f in (forests[args.warmup], forests[-1]):
+        pa = halo.PrefixAttention(params, f, dev)
+        ref.append(_time_launches(pa.bind(w.q, w.k_pool, w.v_pool, o, lse, stream), 20, 5, stream) / 1e3)
+        del pa
+    print(json.dumps({
+        "metric": "decode loop: time per step (plan update + metadata upload + attention call)",
+        "value": round(wall, 5), "unit": "ms/step", "higher_is_better": False, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "gpu_ms_per_step": round(gpu, 5),
+        "host_update_ms_median": round(host_ms[len(host_ms) // 2], 4),
+        "attention_only_ms_first_last": [round(x, 5) for x in ref],
+        "overhead_vs_attention_only": round(gpu / (0.5 * (ref[0] + ref[1])) - 1, 4),
+        "steps_updated_in_place": applied, "pages_opened": int(nf), "dtype": "bf16" if w.dtype.itemsize == 2 else "f32",
+        "data": "synthetic", "config": {"workload": w.name, "requests": len(w.req_paths)}}), flush=True)
 
 
 def measure_workload(name, args, dev, pool_fill=0.0, with_cpu=False, percentiles=False):

@@ -192,11 +192,22 @@ halo_status_t halo_plan_create_with_options(const halo_attn_params_t* params,
  * while an upload of it is still in flight. */
 halo_status_t halo_plan_update_lengths(halo_plan_t* plan, const halo_forest_t* forest);
 
-/* Copy the plan's metadata (page ids, work lists) into device_meta, a caller-owned 256-byte aligned device buffer of at least
+/* Copy the plan's metadata (page ids, work lists) into device_meta, a
+ * caller-owned 256-byte aligned device buffer of at least
  * device_meta_bytes, asynchronously on stream. The plan must stay alive
  * until the copy has completed. */
 halo_status_t halo_plan_upload(const halo_plan_t* plan, void* device_meta,
                                size_t device_meta_bytes, void* stream);
+
+/* halo_plan_upload of only what halo_plan_update_lengths can change (the
+ * segment lengths, page ids, work items, their records and spans: about
+ * half of a decode plan's metadata), for a decode loop that updates its
+ * plan in place every step. device_meta must already hold an upload of
+ * this same plan (halo_plan_upload, or this call, after any number of
+ * updates since); after halo_plan_create, use halo_plan_upload. Same
+ * arguments, errors and lifetime rules as halo_plan_upload. */
+halo_status_t halo_plan_upload_update(const halo_plan_t* plan, void* device_meta,
+                                      size_t device_meta_bytes, void* stream);
 
 void halo_plan_destroy(halo_plan_t* plan);
 

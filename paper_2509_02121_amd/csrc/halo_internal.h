@@ -99,7 +99,9 @@ struct Row {
   int32_t slot;        // partial slot, or -1 when the row is final here
 };
 
-// Offsets (bytes) of the arrays packed in the device metadata buffer.
+// Offsets (bytes) of the arrays packed in the device metadata buffer, in
+// this order. halo_plan_update_lengths rewrites only arrays from seg_len up
+// to (not including) rows, which halo_plan_upload_update relies on.
 struct MetaLayout {
   size_t seg_page_off = 0;   // int32 [S]  first page slot of each segment
   size_t seg_len = 0;        // int32 [S]

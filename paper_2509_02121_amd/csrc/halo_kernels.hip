@@ -1319,6 +1319,14 @@ halo_status_t run_attention(const halo_plan_t* plan, bool want_prefill, const vo
 
 }  // namespace
 
+namespace {
+halo_status_t upload_bytes(void* dst, const void* src, size_t n, hipStream_t stream) {
+  hipError_t e = hipMemcpyAsync(dst, src, n, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return fail(HALO_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+  return HALO_OK;
+}
+}  // namespace
+
 extern "C" halo_status_t halo_plan_upload(const halo_plan_t* plan, void* device_meta,
                                           size_t device_meta_bytes, void* stream) {
   clear_error();
@@ -1327,10 +1335,22 @@ extern "C" halo_status_t halo_plan_upload(const halo_plan_t* plan, void* device_
     return fail(HALO_ERR_INVALID_ARGUMENT, "device_meta needs " + std::to_string(plan->layout.total) + " bytes");
   if ((reinterpret_cast<uintptr_t>(device_meta) & 255) != 0)
     return fail(HALO_ERR_INVALID_ARGUMENT, "device_meta must be 256-byte aligned");
-  hipError_t e = hipMemcpyAsync(device_meta, plan->meta.data(), plan->layout.total, hipMemcpyHostToDevice,
-                                static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(HALO_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
-  return HALO_OK;
+  return upload_bytes(device_meta, plan->meta.data(), plan->layout.total, static_cast<hipStream_t>(stream));
+}
+
+extern "C" halo_status_t halo_plan_upload_update(const halo_plan_t* plan, void* device_meta,
+                                                 size_t device_meta_bytes, void* stream) {
+  clear_error();
+  if (!plan || !device_meta) return fail(HALO_ERR_INVALID_ARGUMENT, "plan and device_meta must not be NULL");
+  if (device_meta_bytes < plan->layout.total)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "device_meta needs " + std::to_string(plan->layout.total) + " bytes");
+  if ((reinterpret_cast<uintptr_t>(device_meta) & 255) != 0)
+    return fail(HALO_ERR_INVALID_ARGUMENT, "device_meta must be 256-byte aligned");
+  // The sections an in-place update rewrites lie between the segment
+  // length table and the row table, in that order in the image.
+  const size_t at = plan->layout.seg_len, end = plan->layout.rows;
+  return upload_bytes(static_cast<uint8_t*>(device_meta) + at, plan->meta.data() + at, end - at,
+                      static_cast<hipStream_t>(stream));
 }
 
 extern "C" halo_status_t halo_prefix_attn_decode(const halo_plan_t* plan, const void* device_meta,

@@ -68,7 +68,7 @@ class PlanOptions(ctypes.Structure):
 
 EXPORTED_SYMBOLS = (
     "halo_plan_create", "halo_plan_create_with_options", "halo_plan_options_default", "halo_plan_upload",
-    "halo_plan_destroy", "halo_plan_get_stats", "halo_plan_update_lengths",
+    "halo_plan_upload_update", "halo_plan_destroy", "halo_plan_get_stats", "halo_plan_update_lengths",
     "halo_plan_inspect",
     "halo_prefix_attn_decode", "halo_prefix_attn_prefill", "halo_prefix_attn_decode_noalloc",
     "halo_kv_page_gather",
@@ -137,6 +137,8 @@ def load_library(require_gpu=False):
     lib.halo_plan_update_lengths.restype = ctypes.c_int
     lib.halo_plan_upload.argtypes = [vp, vp, sz, vp]
     lib.halo_plan_upload.restype = ctypes.c_int
+    lib.halo_plan_upload_update.argtypes = [vp, vp, sz, vp]
+    lib.halo_plan_upload_update.restype = ctypes.c_int
     lib.halo_plan_destroy.argtypes = [vp]
     lib.halo_plan_destroy.restype = None
     lib.halo_plan_get_stats.argtypes = [vp, ctypes.POINTER(PlanStats)]
@@ -338,6 +340,13 @@ class Plan:
         _check(_LIB.halo_plan_upload(self._handle, device_meta.data_ptr(),
                                      device_meta.numel() * device_meta.element_size(),
                                      _stream_handle(stream)))
+
+    def upload_update(self, device_meta, stream=None):
+        """halo_plan_upload_update: only what update_lengths changes, into a
+        buffer that already holds an upload of this plan."""
+        _check(_LIB.halo_plan_upload_update(self._handle, device_meta.data_ptr(),
+                                            device_meta.numel() * device_meta.element_size(),
+                                            _stream_handle(stream)))
 
     def close(self):
         if self._handle is not None and _LIB is not None:
@@ -667,56 +676,111 @@ class PrefixAttention:
 
     run() enqueues the whole path (attention items, then the merge) on the
     current stream and returns (o, lse).
+
+    The device metadata is double-buffered. update() uploads the next batch
+    step's plan into the buffer the current step does not use, on a copy
+    stream of its own (or the stream given), after every run already
+    enqueued that read that buffer; a run waits for its buffer's upload. The
+    copy of step t + 1's plan therefore overlaps step t's kernels, and after
+    an in-place update it copies only what the update can change.
     """
 
     def __init__(self, params, csr, device="cuda", options=None):
         import torch
         load_library(require_gpu=True)
         self.plan = Plan.from_csr(params, csr, options)
+        self.options = options
         self.device = torch.device(device)
-        self.meta = torch.empty(max(self.plan.device_meta_bytes, 256), dtype=torch.uint8, device=self.device)
+        self._metas = [self._meta_buffer(self.plan.device_meta_bytes), None]
+        self._cur = 0
         self.workspace = (torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=self.device)
                           if self.plan.workspace_bytes else None)
-        upload_stream = torch.cuda.current_stream(self.device)
-        self.plan.upload(self.meta, upload_stream)
-        # runs on another stream wait for this event, so they never read
-        # device_meta before the copy has landed
-        self._uploaded = torch.cuda.Event()
-        self._uploaded.record(upload_stream)
-        self._upload_stream = upload_stream
+        self._copy_stream = torch.cuda.Stream(device=self.device)
+        # runs that read buffer i since its last upload: an event after the
+        # last run() per stream, and the streams of bound callables (whose
+        # calls are not tracked one by one: the upload waits for everything
+        # enqueued on those streams)
+        self._runs = [{}, {}]
+        self._bound = [set(), set()]
+        self._uploaded = [None, None]
+        self._upload_streams = [None, None]
+        # the Plan object whose upload buffer i holds (an in-place update
+        # then needs only halo_plan_upload_update)
+        self._holds = [None, None]
+        self._upload(0, torch.cuda.current_stream(self.device))
         self.out_dtype = {HALO_F32: torch.float32, HALO_BF16: torch.bfloat16}[params.out_dtype]
+
+    @property
+    def meta(self):
+        """The device metadata buffer of the current plan."""
+        return self._metas[self._cur]
+
+    def _meta_buffer(self, nbytes):
+        import torch
+        return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+
+    def _upload(self, i, stream):
+        import torch
+        for u, ev in self._runs[i].items():
+            if u != stream:
+                stream.wait_event(ev)
+        for u in self._bound[i]:
+            if u != stream:
+                stream.wait_stream(u)
+        self._runs[i].clear()
+        self._bound[i].clear()
+        if self._holds[i] is self.plan:
+            self.plan.upload_update(self._metas[i], stream)
+        else:
+            self.plan.upload(self._metas[i], stream)
+            self._holds[i] = self.plan
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        self._uploaded[i] = ev
+        self._upload_streams[i] = stream
 
     def update(self, csr, stream=None):
         """Bring the plan up to date with `csr` (the next decode step's
         forest): the length update when it applies, else a new plan (with
         larger metadata and workspace buffers if needed). Uploads the new
-        metadata on `stream` (None: the current stream); later runs on that
-        stream are ordered after the runs already enqueued there. Returns
-        True if the update applied."""
+        metadata into the other buffer, on `stream` (None: this object's copy
+        stream). Callables from bind() keep the plan they were bound with:
+        bind again after update(). Returns True if the update applied."""
         import torch
-        # the previous upload read the host image asynchronously
-        self._uploaded.synchronize()
+        # the last upload read the host image asynchronously
+        self._uploaded[self._cur].synchronize()
         applied = self.plan.update_lengths(csr)
+        nxt = 1 - self._cur
         if not applied:
-            self.plan = Plan.from_csr(self.plan.params, csr)
-            if self.plan.device_meta_bytes > self.meta.numel():
-                self.meta = torch.empty(self.plan.device_meta_bytes, dtype=torch.uint8, device=self.device)
+            self.plan = Plan.from_csr(self.plan.params, csr, self.options)
             ws_have = self.workspace.numel() if self.workspace is not None else 0
             if self.plan.workspace_bytes > ws_have:
+                # runs in flight may still use the old workspace
+                torch.cuda.synchronize(self.device)
                 self.workspace = torch.empty(self.plan.workspace_bytes, dtype=torch.uint8, device=self.device)
-        upload_stream = stream if stream is not None else torch.cuda.current_stream(self.device)
-        self.plan.upload(self.meta, upload_stream)
-        self._uploaded = torch.cuda.Event()
-        self._uploaded.record(upload_stream)
-        self._upload_stream = upload_stream
+        if self._metas[nxt] is None or self._metas[nxt].numel() < self.plan.device_meta_bytes:
+            torch.cuda.synchronize(self.device)
+            self._metas[nxt] = self._meta_buffer(self.plan.device_meta_bytes)
+            self._holds[nxt] = None
+        self._upload(nxt, stream if stream is not None else self._copy_stream)
+        self._cur = nxt
         return applied
 
-    def _after_upload(self, stream):
-        """Make `stream` (None: the current stream) wait for the metadata upload."""
+    def _before_run(self, stream):
+        """Make `stream` (None: the current stream) wait for the current
+        buffer's upload; returns that stream."""
         import torch
         s = stream if stream is not None else torch.cuda.current_stream(self.device)
-        if s != self._upload_stream:
-            s.wait_event(self._uploaded)
+        if s != self._upload_streams[self._cur]:
+            s.wait_event(self._uploaded[self._cur])
+        return s
+
+    def _after_run(self, s):
+        """Note that the run just enqueued on `s` reads the current buffer."""
+        import torch
+        ev = torch.cuda.Event()
+        ev.record(s)
+        self._runs[self._cur][s] = ev
 
     def alloc_outputs(self, q):
         import torch
@@ -731,7 +795,7 @@ class PrefixAttention:
         fn = _LIB.halo_prefix_attn_prefill if self.plan.is_prefill else _LIB.halo_prefix_attn_decode
         ws = self.workspace
         _check_run(self.plan, self.meta, q, k_pool, v_pool, o, lse, ws)
-        self._after_upload(stream)
+        self._bound[self._cur].add(self._before_run(stream))
         args = (self.plan._handle, self.meta.data_ptr(), q.data_ptr(), k_pool.data_ptr(),
                 v_pool.data_ptr(), o.data_ptr(), lse.data_ptr() if lse is not None else None,
                 ws.data_ptr() if ws is not None else None,
@@ -748,6 +812,7 @@ class PrefixAttention:
             o, lse_new = self.alloc_outputs(q)
             lse = lse if lse is not None else lse_new
         fn = prefix_attn_prefill if self.plan.is_prefill else prefix_attn_decode
-        self._after_upload(stream)
+        s = self._before_run(stream)
         fn(self.plan, self.meta, q, k_pool, v_pool, o, lse, self.workspace, stream)
+        self._after_run(s)
         return o, lse

@@ -355,6 +355,10 @@ def test_run_calls_reject_bad_arguments_without_touching_the_gpu(lib):
     rc = lib.halo_prefix_attn_decode(plan._handle, fake + 8, fake, fake, fake, fake, None, fake,
                                      plan.workspace_bytes, None)
     assert rc == halo.HALO_ERR_INVALID_ARGUMENT     # device_meta not 256-byte aligned
+    for upload in (lib.halo_plan_upload, lib.halo_plan_upload_update):
+        assert upload(plan._handle, None, 1 << 30, None) == halo.HALO_ERR_INVALID_ARGUMENT
+        assert upload(plan._handle, fake, 255, None) == halo.HALO_ERR_INVALID_ARGUMENT      # too small
+        assert upload(plan._handle, fake + 8, 1 << 30, None) == halo.HALO_ERR_INVALID_ARGUMENT  # misaligned
     p2 = halo.AttnParams(4, 2, 96, 16, 3, halo.HALO_F32, halo.HALO_F32, 0.125)
     rc = lib.halo_kv_page_gather(fake, ctypes.byref(p2), 0, fake, fake, fake, fake, 1, fake, None, None)
     assert rc == halo.HALO_ERR_UNSUPPORTED

@@ -24,7 +24,7 @@ def _both(w):
     o2.fill_(float("nan"))
     l2.fill_(float("nan"))
     pa.run(w.q, w.k_pool, w.v_pool, o1, l1)
-    pa._after_upload(None)
+    pa._before_run(None)
     halo.prefix_attn_decode_noalloc(pa.plan, pa.meta, w.q, w.k_pool, w.v_pool, o2, l2)
     torch.cuda.synchronize()
     return o1.cpu(), l1.cpu(), o2.cpu(), l2.cpu(), pa
