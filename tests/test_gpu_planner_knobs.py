@@ -103,3 +103,25 @@ def test_long_private_spans_and_grown_plans(gpu_lib, dtype, d, opts):
     torch.cuda.synchronize()
     assert_parity(w, o.double().cpu().numpy(), lse.double().cpu().numpy(), ro, rl, rows,
                   f"long grown {dtype} {d}")
+
+
+@pytest.mark.parametrize("dtype,opts", [(torch.float32, None), (torch.bfloat16, {"wide": 0})],
+                         ids=["f32", "bf16-narrow"])
+def test_long_prefixes_in_narrow_prefill_items(gpu_lib, dtype, opts):
+    """Prefill chunks over 1500-3000-token cached prefixes in narrow items:
+    a first span of at most 512 keys, later spans of up to 1024, and the
+    causal chunk span after them (oracle parity)."""
+    print(f"case: long prefixes, narrow prefill {dtype} {opts}", flush=True)
+    rng = np.random.default_rng(5151)
+    n_req = 6
+    seg_len = [int(rng.integers(1500, 3000))] + [int(x) for x in rng.integers(1, 100, size=n_req)]
+    paths = [[0, 1 + r] for r in range(n_req)]
+    q_len = seg_len[1:]
+    w = build_workload("longpf", 600, 8, 2, 128, dtype, seg_len, paths, q_len,
+                       value_scale=0.5 if dtype == torch.bfloat16 else 1.0)
+    plan = halo.Plan.from_csr(params_of(w), w.forest_csr(), opts)
+    spans = plan.inspect()["spans"]
+    assert (spans[:, 2] - spans[:, 1]).max() > 512, "later spans longer than a first span"
+    o, lse = _run(w, opts)
+    ro, rl, rows = oracle_for(w)
+    assert_parity(w, o, lse, ro, rl, rows, f"long prefix prefill {dtype}")
