@@ -529,6 +529,12 @@ def main():
     torch.cuda.set_device(dev)
     head = measure_workload(args.workload, args, dev, pool_fill=args.pool_fill,
                             with_cpu=not args.no_cpu_baseline, percentiles=True)
+    decode_loop = None
+    if not args.no_secondary and not args.pool_fill and not w_is_prefill(args.workload):
+        # the same batch as a decode loop (a token per request and step, the
+        # plan updated in place and uploaded beside the running kernels)
+        decode_loop = decode_loop_measure(args.workload, 100, 10)
+        torch.cuda.empty_cache()
     secondary = {}
     if not args.no_secondary and not args.pool_fill:
         for name in SECONDARY_WORKLOADS:
@@ -565,6 +571,8 @@ def main():
                                                    "effective_hbm_gbps", "config", "host_plan", "roofline")}
                              for k, v in secondary.items()}
     del w
+    if decode_loop is not None:
+        line["decode_loop"] = decode_loop
     print(json.dumps(line), flush=True)
 
 
@@ -621,6 +629,14 @@ def _plan_timing(halo, params, csr, device_meta, stream, repeats=7):
     return res
 
 
+def w_is_prefill(name):
+    """Whether the named workload is a prefill batch."""
+    import numpy as np
+    from workloads import synth
+    index = synth.CONFIG_NAMES.index(name)
+    return synth._forest(index, np.random.Generator(np.random.PCG64(1000 + index)))[2] is not None
+
+
 def _decode_loop_pages(name, n_steps):
     """Spare pages a decode loop of n_steps steps needs: every private
     segment opens a page every 16 steps."""
@@ -633,7 +649,18 @@ def _decode_loop_pages(name, n_steps):
 
 
 def decode_loop_bench(args):
-    """A decode loop (one JSON line): each step every request appends one
+    """`--decode-loop`: decode_loop_measure on --workload, one JSON line."""
+    import sys as _sys
+    d = decode_loop_measure(args.workload, args.steps, args.warmup)
+    if d is None:
+        _sys.exit(2)
+    print(json.dumps({"metric": "decode loop: time per step (plan update + metadata upload + attention call)",
+                      "value": d.pop("ms_per_step"), "unit": "ms/step", "higher_is_better": False, "n_gpus": 1,
+                      "steps": args.steps, "warmup": args.warmup, **d}), flush=True)
+
+
+def decode_loop_measure(workload, steps, warmup):
+    """A decode loop: each step every request appends one
     token to its private suffix (a spare page of the pool when its last page
     is full), the plan follows (halo_plan_update_lengths, a new plan when
     that refuses), its metadata is uploaded into the buffer the running step
@@ -651,12 +678,11 @@ def decode_loop_bench(args):
 
     halo.load_library(require_gpu=True)
     dev = torch.device("cuda", 0)
-    n_steps = args.warmup + args.steps
-    w = make_config(args.workload, device=dev, poison=False,
-                    extra_pages=_decode_loop_pages(args.workload, n_steps))
+    n_steps = warmup + steps
+    w = make_config(workload, device=dev, poison=False, extra_pages=_decode_loop_pages(workload, n_steps))
     if w.is_prefill:
         print("--decode-loop needs a decode workload", file=sys.stderr)
-        sys.exit(2)
+        return None
     params = halo.make_params(w.num_q_heads, w.num_kv_heads, w.head_dim, w.dtype, w.num_pool_pages,
                               w.scale, w.dtype)
     csr0 = w.forest_csr()
@@ -674,7 +700,7 @@ def decode_loop_bench(args):
         k = int(opens.sum())
         if nf + k > len(free):
             print("--decode-loop: the pool has too few spare pages for that many steps", file=sys.stderr)
-            sys.exit(2)
+            return None
         ids = np.insert(ids, ip[1:][opens], free[nf:nf + k])
         nf += k
         ip = np.concatenate([[0], np.cumsum(np.diff(ip) + opens)])
@@ -693,7 +719,7 @@ def decode_loop_bench(args):
         runner.run(w.q, w.k_pool, w.v_pool, o, lse)
         return ok
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     host_ms.clear()
@@ -701,29 +727,27 @@ def decode_loop_bench(args):
     e1 = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e0.record(stream)
-    for i in range(args.warmup, n_steps):
+    for i in range(warmup, n_steps):
         applied += int(step(i))
     e1.record(stream)
     torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) * 1e3 / args.steps
-    gpu = e0.elapsed_time(e1) / args.steps
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    gpu = e0.elapsed_time(e1) / steps
     host_ms.sort()
     # the batch grows by a token per request and step: the attention call
     # alone on the timed region's first and last forest, for reference
     ref = []
-    for f in (forests[args.warmup], forests[-1]):
+    for f in (forests[warmup], forests[-1]):
         pa = halo.PrefixAttention(params, f, dev)
         ref.append(_time_launches(pa.bind(w.q, w.k_pool, w.v_pool, o, lse, stream), 20, 5, stream) / 1e3)
         del pa
-    print(json.dumps({
-        "metric": "decode loop: time per step (plan update + metadata upload + attention call)",
-        "value": round(wall, 5), "unit": "ms/step", "higher_is_better": False, "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "gpu_ms_per_step": round(gpu, 5),
-        "host_update_ms_median": round(host_ms[len(host_ms) // 2], 4),
-        "attention_only_ms_first_last": [round(x, 5) for x in ref],
-        "overhead_vs_attention_only": round(gpu / (0.5 * (ref[0] + ref[1])) - 1, 4),
-        "steps_updated_in_place": applied, "pages_opened": int(nf), "dtype": "bf16" if w.dtype.itemsize == 2 else "f32",
-        "data": "synthetic", "config": {"workload": w.name, "requests": len(w.req_paths)}}), flush=True)
+    return {"ms_per_step": round(wall, 5), "gpu_ms_per_step": round(gpu, 5),
+            "host_update_ms_median": round(host_ms[len(host_ms) // 2], 4),
+            "attention_only_ms_first_last": [round(x, 5) for x in ref],
+            "overhead_vs_attention_only": round(gpu / (0.5 * (ref[0] + ref[1])) - 1, 4),
+            "steps_updated_in_place": applied, "pages_opened": int(nf),
+            "dtype": "bf16" if w.dtype.itemsize == 2 else "f32", "data": "synthetic",
+            "config": {"workload": w.name, "requests": len(w.req_paths), "steps": steps}}
 
 
 def measure_workload(name, args, dev, pool_fill=0.0, with_cpu=False, percentiles=False):
