@@ -463,6 +463,8 @@ def main():
     ap.add_argument("--gather", action="store_true",
                     help="only time the page gather of the workload's whole working set (every "
                          "segment, K and V pools) into dense token-major buffers")
+    ap.add_argument("--no-decode-loop", action="store_true",
+                    help="leave the decode-loop measurement out of the default line")
     ap.add_argument("--decode-loop", action="store_true",
                     help="only time a decode loop: per step one token more per request, the plan "
                          "update and upload, and the attention call (wall clock and GPU time)")
@@ -529,12 +531,6 @@ def main():
     torch.cuda.set_device(dev)
     head = measure_workload(args.workload, args, dev, pool_fill=args.pool_fill,
                             with_cpu=not args.no_cpu_baseline, percentiles=True)
-    decode_loop = None
-    if not args.no_secondary and not args.pool_fill and not w_is_prefill(args.workload):
-        # the same batch as a decode loop (a token per request and step, the
-        # plan updated in place and uploaded beside the running kernels)
-        decode_loop = decode_loop_measure(args.workload, 100, 10)
-        torch.cuda.empty_cache()
     secondary = {}
     if not args.no_secondary and not args.pool_fill:
         for name in SECONDARY_WORKLOADS:
@@ -571,8 +567,13 @@ def main():
                                                    "effective_hbm_gbps", "config", "host_plan", "roofline")}
                              for k, v in secondary.items()}
     del w
-    if decode_loop is not None:
-        line["decode_loop"] = decode_loop
+    if not (args.no_secondary or args.no_decode_loop or args.pool_fill or w_is_prefill(args.workload)):
+        # the same batch as a decode loop (a token per request and step, the
+        # plan updated in place and uploaded beside the running kernels);
+        # last, since its copy stream slows the small secondary calls after it
+        secondary.clear()
+        torch.cuda.empty_cache()
+        line["decode_loop"] = decode_loop_measure(args.workload, 100, 10)
     print(json.dumps(line), flush=True)
 
 
