@@ -1,7 +1,9 @@
 """The C ABI from a C++ program with no Python and no torch (GPU): the
 driver in tests/abi_driver reads a seeded batch from a file, runs
 halo_plan_create, halo_plan_upload and halo_prefix_attn_decode with the HIP
-runtime alone, and writes O and LSE back; they match the oracle."""
+runtime alone, and writes O and LSE back; they match the oracle. In its
+loop mode it decodes the batch's last steps, the plan brought up to date in
+place each step (halo_plan_update_lengths, halo_plan_upload_update)."""
 
 import os
 import subprocess
@@ -53,3 +55,31 @@ def test_decode_through_c_driver(gpu_lib, tmp_path, index, out_dtype):
     lse = lse.reshape(w.q.shape[0], w.num_q_heads)
     ro, rl, rr = oracle_for(w)
     assert_parity(w, o, lse, ro, rl, rr, f"C driver config {index}")
+
+
+@pytest.mark.parametrize("index,steps", [(1, 40), (2, 24)])
+def test_decode_loop_through_c_driver(gpu_lib, tmp_path, index, steps):
+    """The driver plans the batch with every private suffix `steps` tokens
+    shorter, then appends a token to each per step (pages reopened from the
+    batch's own page lists), updating the plan in place and uploading only
+    what changed, double-buffered on a copy stream; the last step is the
+    batch itself and matches the oracle."""
+    print(f"case: C driver decode loop config {index} steps {steps}", flush=True)
+    w = make_config(index)
+    inp, outp = tmp_path / "in.bin", tmp_path / "out.bin"
+    _write_input(inp, w, torch.bfloat16)
+    r = subprocess.run([DRIVER, str(inp), str(outp), str(steps)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    print(r.stdout.strip(), flush=True)
+    line = next(x for x in r.stdout.splitlines() if x.startswith("loop "))
+    fields = line.split()
+    assert int(fields[fields.index("in_place") + 1]) == steps, line
+    rows = w.q.shape[0] * w.num_q_heads
+    raw = np.fromfile(outp, np.uint8)
+    o_bytes = rows * w.head_dim * 2
+    o = torch.from_numpy(raw[:o_bytes].copy()).view(torch.bfloat16).float().numpy().astype(np.float64)
+    lse = np.frombuffer(raw[o_bytes:].tobytes(), np.float32).astype(np.float64)
+    o = o.reshape(w.q.shape[0], w.num_q_heads, w.head_dim)
+    lse = lse.reshape(w.q.shape[0], w.num_q_heads)
+    ro, rl, rr = oracle_for(w)
+    assert_parity(w, o, lse, ro, rl, rr, f"C driver loop config {index}")
