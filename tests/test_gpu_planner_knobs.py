@@ -125,3 +125,44 @@ def test_long_prefixes_in_narrow_prefill_items(gpu_lib, dtype, opts):
     o, lse = _run(w, opts)
     ro, rl, rows = oracle_for(w)
     assert_parity(w, o, lse, ro, rl, rows, f"long prefix prefill {dtype}")
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_long_forests_with_random_options_fresh_and_grown(gpu_lib, seed):
+    """Random decode forests with suffixes up to 3000 tokens and random
+    options (growth reserve, private and shared chunk lengths, wide items):
+    a fresh plan, and a plan made for private segments up to the reserve
+    shorter (fewer pages) and then updated in place to the full forest, both
+    against the oracle."""
+    rng = np.random.default_rng(7000 + seed)
+    dtype = torch.bfloat16 if seed % 3 else torch.float32
+    d = 128 if seed % 4 else 64
+    seg_len, paths, _ = random_forest(rng, int(rng.integers(2, 24)), max_len=int(rng.choice([600, 1500, 3000])))
+    opts = {"append_reserve": int(rng.integers(1, 257))}
+    if rng.random() < 0.5:
+        opts["kc_private"] = int(rng.integers(1, 100)) * 32
+    if rng.random() < 0.3:
+        opts["kc_shared"] = int(rng.integers(1, 32)) * 32
+    if dtype == torch.bfloat16 and rng.random() < 0.3:
+        opts["wide"] = 1
+    print(f"case: random long forest {seed} {dtype} d={d} {opts}", flush=True)
+    w = build_workload("sweep", 9000 + seed, 8, 2, d, dtype, seg_len, paths, None,
+                       value_scale=0.5 if dtype == torch.bfloat16 else 1.0)
+    o, lse = _run(w, opts)
+    ro, rl, rows = oracle_for(w)
+    assert_parity(w, o, lse, ro, rl, rows, f"random long fresh {seed}")
+    full = w.forest_csr()
+    refs = np.bincount(full["req_seg_ids"], minlength=len(seg_len))
+    cut = np.where((refs == 1) & (np.asarray(seg_len) > 1),
+                   rng.integers(0, opts["append_reserve"] + 1, size=len(seg_len)), 0)
+    short_len = np.maximum(np.asarray(full["seg_len"], np.int64) - cut, np.minimum(1, np.asarray(full["seg_len"])))
+    pages = [list(p[:(int(n) + 15) // 16]) for p, n in zip(w.seg_pages, short_len)]
+    short = dict(full, seg_len=short_len.astype(np.int32),
+                 seg_page_indptr=np.concatenate([[0], np.cumsum([len(p) for p in pages])]).astype(np.int32),
+                 seg_page_ids=np.concatenate([np.asarray(p, np.int32) for p in pages] + [np.zeros(0, np.int32)]))
+    pa = halo.PrefixAttention(params_of(w), short, "cuda", opts)
+    assert pa.update(full), "growth within the reserve updates in place"
+    o, lse = pa.run(w.q, w.k_pool, w.v_pool)
+    torch.cuda.synchronize()
+    assert_parity(w, o.double().cpu().numpy(), lse.double().cpu().numpy(), ro, rl, rows,
+                  f"random long grown {seed}")
